@@ -1,0 +1,163 @@
+"""Plain, slow, fp64 reference of the group-masked linear layer of GroupMask.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path may import or call this
+module: only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` do.  It shares no code with the HIP library.
+
+Every function is the paper's definition written out in NumPy float64; bf16 and
+fp32 inputs widen to fp64 exactly, so the only rounding here is fp64's.
+
+Readings taken where the paper is silent (each is listed with its reason in the
+design notes of the repository):
+
+* Gumbel-Sigmoid (Sec. 2.2 cites the relaxation without printing it): the
+  binary-concrete form y = sigmoid((logit + ln u - ln(1-u)) / tau) with one
+  uniform variate u per group.  ln u - ln(1-u) is a logistic variate, i.e. the
+  difference of two independent Gumbel variates, so P(z > 0) = sigmoid(logit).
+  This choice of noise form is pinned only by the statistical property above,
+  not by any number printed in the paper ("parity unpinned" for the exact form).
+* Hard decision: keep iff y > 1/2, i.e. iff z = logit + noise > 0; z == 0 prunes.
+* STE (Sec. 2.2): the forward uses the binary selector; the backward uses the
+  derivative of the relaxation, d y / d logit = y (1 - y) / tau.
+* Evaluation mode (Sec. 2.2, Appendix F): no noise; keep iff logit > 0.
+* Soft selectors: a fractional mask value scales its group; only exact zeros
+  prune.  The paper's forward is binary; this generalisation keeps the soft
+  output usable.
+* Groups are 1 x g blocks of consecutive input columns of one output row
+  (Sec. 2.1 with g_out = 1, g_in = g).  ``expand_mask`` also takes g_out > 1.
+* dgate is produced for every group, pruned or kept, because the STE passes a
+  gradient to every selector; it does not depend on the mask values.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+__all__ = [
+    "from_bf16", "logistic_noise", "gate", "gate_bwd", "expand_mask", "masked_weight",
+    "linear_fwd", "linear_bwd_dx", "linear_bwd_dgate", "linear_bwd", "sparsity",
+    "preserved_rate", "near_threshold", "kept_count",
+]
+
+
+def from_bf16(bits) -> np.ndarray:
+    """bf16 bit patterns (uint16) to float64: the 16 bits are the top half of an IEEE fp32."""
+    b = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+    return b.view(np.float32).astype(np.float64)
+
+
+# ---------------------------------------------------------------- gate (Sec. 2.2)
+
+def logistic_noise(u) -> np.ndarray:
+    """Noise term of the Gumbel-Sigmoid relaxation: ln u - ln(1 - u), for u in (0, 1)."""
+    u = np.asarray(u, dtype=np.float64)
+    return np.log(u) - np.log1p(-u)
+
+
+def gate(logits, noise, tau: float, hard: bool):
+    """Gumbel-Sigmoid gate with straight-through forward (Sec. 2.2; Appendix F for eval).
+
+    z = logit + (ln u - ln(1-u)), or z = logit when ``noise`` is None (evaluation);
+    y = sigmoid(z / tau).  Returns (mask, y): mask = [y > 1/2] when ``hard``,
+    else mask = y.
+    """
+    z = np.asarray(logits, dtype=np.float64)
+    if noise is not None:
+        z = z + logistic_noise(noise)
+    y = 1.0 / (1.0 + np.exp(-z / float(tau)))
+    if hard:
+        # sigmoid is strictly increasing with sigmoid(0) = 1/2, so y > 1/2 holds exactly
+        # when z > 0; testing z keeps the decision exact where fp64 rounds y to 1/2.
+        mask = (z > 0.0).astype(np.float64)
+    else:
+        mask = y.copy()
+    return mask, y
+
+
+def gate_bwd(dmask, y, tau: float) -> np.ndarray:
+    """Straight-through backward (Sec. 2.2): d logit = d mask * y (1 - y) / tau."""
+    y = np.asarray(y, dtype=np.float64)
+    return np.asarray(dmask, dtype=np.float64) * y * (1.0 - y) / float(tau)
+
+
+def near_threshold(y, band: float = 1e-6) -> np.ndarray:
+    """Gates whose relaxed value lies within ``band`` of the 1/2 threshold."""
+    return np.abs(np.asarray(y, dtype=np.float64) - 0.5) <= band
+
+
+# ------------------------------------------------------- mask and weight (Eq. 1)
+
+def expand_mask(B, g_in: int, g_out: int = 1) -> np.ndarray:
+    """Full-resolution mask M = B (Kronecker) 1_{g_out x g_in} (Eq. 1)."""
+    B = np.asarray(B, dtype=np.float64)
+    return np.kron(B, np.ones((g_out, g_in), dtype=np.float64))
+
+
+def masked_weight(W, B, g_in: int, g_out: int = 1) -> np.ndarray:
+    """Pruned weight W_hat = W (elementwise) M (Eq. 1)."""
+    W = np.asarray(W, dtype=np.float64)
+    M = expand_mask(B, g_in, g_out)
+    if M.shape != W.shape:
+        raise ValueError(f"mask expands to {M.shape}, weight is {W.shape}")
+    return W * M
+
+
+# ------------------------------------------------------------ masked linear layer
+
+def linear_fwd(X, W, B, g: int) -> np.ndarray:
+    """Student forward of one target linear: Y = X W_hat^T (Eq. 1 applied to nn.Linear)."""
+    X = np.asarray(X, dtype=np.float64)
+    return X @ masked_weight(W, B, g).T
+
+
+def linear_bwd_dx(dY, W, B, g: int) -> np.ndarray:
+    """Input gradient through the frozen masked weight: dX = dY W_hat."""
+    return np.asarray(dY, dtype=np.float64) @ masked_weight(W, B, g)
+
+
+def linear_bwd_dgate(dY, X, W, g: int) -> np.ndarray:
+    """Selector gradient: dgate[o, v] = sum over the group's entries of W * (dY^T X).
+
+    Y is linear in each selector, so d<dY, Y>/dB[o, v] = sum_{i in group v} W[o, i] (dY^T X)[o, i];
+    the weight itself gets no gradient (frozen, Sec. 2.4).
+    """
+    dY = np.asarray(dY, dtype=np.float64)
+    X = np.asarray(X, dtype=np.float64)
+    W = np.asarray(W, dtype=np.float64)
+    d_out, d_in = W.shape
+    if d_in % g:
+        raise ValueError("d_in must be a multiple of g")
+    G = dY.T @ X
+    return (W * G).reshape(d_out, d_in // g, g).sum(axis=2)
+
+
+def linear_bwd(dY, X, W, B, g: int):
+    """(dX, dgate) of one masked linear."""
+    return linear_bwd_dx(dY, W, B, g), linear_bwd_dgate(dY, X, W, g)
+
+
+# ------------------------------------------------------ sparsity ratios (Eq. 2)
+
+def kept_count(B) -> int:
+    """Number of retained groups of a selector matrix."""
+    return int(np.count_nonzero(np.asarray(B)))
+
+
+def sparsity(selectors, shapes):
+    """Layer-wise and overall sparsity (Eq. 2).
+
+    selectors: list of B^l arrays; shapes: list of (d_out, d_in).
+    s^l = 1 - sum(B^l) / (G_out G_in); s = sum_l s^l d_out d_in / sum_l d_out d_in.
+    """
+    s_layer = []
+    for B in selectors:
+        B = np.asarray(B)
+        s_layer.append(1.0 - np.count_nonzero(B) / float(B.size))
+    sizes = np.array([float(do) * float(di) for do, di in shapes])
+    s = float(np.sum(np.array(s_layer) * sizes) / np.sum(sizes))
+    return s_layer, s
+
+
+def preserved_rate(B, g_in: int, g_out: int = 1) -> float:
+    """Active weights / total weights after applying the binary mask (Appendix F)."""
+    M = expand_mask((np.asarray(B) != 0).astype(np.float64), g_in, g_out)
+    return float(M.sum() / M.size)

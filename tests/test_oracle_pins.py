@@ -1,0 +1,417 @@
+"""Pins of the fp64 oracle against what the paper and the mathematics fix.
+
+None of these re-types an oracle formula: each compares the oracle with an
+independent route (brute-force loops, a closed form, an identity that holds only
+for the correct operator, a library routine on a special case, the paper's own
+printed numbers).  The mutation test at the end plants plausible mistakes in
+copies of the oracle functions and checks that at least one pin catches each.
+"""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import scipy.special
+
+import oracle
+import workloads
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _rand(shape, key, scale=1.0):
+    return workloads.gen.rng_for(900, *key).standard_normal(shape) * scale
+
+
+def _soft_mask(shape, key, p_zero=0.4):
+    r = workloads.gen.rng_for(901, *key)
+    m = r.uniform(0.05, 1.5, size=shape)
+    m[r.uniform(size=shape) < p_zero] = 0.0
+    return m
+
+
+# ----------------------------------------------------------- brute force (loops)
+
+def _brute_fwd(X, W, B, g):
+    T, d_in = X.shape
+    d_out = W.shape[0]
+    Y = [[0.0] * d_out for _ in range(T)]
+    for t in range(T):
+        for o in range(d_out):
+            acc = 0.0
+            for i in range(d_in):
+                acc += X[t][i] * W[o][i] * B[o][i // g]
+            Y[t][o] = acc
+    return np.array(Y)
+
+
+def _brute_dx(dY, W, B, g):
+    T, d_out = dY.shape
+    d_in = W.shape[1]
+    dX = [[0.0] * d_in for _ in range(T)]
+    for t in range(T):
+        for i in range(d_in):
+            acc = 0.0
+            for o in range(d_out):
+                acc += dY[t][o] * W[o][i] * B[o][i // g]
+            dX[t][i] = acc
+    return np.array(dX)
+
+
+def _brute_dgate(dY, X, W, g):
+    T, d_out = dY.shape
+    d_in = X.shape[1]
+    out = [[0.0] * (d_in // g) for _ in range(d_out)]
+    for o in range(d_out):
+        for v in range(d_in // g):
+            acc = 0.0
+            for i in range(v * g, (v + 1) * g):
+                for t in range(T):
+                    acc += dY[t][o] * X[t][i] * W[o][i]
+            out[o][v] = acc
+    return np.array(out)
+
+
+TINY = [(3, 5, 2, 4), (2, 4, 3, 2), (4, 3, 1, 8), (1, 6, 4, 1)]  # (T, d_out, G_in, g)
+
+
+@pytest.mark.parametrize("T,d_out,G_in,g", TINY)
+def test_fwd_matches_brute_force(T, d_out, G_in, g):
+    d_in = G_in * g
+    X, W = _rand((T, d_in), (1, T)), _rand((d_out, d_in), (2, T))
+    B = _soft_mask((d_out, G_in), (3, T))
+    np.testing.assert_allclose(oracle.linear_fwd(X, W, B, g), _brute_fwd(X, W, B, g), rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("T,d_out,G_in,g", TINY)
+def test_dx_matches_brute_force(T, d_out, G_in, g):
+    d_in = G_in * g
+    dY, W = _rand((T, d_out), (4, T)), _rand((d_out, d_in), (5, T))
+    B = _soft_mask((d_out, G_in), (6, T))
+    np.testing.assert_allclose(oracle.linear_bwd_dx(dY, W, B, g), _brute_dx(dY, W, B, g), rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("T,d_out,G_in,g", TINY)
+def test_dgate_matches_brute_force(T, d_out, G_in, g):
+    d_in = G_in * g
+    dY, X, W = _rand((T, d_out), (7, T)), _rand((T, d_in), (8, T)), _rand((d_out, d_in), (9, T))
+    np.testing.assert_allclose(oracle.linear_bwd_dgate(dY, X, W, g), _brute_dgate(dY, X, W, g), rtol=1e-12, atol=1e-12)
+
+
+# ----------------------------------------------------------- special cases (Eq. 1)
+
+def test_all_ones_mask_is_dense_linear():
+    # Teacher pass: B = 1 gives the dense frozen layer (Sec. 2.4).
+    T, d_out, d_in, g = 7, 12, 32, 8
+    X, W, dY = _rand((T, d_in), (10,)), _rand((d_out, d_in), (11,)), _rand((T, d_out), (12,))
+    ones = np.ones((d_out, d_in // g))
+    np.testing.assert_allclose(oracle.linear_fwd(X, W, ones, g), np.matmul(X, W.T), rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(oracle.linear_bwd_dx(dY, W, ones, g), np.matmul(dY, W), rtol=1e-13, atol=1e-13)
+
+
+def test_all_zeros_mask_gives_exact_zero():
+    T, d_out, d_in, g = 5, 8, 16, 4
+    X, W, dY = _rand((T, d_in), (13,)), _rand((d_out, d_in), (14,)), _rand((T, d_out), (15,))
+    zeros = np.zeros((d_out, d_in // g))
+    assert np.all(oracle.linear_fwd(X, W, zeros, g) == 0.0)
+    assert np.all(oracle.linear_bwd_dx(dY, W, zeros, g) == 0.0)
+
+
+def test_group_spanning_whole_row_is_output_row_pruning():
+    T, d_out, d_in = 6, 10, 24
+    X, W = _rand((T, d_in), (16,)), _rand((d_out, d_in), (17,))
+    keep = (np.arange(d_out) % 3 != 1).astype(float)[:, None]
+    Y = oracle.linear_fwd(X, W, keep, d_in)
+    dense = np.matmul(X, W.T)
+    for o in range(d_out):
+        if keep[o, 0]:
+            np.testing.assert_allclose(Y[:, o], dense[:, o], rtol=1e-13, atol=1e-13)
+        else:
+            assert np.all(Y[:, o] == 0.0)
+
+
+def test_unit_groups_give_textbook_mask_gradient():
+    # g = 1 is an elementwise mask: d<dY, X (W*M)^T>/dM = W * (dY^T X).
+    T, d_out, d_in = 9, 7, 5
+    dY, X, W = _rand((T, d_out), (18,)), _rand((T, d_in), (19,)), _rand((d_out, d_in), (20,))
+    ref = W * np.einsum("to,ti->oi", dY, X)
+    np.testing.assert_allclose(oracle.linear_bwd_dgate(dY, X, W, 1), ref, rtol=1e-12, atol=1e-12)
+
+
+def test_expand_mask_is_kronecker_block_layout():
+    B = np.array([[1.0, 0.0, 2.0], [0.0, 3.0, 0.0]])
+    M = oracle.expand_mask(B, 2, 3)
+    assert M.shape == (6, 6)
+    for r, c in itertools.product(range(6), range(6)):
+        assert M[r, c] == B[r // 3, c // 2]
+
+
+# --------------------------------------------------- identities of the backward
+
+def test_dx_is_the_adjoint_of_the_forward():
+    T, d_out, G_in, g = 6, 9, 3, 4
+    d_in = G_in * g
+    W, B, dY = _rand((d_out, d_in), (21,)), _soft_mask((d_out, G_in), (22,)), _rand((T, d_out), (23,))
+    dX = oracle.linear_bwd_dx(dY, W, B, g)
+    for k in range(3):
+        X = _rand((T, d_in), (24, k))
+        lhs = float(np.sum(dX * X))
+        rhs = float(np.sum(dY * oracle.linear_fwd(X, W, B, g)))
+        assert lhs == pytest.approx(rhs, rel=1e-12, abs=1e-12)
+
+
+@pytest.mark.parametrize("h", [1e-3, 0.5, 3.0])
+def test_dgate_matches_central_finite_differences(h):
+    # <dY, Y(B)> is linear in every selector, so the central difference is exact for any h.
+    T, d_out, G_in, g = 4, 5, 3, 4
+    d_in = G_in * g
+    dY, X, W = _rand((T, d_out), (25,)), _rand((T, d_in), (26,)), _rand((d_out, d_in), (27,))
+    B = _soft_mask((d_out, G_in), (28,))
+    dgate = oracle.linear_bwd_dgate(dY, X, W, g)
+    for o, v in itertools.product(range(d_out), range(G_in)):
+        Bp, Bm = B.copy(), B.copy()
+        Bp[o, v] += h
+        Bm[o, v] -= h
+        fd = (np.sum(dY * oracle.linear_fwd(X, W, Bp, g)) - np.sum(dY * oracle.linear_fwd(X, W, Bm, g))) / (2 * h)
+        assert fd == pytest.approx(dgate[o, v], rel=1e-9, abs=1e-9)
+
+
+def test_dgate_euler_and_row_sum_identities():
+    T, d_out, G_in, g = 8, 6, 4, 8
+    d_in = G_in * g
+    dY, X, W = _rand((T, d_out), (29,)), _rand((T, d_in), (30,)), _rand((d_out, d_in), (31,))
+    B = _soft_mask((d_out, G_in), (32,))
+    dgate = oracle.linear_bwd_dgate(dY, X, W, g)
+    # Euler: Y is homogeneous of degree one in the selectors.
+    assert float(np.sum(B * dgate)) == pytest.approx(float(np.sum(dY * oracle.linear_fwd(X, W, B, g))), rel=1e-12)
+    # Summing a row's groups recovers the dense row's contribution.
+    dense = np.matmul(X, W.T)
+    np.testing.assert_allclose(dgate.sum(axis=1), np.sum(dY * dense, axis=0), rtol=1e-12, atol=1e-12)
+
+
+def test_dgate_two_factorisations_agree():
+    # sum_i W[o,i] (dY^T X)[o,i] over a group == sum_t dY[t,o] (X[t,group] . W[o,group]).
+    T, d_out, G_in, g = 5, 4, 3, 8
+    d_in = G_in * g
+    dY, X, W = _rand((T, d_out), (33,)), _rand((T, d_in), (34,)), _rand((d_out, d_in), (35,))
+    per_token = np.zeros((d_out, G_in))
+    for o in range(d_out):
+        for v in range(G_in):
+            cols = slice(v * g, (v + 1) * g)
+            per_token[o, v] = float(np.dot(dY[:, o], X[:, cols] @ W[o, cols]))
+    np.testing.assert_allclose(oracle.linear_bwd_dgate(dY, X, W, g), per_token, rtol=1e-12, atol=1e-12)
+
+
+# --------------------------------------------------------------- gate (Sec. 2.2)
+
+def test_hard_gate_is_thresholded_sigmoid():
+    r = workloads.gen.rng_for(40)
+    logits = r.standard_normal(4096) * 3
+    u = workloads.draw_uniform_noise(r, 4096).astype(np.float64)
+    for tau in (0.25, 0.4, 0.5, 2.0):
+        m, y = oracle.gate(logits, u, tau, hard=True)
+        y_ref = scipy.special.expit((logits + scipy.special.logit(u)) / tau)
+        np.testing.assert_allclose(y, y_ref, rtol=1e-12, atol=1e-15)
+        assert np.array_equal(m, (y_ref > 0.5).astype(float))
+        ms, ys = oracle.gate(logits, u, tau, hard=False)
+        np.testing.assert_allclose(ms, y_ref, rtol=1e-12, atol=1e-15)
+
+
+def test_hard_gate_does_not_depend_on_temperature():
+    r = workloads.gen.rng_for(41)
+    logits = r.standard_normal(2048)
+    u = workloads.draw_uniform_noise(r, 2048)
+    ref, _ = oracle.gate(logits, u, 1.0, True)
+    for tau in (0.1, 0.4, 0.5, 7.0):
+        assert np.array_equal(oracle.gate(logits, u, tau, True)[0], ref)
+
+
+def test_noise_is_neutral_at_one_half_and_antisymmetric():
+    assert oracle.logistic_noise(0.5) == 0.0
+    u = np.array([2.0 ** -20, 0.125, 0.3125, 0.4375])  # dyadic, so 1 - u is exact
+    np.testing.assert_allclose(oracle.logistic_noise(u), -oracle.logistic_noise(1 - u), rtol=1e-12)
+    _, y1 = oracle.gate([0.7], [0.5], 0.4, False)
+    assert y1[0] == pytest.approx(1 / (1 + math.exp(-0.7 / 0.4)), rel=1e-15)
+
+
+def test_sigmoid_symmetry():
+    z = np.linspace(-8, 8, 97)
+    _, yp = oracle.gate(z, None, 0.5, False)
+    _, ym = oracle.gate(-z, None, 0.5, False)
+    np.testing.assert_allclose(yp + ym, 1.0, rtol=0, atol=1e-15)
+
+
+def test_eval_mode_thresholds_logits():
+    logits = np.array([-2.0, -1e-30, 0.0, 1e-30, 3.0])
+    m, _ = oracle.gate(logits, None, 0.4, True)
+    assert m.tolist() == [0.0, 0.0, 0.0, 1.0, 1.0]
+
+
+def test_keep_probability_is_sigmoid_of_logit():
+    # Binary-concrete property: with u ~ U(0,1), P(logit + ln u - ln(1-u) > 0) = sigmoid(logit).
+    r = workloads.gen.rng_for(42)
+    n = 200_000
+    for logit in (-1.5, 0.0, 0.8):
+        u = workloads.draw_uniform_noise(r, n)
+        m, _ = oracle.gate(np.full(n, logit), u, 0.4, True)
+        p = 1 / (1 + math.exp(-logit))
+        assert abs(m.mean() - p) < 5 * math.sqrt(p * (1 - p) / n)
+
+
+def test_ste_derivative_matches_finite_difference_of_relaxation():
+    r = workloads.gen.rng_for(43)
+    logits = r.standard_normal(64)
+    u = workloads.draw_uniform_noise(r, 64)
+    up = r.standard_normal(64)
+    for tau in (0.4, 0.5):
+        _, y = oracle.gate(logits, u, tau, False)
+        dl = oracle.gate_bwd(up, y, tau)
+        h = 1e-6
+        yp = scipy.special.expit((logits + h + scipy.special.logit(u.astype(float))) / tau)
+        ym = scipy.special.expit((logits - h + scipy.special.logit(u.astype(float))) / tau)
+        np.testing.assert_allclose(dl, up * (yp - ym) / (2 * h), rtol=1e-6, atol=1e-9)
+
+
+def test_near_threshold_band():
+    y = np.array([0.5, 0.5 + 0.9e-6, 0.5 - 2e-6, 0.7])
+    assert oracle.near_threshold(y).tolist() == [True, True, False, False]
+
+
+# ------------------------------------------------- budget and sparsity (Eq. 2)
+
+def test_budgeted_inputs_give_exact_kept_count():
+    case = workloads.make_linear_case((44,), 4, 1024, 1024, 256, 2048, tau=0.5)
+    m, y = oracle.gate(case.logits, case.noise, case.tau, True)
+    assert oracle.kept_count(m) == 2048
+    assert np.array_equal(m, case.mask.astype(float))
+    assert not oracle.near_threshold(y).any()
+
+
+def test_sparsity_closed_forms():
+    shapes = [(4, 8), (2, 8)]
+    B1 = np.ones((4, 2))
+    B2 = np.zeros((2, 2))
+    s_l, s = oracle.sparsity([B1, B2], shapes)
+    assert s_l == [0.0, 1.0]
+    assert s == pytest.approx(16 / 48)
+    B1[0, 0] = 0
+    s_l, s = oracle.sparsity([B1, B2], shapes)
+    assert s_l[0] == pytest.approx(1 / 8)
+    assert s == pytest.approx((32 / 8 + 16) / 48)
+
+
+def test_paper_category_rates_reproduce_global_rate():
+    """Sec. 3.5 prints 36.6 % kept for attention, 56.6 % for MLP and 49.98 % overall."""
+    with open(os.path.join(GOLDEN, "paper_preserved_rates.json")) as f:
+        gold = json.load(f)
+    selectors, shapes = [], []
+    for _layer in range(32):
+        for name, d_out, d_in in workloads.LLAMA2_7B_LINEARS:
+            rate = gold["attention_preserved"] if name in ("q", "k", "v", "o") else gold["mlp_preserved"]
+            G = (d_out * d_in) // 256
+            B = np.zeros(G)
+            B[: int(round(rate * G))] = 1
+            selectors.append(B)
+            shapes.append((d_out, d_in))
+    _, s = oracle.sparsity(selectors, shapes)
+    assert abs((1 - s) - gold["global_preserved"]) <= gold["printed_precision"]
+
+
+def test_preserved_rate_counts_active_weights():
+    B = np.array([[1, 0, 1, 1], [0, 0, 1, 0]])
+    assert oracle.preserved_rate(B, 3) == pytest.approx(4 / 8)
+    with open(os.path.join(GOLDEN, "paper_decision_count.json")) as f:
+        gold = json.load(f)
+    d_out, d_in = 512, 1024
+    B = np.ones((d_out // gold["g_out"], d_in // gold["g_in"]))
+    assert (d_out * d_in) / B.size == gold["reduction_factor"]
+
+
+# ------------------------------------------------------- the pins catch mistakes
+
+def _mutant_fwd_strided_groups(X, W, B, g):
+    # selector v applied to columns v, v + G_in, v + 2 G_in, ... instead of a contiguous block
+    M = np.tile(np.asarray(B, dtype=float), (1, g))
+    return np.asarray(X, float) @ (np.asarray(W, float) * M).T
+
+
+def _mutant_dgate_no_weight(dY, X, W, g):
+    d_out, d_in = np.asarray(W).shape
+    G = np.asarray(dY, float).T @ np.asarray(X, float)
+    return G.reshape(d_out, d_in // g, g).sum(axis=2)
+
+
+def _mutant_dgate_strided_groups(dY, X, W, g):
+    d_out, d_in = np.asarray(W).shape
+    G = np.asarray(dY, float).T @ np.asarray(X, float)
+    return (np.asarray(W, float) * G).reshape(d_out, g, d_in // g).sum(axis=1)
+
+
+def _mutant_dx_unmasked(dY, W, B, g):
+    return np.asarray(dY, float) @ np.asarray(W, float)
+
+
+def _mutant_gate_sign(logits, noise, tau, hard):
+    z = np.asarray(logits, float)
+    if noise is not None:
+        z = z - oracle.logistic_noise(noise)
+    y = 1 / (1 + np.exp(-z / tau))
+    return ((y > 0.5).astype(float) if hard else y), y
+
+
+_ORIG_GATE = oracle.gate
+
+
+def _mutant_gate_ge(logits, noise, tau, hard):
+    m, y = _ORIG_GATE(logits, noise, tau, False)
+    return ((y >= 0.5).astype(float) if hard else y), y
+
+
+def _mutant_ste_no_tau(dmask, y, tau):
+    y = np.asarray(y, float)
+    return np.asarray(dmask, float) * y * (1 - y)
+
+
+def _mutant_sparsity_unweighted(selectors, shapes):
+    s_l = [1.0 - np.count_nonzero(B) / float(np.asarray(B).size) for B in selectors]
+    return s_l, float(np.mean(s_l))
+
+
+MUTANTS = [
+    ("linear_fwd", _mutant_fwd_strided_groups),
+    ("linear_bwd_dgate", _mutant_dgate_no_weight),
+    ("linear_bwd_dgate", _mutant_dgate_strided_groups),
+    ("linear_bwd_dx", _mutant_dx_unmasked),
+    ("gate", _mutant_gate_sign),
+    ("gate", _mutant_gate_ge),
+    ("gate_bwd", _mutant_ste_no_tau),
+    ("sparsity", _mutant_sparsity_unweighted),
+]
+
+PIN_TESTS = [
+    lambda: [test_fwd_matches_brute_force(*c) for c in TINY],
+    lambda: [test_dx_matches_brute_force(*c) for c in TINY],
+    lambda: [test_dgate_matches_brute_force(*c) for c in TINY],
+    test_dx_is_the_adjoint_of_the_forward,
+    lambda: test_dgate_matches_central_finite_differences(0.5),
+    test_dgate_euler_and_row_sum_identities,
+    test_hard_gate_is_thresholded_sigmoid,
+    test_eval_mode_thresholds_logits,
+    test_ste_derivative_matches_finite_difference_of_relaxation,
+    test_paper_category_rates_reproduce_global_rate,
+    test_budgeted_inputs_give_exact_kept_count,
+]
+
+
+@pytest.mark.parametrize("name,mutant", MUTANTS, ids=[m[1].__name__ for m in MUTANTS])
+def test_pins_catch_planted_mistake(monkeypatch, name, mutant):
+    monkeypatch.setattr(oracle, name, mutant)
+    caught = 0
+    for pin in PIN_TESTS:
+        try:
+            pin()
+        except AssertionError:
+            caught += 1
+    assert caught > 0, f"no pin caught the planted mistake in {name}"
