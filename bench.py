@@ -1,0 +1,282 @@
+#!/usr/bin/env python3
+"""Throughput of the group-masked linear layer's mask-learning step on one MI355X.
+
+A step is one pass of the whole hot path over one batch: gate (Gumbel-Sigmoid,
+hard STE forward) -> masked forward -> backward (dX and dgate) -> gate backward.
+The headline workload is a LLaMA-2-7B attention projection: W [4096, 4096],
+X [4096 tokens, 4096], 1x256 groups, half of the 65,536 groups kept at random.
+
+Counted work per step: kept FLOPs 2*T*nnz for the forward and for dX, dense
+FLOPs 2*T*d_out*d_in for dgate (every selector receives a gradient).  Inputs
+are seeded synthetic tensors resident in HBM before timing starts.
+
+The JSON line also carries the roofline of the dominant kernel (dgate), the
+fp64 oracle timed on the host cores as a reported baseline, and the decode
+GEMV bandwidth on LLaMA-2-13B shapes.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def _parse():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="approximate host time spent timing the oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-gemv", action="store_true")
+    ap.add_argument("--gemv-layers", type=int, default=40)
+    ap.add_argument("--profile-copy-mib", type=int, default=0,
+                    help="also run a plain device copy of this size (counter calibration runs)")
+    return ap.parse_args()
+
+
+# ------------------------------------------------------------------ inputs
+
+def _headline_case():
+    import workloads
+    cfg = workloads.config("attn_4096")
+    _, d_out, d_in = cfg["linears"][0]
+    case = workloads.make_linear_case((2, 0, 0), cfg["T"], d_in, d_out, cfg["g"], None, tau=cfg["tau"])
+    return cfg, case
+
+
+def _to_device(case):
+    import torch
+
+    def bf16(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+    def f32(a):
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+
+    return dict(X=bf16(case.X), W=bf16(case.W), dY=bf16(case.dY), logits=f32(case.logits), noise=f32(case.noise))
+
+
+# ------------------------------------------------------------------ the step
+
+class Step:
+    """Buffers and the sequence of library calls of one mask-learning step."""
+
+    def __init__(self, d, g, tau):
+        import torch
+        import paper_2609_33977_amd as gm
+        self.gm, self.d, self.g, self.tau = gm, d, g, tau
+        T, d_in = d["X"].shape
+        d_out = d["W"].shape[0]
+        G_in = d_in // g
+        dev = "cuda"
+        self.mask = torch.empty(d_out, G_in, dtype=torch.float32, device=dev)
+        self.soft = torch.empty(d_out, G_in, dtype=torch.float32, device=dev)
+        self.Y = torch.empty(T, d_out, dtype=torch.bfloat16, device=dev)
+        self.dX = torch.empty(T, d_in, dtype=torch.bfloat16, device=dev)
+        self.dgate = torch.empty(d_out, G_in, dtype=torch.float32, device=dev)
+        self.dlogits = torch.empty(d_out, G_in, dtype=torch.float32, device=dev)
+        self.ws = torch.empty(max(gm.gm_workspace_size(gm.GM_OP_BWD, T, d_in, d_out, g), 16), dtype=torch.uint8,
+                              device=dev)
+        self.fws = torch.empty(max(gm.gm_workspace_size(gm.GM_OP_FWD, T, d_in, d_out, g), 16), dtype=torch.uint8,
+                               device=dev)
+
+    def gate(self):
+        self.gm.gm_gate(self.d["logits"], self.d["noise"], self.tau, True, self.mask, self.soft)
+
+    def fwd(self):
+        self.gm.gm_masked_linear_fwd(self.d["X"], self.d["W"], self.mask, self.g, self.Y, self.fws)
+
+    def bwd(self):
+        self.gm.gm_masked_linear_bwd(self.d["dY"], self.d["X"], self.d["W"], self.mask, self.g, self.dX, self.dgate,
+                                     self.ws)
+
+    def gate_bwd(self):
+        self.gm.gm_gate_bwd(self.dgate, self.soft, self.tau, self.dlogits)
+
+    def dgate_only(self):
+        self.gm.gm_masked_linear_bwd(self.d["dY"], self.d["X"], self.d["W"], self.mask, self.g, None, self.dgate,
+                                     self.ws)
+
+    def __call__(self):
+        self.gate()
+        self.fwd()
+        self.bwd()
+        self.gate_bwd()
+
+
+def _events_ms(fn, n):
+    """Average duration of fn() on the current stream, from HIP events around each call."""
+    import torch
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+    for i in range(n):
+        starts[i].record()
+        fn()
+        ends[i].record()
+    torch.cuda.synchronize()
+    return float(np.mean([s.elapsed_time(e) for s, e in zip(starts, ends)]))
+
+
+# ------------------------------------------------------------------ CPU baseline
+
+def _cpu_baseline(case, flops_per_step, budget_s):
+    """The fp64 oracle, as it stands, timed on this host over whole steps of the workload."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([int(i.get("num_threads", 1)) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    X, W, dY = oracle.from_bf16(case.X), oracle.from_bf16(case.W), oracle.from_bf16(case.dY)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        m, y = oracle.gate(case.logits, case.noise, case.tau, True)
+        oracle.linear_fwd(X, W, m, case.g)
+        _, dgate = oracle.linear_bwd(dY, X, W, m, case.g)
+        oracle.gate_bwd(dgate, y, case.tau)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or el / reps * (reps + 1) > 2.5 * budget_s:
+            break
+    sec = el / reps
+    return {"value": flops_per_step / sec / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"{reps} whole step(s) of the headline workload (gate, fwd, dX, dgate, STE) in fp64 NumPy, "
+                      f"{sec:.2f} s per step"}
+
+
+# ------------------------------------------------------------------ decode GEMV
+
+def _gemv_bandwidth(n_layers, reps):
+    """Decode forward (T=1) over the seven LLaMA-2-13B linears of n_layers distinct layers at 50 % sparsity."""
+    import torch
+    import paper_2609_33977_amd as gm
+    import workloads
+    cfg = workloads.config("llama2_13b_infer")
+    g = cfg["g"]
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(workloads.SEED)
+    mats, kept_bytes, other_bytes = [], 0, 0
+    for _ in range(n_layers):
+        for _, d_out, d_in in cfg["linears"]:
+            W = (torch.randn(d_out, d_in, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
+            G = d_out * (d_in // g)
+            m = torch.zeros(G, device="cuda")
+            m[torch.randperm(G, device="cuda", generator=gen)[: G // 2]] = 1.0
+            X = torch.randn(1, d_in, device="cuda", generator=gen).to(torch.bfloat16)
+            Y = torch.empty(1, d_out, dtype=torch.bfloat16, device="cuda")
+            mats.append((X, W, m.view(d_out, d_in // g), Y))
+            kept_bytes += (G // 2) * g * 2
+            other_bytes += G * 4 + 2 * d_in + 2 * d_out
+    torch.cuda.synchronize()
+
+    def one_pass():
+        for X, W, m, Y in mats:
+            gm.gm_masked_linear_fwd(X, W, m, g, Y)
+
+    one_pass()
+    torch.cuda.synchronize()
+    ms = _events_ms(one_pass, reps)
+    total = kept_bytes + other_bytes
+    return {"workload": f"LLaMA-2-13B decode T=1, 7 linears x {n_layers} distinct layers, 1x{g} groups, 50% kept",
+            "GB/s": total / (ms / 1e3) / 1e9, "frac_of_peak": total / (ms / 1e3) / 1e9 / PEAK_HBM_GBS,
+            "bytes_per_pass": total, "ms_per_pass": ms, "launches_per_pass": len(mats)}
+
+
+# ------------------------------------------------------------------ main
+
+def main():
+    args = _parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU; --gpus {args.gpus} is not supported (this build has no multi-GPU path).",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    import paper_2609_33977_amd  # noqa: F401  (fails loudly when the HIP library is missing)
+
+    cfg, case = _headline_case()
+    T, d_in, d_out, g = case.T, case.d_in, case.d_out, case.g
+    kept = case.kept
+    nnz = kept * g
+    flops = {"fwd": 2.0 * T * nnz, "dx": 2.0 * T * nnz, "dgate": 2.0 * T * d_out * d_in}
+    flops_step = sum(flops.values())
+
+    d = _to_device(case)
+    step = Step(d, g, case.tau)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    if int(step.mask.sum().item()) != kept:
+        raise RuntimeError("gate kept count differs from the budget")
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    tflops = flops_step / (ms_per_step / 1e3) / 1e12
+
+    # Per-call breakdown and the dominant kernel's launch duration (HIP events on the launch stream).
+    reps = max(args.steps, 5)
+    breakdown = {name: _events_ms(getattr(step, name), reps) for name in ("gate", "fwd", "bwd", "gate_bwd")}
+    dgate_ms = _events_ms(step.dgate_only, reps)
+    dgate_tflops = flops["dgate"] / (dgate_ms / 1e3) / 1e12
+    fwd_tflops = flops["fwd"] / (breakdown["fwd"] / 1e3) / 1e12
+
+    if args.profile_copy_mib:
+        src = torch.empty(args.profile_copy_mib << 20, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+
+    gemv = None
+    if not args.no_gemv:
+        gemv = _gemv_bandwidth(args.gemv_layers, max(3, args.steps // 4))
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = _cpu_baseline(case, flops_step, args.cpu_seconds)
+
+    out = {
+        "metric": "masked-linear fwd+bwd TFLOP/s & % bf16 MFMA peak; sparse GEMV GB/s",
+        "value": tflops,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "LLaMA-2-7B attention projection: W 4096x4096, X 4096 tokens (2 x 2048), "
+                               "1x256 groups, 50% of 65,536 groups kept at random; gate + fwd + dX + dgate + STE",
+                   "T": T, "d_in": d_in, "d_out": d_out, "g": g, "kept_groups": kept, "tau": case.tau},
+        "frac_of_bf16_peak": tflops / PEAK_BF16_TFLOPS,
+        "roofline": {"bound": "mfma", "achieved": dgate_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": dgate_tflops / PEAK_BF16_TFLOPS, "traffic": None},
+        "kernels": {"dominant": "dgate_kernel<256> (dY^T X tile + fused W-weighted group reduction)",
+                    "dgate_flops_per_launch": flops["dgate"], "dgate_avg_launch_ms": dgate_ms,
+                    "fwd_kept_tflops": fwd_tflops, "breakdown_ms": breakdown},
+        "cpu_baseline": cpu,
+        "gemv": gemv,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

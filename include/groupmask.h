@@ -1,0 +1,175 @@
+/*
+ * groupmask.h -- C ABI of the group-masked linear layer of GroupMask
+ * (layer-adaptive group-wise sparsity with frozen weights, Sec. 2).
+ *
+ * One target linear layer holds a frozen weight W [d_out, d_in].  Its input
+ * dimension is cut into G_in = d_in / g groups of g consecutive columns, so
+ * every output row o owns the groups (o, v), v = 0 .. G_in-1, each covering
+ * W[o, v*g : (v+1)*g] (Sec. 2.1 with a 1 x g group shape; Eq. 1 expands the
+ * selector matrix B [d_out, G_in] to the full-resolution mask by a Kronecker
+ * product with a 1 x g block of ones).
+ *
+ * Conventions shared by every call:
+ *   - bf16 tensors are passed as uint16_t bit patterns; fp32 as float.
+ *   - All tensors are dense, row-major, contiguous, in the nn.Linear
+ *     convention: X [T, d_in], W [d_out, d_in], Y / dY [T, d_out],
+ *     mask / dgate [d_out, G_in].
+ *   - Every pointer argument is a DEVICE pointer unless stated otherwise, and
+ *     must be 16-byte aligned.  The caller owns every buffer; the library never
+ *     allocates or frees device memory.  Scratch space is passed in as a
+ *     caller-owned workspace sized by gm_workspace_size().
+ *   - Every call validates its arguments before launching anything and returns
+ *     a gm_status; nothing aborts and no exception crosses the ABI.  On an
+ *     error return no kernel has been launched and no output was touched.
+ *   - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL is the
+ *     null stream).  No call synchronises the host.  Calls that share a
+ *     workspace must be ordered on one stream.
+ *   - Only gfx950 (MI355X) devices are supported; any other device returns
+ *     GM_ERR_DEVICE.
+ */
+#ifndef GROUPMASK_H
+#define GROUPMASK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GM_ABI_VERSION 1
+
+/* Same object as a hipStream_t, declared here so that callers need no HIP headers. */
+typedef struct ihipStream_t* gm_stream_t;
+
+typedef enum gm_status {
+  GM_OK = 0,
+  GM_ERR_NULL = 1,      /* a required pointer is NULL */
+  GM_ERR_SHAPE = 2,     /* a size is out of range or inconsistent */
+  GM_ERR_VALUE = 3,     /* a scalar argument is out of range (tau, hard) */
+  GM_ERR_ALIGN = 4,     /* a pointer is not 16-byte aligned */
+  GM_ERR_WORKSPACE = 5, /* workspace missing or smaller than gm_workspace_size() */
+  GM_ERR_DEVICE = 6     /* not a gfx950 device, or a HIP launch error */
+} gm_status;
+
+/* Operation codes for gm_workspace_size(). */
+enum { GM_OP_FWD = 0, GM_OP_BWD = 1 };
+
+/* Returns GM_ABI_VERSION of the built library. */
+int gm_abi_version(void);
+
+/* Static, NUL-terminated description of a status code (host memory, never freed). */
+const char* gm_status_string(gm_status status);
+
+/*
+ * gm_gate -- Gumbel-Sigmoid gate with straight-through forward (Sec. 2.2;
+ * evaluation-time thresholding, Sec. 2.2 and Appendix F).
+ *
+ * For each of the n groups (a flat array, so the selectors of many layers can
+ * go through one call):
+ *   z    = logits[j] + (noise ? ln(noise[j]) - ln(1 - noise[j]) : 0)
+ *   y    = 1 / (1 + exp(-z / tau))
+ *   mask_out[j] = hard ? (z > 0 ? 1 : 0) : y       (z > 0 is exactly y > 1/2)
+ *   soft_out[j] = y                                  (only if soft_out != NULL)
+ * noise holds one uniform variate per group in the open interval (0, 1); NULL
+ * selects evaluation mode (noise removed).  Precondition, not checked: noise
+ * values lie in (0, 1).
+ *   logits   [n] fp32, required
+ *   noise    [n] fp32 or NULL
+ *   n        >= 0 (n == 0 is a no-op)
+ *   tau      > 0 and finite
+ *   hard     0 or 1
+ *   mask_out [n] fp32, required
+ *   soft_out [n] fp32 or NULL; keep it for the backward (gm_gate_bwd)
+ */
+gm_status gm_gate(const float* logits, const float* noise, int64_t n, float tau, int hard,
+                  float* mask_out, float* soft_out, gm_stream_t stream);
+
+/*
+ * gm_gate_bwd -- straight-through backward of the gate (Sec. 2.2): the
+ * gradient passes through the continuous relaxation,
+ *   dlogits[j] = dmask[j] * y[j] * (1 - y[j]) / tau,
+ * where y = soft_out of the forward and dmask the gradient of the selector
+ * (dgate of gm_masked_linear_bwd).
+ *   dmask, soft, dlogits: [n] fp32, required; n >= 0; tau > 0 and finite.
+ *   dlogits may alias dmask.
+ */
+gm_status gm_gate_bwd(const float* dmask, const float* soft, int64_t n, float tau, float* dlogits,
+                      gm_stream_t stream);
+
+/*
+ * gm_workspace_size -- host-only query of the workspace (bytes) that
+ * gm_masked_linear_fwd (op = GM_OP_FWD) or gm_masked_linear_bwd
+ * (op = GM_OP_BWD) needs for the given shape.  No device work.
+ *   bytes: HOST pointer, required.
+ */
+gm_status gm_workspace_size(int op, int64_t T, int64_t d_in, int64_t d_out, int32_t g, size_t* bytes);
+
+/*
+ * gm_masked_linear_fwd -- student forward of one target linear (Eq. 1):
+ *   Y = X (W (.) (mask (x) 1_{1 x g}))^T,
+ *   Y[t, o] = sum_v mask[o, v] * sum_{i in group v} X[t, i] W[o, i].
+ * A group with mask == 0 is skipped (its weights are never read); any other
+ * value scales the group (1.0 for a hard selector).  bf16 inputs, fp32
+ * accumulation, Y rounded to bf16 (round to nearest even).
+ *   X    [T, d_in]  bf16       W [d_out, d_in] bf16     mask [d_out, d_in/g] fp32
+ *   Y    [T, d_out] bf16, written in full
+ *   T >= 1; d_in, d_out >= 1 and multiples of 8; g in {64, 128, 256, 512}
+ *   dividing d_in.  Mask values must be finite and >= 0 (not checked).
+ *   ws / ws_bytes: workspace of at least gm_workspace_size(GM_OP_FWD, ...)
+ *   bytes (ws may be NULL when that size is 0).
+ */
+gm_status gm_masked_linear_fwd(const uint16_t* X, const uint16_t* W, const float* mask, int64_t T,
+                               int64_t d_in, int64_t d_out, int32_t g, uint16_t* Y, void* ws,
+                               size_t ws_bytes, gm_stream_t stream);
+
+/*
+ * gm_masked_linear_bwd -- backward of one target linear with frozen W
+ * (Sec. 2.2 STE, Sec. 2.4 frozen weights):
+ *   dX = dY (W (.) expand(mask))                       [T, d_in]   bf16
+ *   dgate[o, v] = sum_{i in group v} W[o, i] (dY^T X)[o, i]   [d_out, G_in] fp32
+ * dgate is produced for every group, kept or pruned, and does not depend on
+ * the mask; the weight gradient is never formed.  Either output may be NULL to
+ * skip it (both NULL is a no-op); mask may be NULL only when dX is NULL.
+ *   Shapes and constraints as gm_masked_linear_fwd; dY [T, d_out] bf16.
+ *   ws / ws_bytes: at least gm_workspace_size(GM_OP_BWD, ...) bytes.
+ */
+gm_status gm_masked_linear_bwd(const uint16_t* dY, const uint16_t* X, const uint16_t* W,
+                               const float* mask, int64_t T, int64_t d_in, int64_t d_out, int32_t g,
+                               uint16_t* dX, float* dgate, void* ws, size_t ws_bytes,
+                               gm_stream_t stream);
+
+/*
+ * gm_pack_rows -- export of a learned mask (Appendix F): copies the retained
+ * groups of W, row by row, into a packed buffer for the pruned model.
+ *   rowptr [d_out + 1] int32: rowptr[o] = number of kept groups in rows < o;
+ *                             rowptr[d_out] = total kept groups k.
+ *   Wp     [capacity, g] bf16: kept group number j of the matrix at Wp[j*g];
+ *   chunk  [capacity] int32:  its group column v;
+ *   scale  [capacity] fp32:   its mask value (1.0 for a hard selector).
+ * Groups with mask == 0 are dropped.  Groups beyond `capacity` are not written:
+ * the caller checks rowptr[d_out] <= capacity (capacity = d_out * d_in / g is
+ * always enough).  Shape constraints as gm_masked_linear_fwd.
+ */
+gm_status gm_pack_rows(const uint16_t* W, const float* mask, int64_t d_in, int64_t d_out, int32_t g,
+                       int64_t capacity, uint16_t* Wp, int32_t* chunk, float* scale,
+                       int32_t* rowptr, gm_stream_t stream);
+
+/*
+ * gm_packed_linear_fwd -- forward of a pruned linear from its packed export
+ * (the inference path of the pruned model): the same Y as gm_masked_linear_fwd
+ * with the mask that gm_pack_rows consumed.  Built for decode-sized T (reads
+ * every kept weight once per 16 tokens); any T >= 1 is accepted.
+ *   X [T, d_in] bf16; Wp, chunk, scale, rowptr as written by gm_pack_rows,
+ *   which must have held every kept group (rowptr[d_out] <= its capacity);
+ *   Y [T, d_out] bf16, written in full.
+ */
+gm_status gm_packed_linear_fwd(const uint16_t* X, const uint16_t* Wp, const int32_t* chunk,
+                               const float* scale, const int32_t* rowptr, int64_t T, int64_t d_in,
+                               int64_t d_out, int32_t g, uint16_t* Y, gm_stream_t stream);
+
+#ifdef __cplusplus
+} /* extern "C" */
+#endif
+
+#endif /* GROUPMASK_H */

@@ -1,0 +1,209 @@
+// C-ABI layer of libgroupmask: argument validation, workspace planning and
+// dispatch to the gfx950 kernels.  Nothing here allocates device memory, and
+// every entry point checks all of its arguments before the first launch.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <mutex>
+
+#include "../../include/groupmask.h"
+#include "gm_launch.h"
+
+#define GM_EXPORT extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+constexpr int64_t kMaxDim = int64_t(1) << 30;  // kernels index rows and columns with 32-bit ints
+constexpr int kMaxGroupCols = 512;             // per-tile group-column list of the forward GEMM
+constexpr int kDecodeTokens = 16;              // forward dispatch: T <= 16 takes the GEMV path
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// gfx950 check, cached per device.
+gm_status check_device() {
+  static std::mutex mu;
+  static signed char ok[256];  // 0 unknown, 1 yes, -1 no
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 256) return GM_ERR_DEVICE;
+  std::lock_guard<std::mutex> lock(mu);
+  if (ok[dev] == 0) {
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return GM_ERR_DEVICE;
+    ok[dev] = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : -1;
+  }
+  return ok[dev] == 1 ? GM_OK : GM_ERR_DEVICE;
+}
+
+gm_status from_hip(hipError_t e) { return e == hipSuccess ? GM_OK : GM_ERR_DEVICE; }
+
+gm_status check_tau(float tau) { return (std::isfinite(tau) && tau > 0.0f) ? GM_OK : GM_ERR_VALUE; }
+
+gm_status check_linear_shape(int64_t T, int64_t d_in, int64_t d_out, int32_t g) {
+  if (T < 1 || d_in < 1 || d_out < 1) return GM_ERR_SHAPE;
+  if (T > kMaxDim || d_in > kMaxDim || d_out > kMaxDim) return GM_ERR_SHAPE;
+  if (d_in % 8 || d_out % 8) return GM_ERR_SHAPE;
+  if (g != 64 && g != 128 && g != 256 && g != 512) return GM_ERR_SHAPE;
+  if (d_in % g) return GM_ERR_SHAPE;
+  if (d_in / g > kMaxGroupCols) return GM_ERR_SHAPE;
+  return GM_OK;
+}
+
+// Workspace of the backward, each part 256-byte aligned:
+//   colcount [G_in] int32 | rows [G_in * d_out] int32 | scales [G_in * d_out] fp32 | dYt [d_out * ldt] bf16
+struct BwdLayout {
+  size_t colcount, rows, scales, dyt, total;
+  int ldt;
+};
+
+BwdLayout bwd_layout(int64_t T, int64_t d_in, int64_t d_out, int32_t g) {
+  BwdLayout L;
+  const size_t G_in = size_t(d_in / g);
+  L.ldt = int(round_up(size_t(T), 8));
+  size_t off = 0;
+  L.colcount = off;
+  off = round_up(off + G_in * sizeof(int32_t), 256);
+  L.rows = off;
+  off = round_up(off + G_in * size_t(d_out) * sizeof(int32_t), 256);
+  L.scales = off;
+  off = round_up(off + G_in * size_t(d_out) * sizeof(float), 256);
+  L.dyt = off;
+  off = round_up(off + size_t(d_out) * size_t(L.ldt) * sizeof(uint16_t), 256);
+  L.total = off;
+  return L;
+}
+
+}  // namespace
+
+GM_EXPORT int gm_abi_version(void) { return GM_ABI_VERSION; }
+
+GM_EXPORT const char* gm_status_string(gm_status status) {
+  switch (status) {
+    case GM_OK: return "ok";
+    case GM_ERR_NULL: return "a required pointer is NULL";
+    case GM_ERR_SHAPE: return "a size is out of range or inconsistent";
+    case GM_ERR_VALUE: return "a scalar argument is out of range";
+    case GM_ERR_ALIGN: return "a pointer is not 16-byte aligned";
+    case GM_ERR_WORKSPACE: return "workspace missing or too small";
+    case GM_ERR_DEVICE: return "unsupported device or HIP launch error";
+  }
+  return "unknown status";
+}
+
+GM_EXPORT gm_status gm_gate(const float* logits, const float* noise, int64_t n, float tau, int hard,
+                            float* mask_out, float* soft_out, gm_stream_t stream) {
+  if (!logits || !mask_out) return GM_ERR_NULL;
+  if (n < 0) return GM_ERR_SHAPE;
+  if (gm_status st = check_tau(tau)) return st;
+  if (hard != 0 && hard != 1) return GM_ERR_VALUE;
+  if (!aligned16(logits) || !aligned16(mask_out) || (noise && !aligned16(noise)) ||
+      (soft_out && !aligned16(soft_out)))
+    return GM_ERR_ALIGN;
+  if (n == 0) return GM_OK;
+  if (gm_status st = check_device()) return st;
+  return from_hip(gm::launch_gate_fwd(logits, noise, n, tau, hard, mask_out, soft_out, stream));
+}
+
+GM_EXPORT gm_status gm_gate_bwd(const float* dmask, const float* soft, int64_t n, float tau, float* dlogits,
+                                gm_stream_t stream) {
+  if (!dmask || !soft || !dlogits) return GM_ERR_NULL;
+  if (n < 0) return GM_ERR_SHAPE;
+  if (gm_status st = check_tau(tau)) return st;
+  if (!aligned16(dmask) || !aligned16(soft) || !aligned16(dlogits)) return GM_ERR_ALIGN;
+  if (n == 0) return GM_OK;
+  if (gm_status st = check_device()) return st;
+  return from_hip(gm::launch_gate_bwd(dmask, soft, n, tau, dlogits, stream));
+}
+
+GM_EXPORT gm_status gm_workspace_size(int op, int64_t T, int64_t d_in, int64_t d_out, int32_t g, size_t* bytes) {
+  if (!bytes) return GM_ERR_NULL;
+  if (op != GM_OP_FWD && op != GM_OP_BWD) return GM_ERR_VALUE;
+  if (gm_status st = check_linear_shape(T, d_in, d_out, g)) return st;
+  *bytes = op == GM_OP_FWD ? 0 : bwd_layout(T, d_in, d_out, g).total;
+  return GM_OK;
+}
+
+GM_EXPORT gm_status gm_masked_linear_fwd(const uint16_t* X, const uint16_t* W, const float* mask, int64_t T,
+                                         int64_t d_in, int64_t d_out, int32_t g, uint16_t* Y, void* ws,
+                                         size_t ws_bytes, gm_stream_t stream) {
+  (void)ws;
+  (void)ws_bytes;
+  if (!X || !W || !mask || !Y) return GM_ERR_NULL;
+  if (gm_status st = check_linear_shape(T, d_in, d_out, g)) return st;
+  if (!aligned16(X) || !aligned16(W) || !aligned16(mask) || !aligned16(Y)) return GM_ERR_ALIGN;
+  if (gm_status st = check_device()) return st;
+  const int t = int(T), di = int(d_in), dout = int(d_out);
+  if (T <= kDecodeTokens && d_in / g <= gm::gemv_max_groups_per_row())
+    return from_hip(gm::launch_gemv_inplace(X, W, mask, t, di, dout, g, Y, stream));
+  return from_hip(gm::launch_fwd(X, W, mask, t, di, dout, g, Y, stream));
+}
+
+GM_EXPORT gm_status gm_masked_linear_bwd(const uint16_t* dY, const uint16_t* X, const uint16_t* W,
+                                         const float* mask, int64_t T, int64_t d_in, int64_t d_out, int32_t g,
+                                         uint16_t* dX, float* dgate, void* ws, size_t ws_bytes,
+                                         gm_stream_t stream) {
+  if (!dY || !X || !W) return GM_ERR_NULL;
+  if (dX && !mask) return GM_ERR_NULL;
+  if (gm_status st = check_linear_shape(T, d_in, d_out, g)) return st;
+  if (!aligned16(dY) || !aligned16(X) || !aligned16(W) || (mask && !aligned16(mask)) || (dX && !aligned16(dX)) ||
+      (dgate && !aligned16(dgate)))
+    return GM_ERR_ALIGN;
+  if (!dX && !dgate) return GM_OK;
+  const BwdLayout L = bwd_layout(T, d_in, d_out, g);
+  if (dX) {
+    if (!ws) return GM_ERR_WORKSPACE;
+    if (ws_bytes < L.total) return GM_ERR_WORKSPACE;
+    if (!aligned16(ws)) return GM_ERR_ALIGN;
+  }
+  if (gm_status st = check_device()) return st;
+
+  const int t = int(T), di = int(d_in), dout = int(d_out), G_in = int(d_in / g);
+  char* base = static_cast<char*>(ws);
+  int* colcount = dX ? reinterpret_cast<int*>(base + L.colcount) : nullptr;
+  int* rows = dX ? reinterpret_cast<int*>(base + L.rows) : nullptr;
+  float* scales = dX ? reinterpret_cast<float*>(base + L.scales) : nullptr;
+  uint16_t* dyt = dX ? reinterpret_cast<uint16_t*>(base + L.dyt) : nullptr;
+
+  if (dX) {
+    if (gm_status st = from_hip(gm::launch_col_lists(mask, dout, G_in, colcount, rows, scales, stream))) return st;
+  }
+  if (dgate) {
+    if (gm_status st = from_hip(gm::launch_dgate(dY, X, W, t, di, dout, g, dgate, dyt, L.ldt, stream))) return st;
+  } else {
+    if (gm_status st = from_hip(gm::launch_transpose(dY, t, dout, dyt, L.ldt, stream))) return st;
+  }
+  if (dX) {
+    if (gm_status st = from_hip(gm::launch_dx(dyt, L.ldt, W, colcount, rows, scales, t, di, dout, g, dX, stream)))
+      return st;
+  }
+  return GM_OK;
+}
+
+GM_EXPORT gm_status gm_pack_rows(const uint16_t* W, const float* mask, int64_t d_in, int64_t d_out, int32_t g,
+                                 int64_t capacity, uint16_t* Wp, int32_t* chunk, float* scale, int32_t* rowptr,
+                                 gm_stream_t stream) {
+  if (!W || !mask || !Wp || !chunk || !scale || !rowptr) return GM_ERR_NULL;
+  if (gm_status st = check_linear_shape(1, d_in, d_out, g)) return st;
+  if (capacity < 0 || capacity > d_out * (d_in / g)) return GM_ERR_SHAPE;
+  if (!aligned16(W) || !aligned16(mask) || !aligned16(Wp) || !aligned16(chunk) || !aligned16(scale) ||
+      !aligned16(rowptr))
+    return GM_ERR_ALIGN;
+  if (gm_status st = check_device()) return st;
+  return from_hip(gm::launch_pack_rows(W, mask, int(d_in), int(d_out), g, capacity, Wp, chunk, scale, rowptr,
+                                       stream));
+}
+
+GM_EXPORT gm_status gm_packed_linear_fwd(const uint16_t* X, const uint16_t* Wp, const int32_t* chunk,
+                                         const float* scale, const int32_t* rowptr, int64_t T, int64_t d_in,
+                                         int64_t d_out, int32_t g, uint16_t* Y, gm_stream_t stream) {
+  if (!X || !Wp || !chunk || !scale || !rowptr || !Y) return GM_ERR_NULL;
+  if (gm_status st = check_linear_shape(T, d_in, d_out, g)) return st;
+  if (!aligned16(X) || !aligned16(Wp) || !aligned16(chunk) || !aligned16(scale) || !aligned16(rowptr) ||
+      !aligned16(Y))
+    return GM_ERR_ALIGN;
+  if (gm_status st = check_device()) return st;
+  return from_hip(
+      gm::launch_gemv_packed(X, Wp, chunk, scale, rowptr, int(T), int(d_in), int(d_out), g, Y, stream));
+}

@@ -1,0 +1,95 @@
+// Gumbel-Sigmoid gate with straight-through estimator (Sec. 2.2), as two
+// coalesced elementwise passes over a flat array of group selectors.
+//
+// Forward:  z = logit + ln u - ln(1 - u)   (logit alone in evaluation mode)
+//           y = 1 / (1 + exp(-z / tau)),  mask = hard ? [z > 0] : y
+// Backward: dlogit = dmask * y (1 - y) / tau
+//
+// Each thread moves 16 bytes per array per step (float4); bytes per group are
+// 4 (logit) + 4 (noise) + 4 (mask) + 4 (soft) in the forward and 12 in the
+// backward, so both passes are bound by HBM bandwidth.
+#include "gm_device.h"
+#include "gm_launch.h"
+
+namespace gm {
+
+__device__ __forceinline__ void gate_one(float l, float u, bool has_noise, float tau, int hard, float& m,
+                                         float& y) {
+  float z = l;
+  if (has_noise) z = l + (logf(u) - logf(1.0f - u));
+  y = 1.0f / (1.0f + expf(-z / tau));
+  m = hard ? (z > 0.0f ? 1.0f : 0.0f) : y;
+}
+
+__global__ __launch_bounds__(256) void gate_fwd_kernel(const float* __restrict__ logits,
+                                                       const float* __restrict__ noise, int64_t n, float tau,
+                                                       int hard, float* __restrict__ mask,
+                                                       float* __restrict__ soft) {
+  const bool has_noise = noise != nullptr;
+  const int64_t nvec = n >> 2;
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < nvec; i += stride) {
+    const float4 l = reinterpret_cast<const float4*>(logits)[i];
+    float4 u = make_float4(0.5f, 0.5f, 0.5f, 0.5f);
+    if (has_noise) u = reinterpret_cast<const float4*>(noise)[i];
+    float4 m, y;
+    gate_one(l.x, u.x, has_noise, tau, hard, m.x, y.x);
+    gate_one(l.y, u.y, has_noise, tau, hard, m.y, y.y);
+    gate_one(l.z, u.z, has_noise, tau, hard, m.z, y.z);
+    gate_one(l.w, u.w, has_noise, tau, hard, m.w, y.w);
+    reinterpret_cast<float4*>(mask)[i] = m;
+    if (soft) reinterpret_cast<float4*>(soft)[i] = y;
+  }
+  if (blockIdx.x == 0 && threadIdx.x < (n & 3)) {
+    const int64_t j = nvec * 4 + threadIdx.x;
+    float m, y;
+    gate_one(logits[j], has_noise ? noise[j] : 0.5f, has_noise, tau, hard, m, y);
+    mask[j] = m;
+    if (soft) soft[j] = y;
+  }
+}
+
+// dlogits may alias dmask: every element is read before it is written by the same thread.
+__global__ __launch_bounds__(256) void gate_bwd_kernel(const float* dmask, const float* __restrict__ soft,
+                                                       int64_t n, float tau, float* dlogits) {
+  const int64_t nvec = n >> 2;
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < nvec; i += stride) {
+    const float4 d = reinterpret_cast<const float4*>(dmask)[i];
+    const float4 y = reinterpret_cast<const float4*>(soft)[i];
+    float4 r;
+    r.x = d.x * y.x * (1.0f - y.x) / tau;
+    r.y = d.y * y.y * (1.0f - y.y) / tau;
+    r.z = d.z * y.z * (1.0f - y.z) / tau;
+    r.w = d.w * y.w * (1.0f - y.w) / tau;
+    reinterpret_cast<float4*>(dlogits)[i] = r;
+  }
+  if (blockIdx.x == 0 && threadIdx.x < (n & 3)) {
+    const int64_t j = nvec * 4 + threadIdx.x;
+    const float y = soft[j];
+    dlogits[j] = dmask[j] * y * (1.0f - y) / tau;
+  }
+}
+
+static unsigned elementwise_grid(int64_t n) {
+  const int64_t nvec = (n + 3) >> 2;
+  int64_t blocks = (nvec + 255) / 256;
+  if (blocks < 1) blocks = 1;
+  if (blocks > 8192) blocks = 8192;  // 32 blocks per CU, grid-stride beyond
+  return unsigned(blocks);
+}
+
+hipError_t launch_gate_fwd(const float* logits, const float* noise, int64_t n, float tau, int hard, float* mask,
+                           float* soft, hipStream_t s) {
+  hipLaunchKernelGGL(gate_fwd_kernel, dim3(elementwise_grid(n)), dim3(256), 0, s, logits, noise, n, tau, hard,
+                     mask, soft);
+  return hipGetLastError();
+}
+
+hipError_t launch_gate_bwd(const float* dmask, const float* soft, int64_t n, float tau, float* dlogits,
+                           hipStream_t s) {
+  hipLaunchKernelGGL(gate_bwd_kernel, dim3(elementwise_grid(n)), dim3(256), 0, s, dmask, soft, n, tau, dlogits);
+  return hipGetLastError();
+}
+
+}  // namespace gm

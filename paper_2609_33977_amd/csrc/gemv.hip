@@ -1,0 +1,182 @@
+// Decode-sized forward of a group-masked linear: Y[t, o] = sum over the kept
+// groups (o, v) of mask[o, v] * sum_{i in v} X[t, i] W[o, i], for up to 16
+// tokens per pass (Eq. 1 applied to the pruned model's linear).
+//
+// One wave per output row.  A group of g bf16 weights is g*2 contiguous bytes;
+// the wave covers 512 consecutive weights per step (512/g groups side by side,
+// 16 bytes per lane), so every kept weight is read from HBM exactly once per
+// pass and pruned groups are never touched.  Bytes per pass: 2 * nnz (kept
+// weights) + index/mask + 2 T (d_in + d_out); the kernel is HBM-bound for small T.
+//
+// Two layouts of the same row-major kept-group sequence:
+//   in place : W [d_out, d_in] with the mask deciding which groups are read;
+//   packed   : Wp [k, g] + chunk [k] + scale [k] + rowptr [d_out + 1] written
+//              by the export (Appendix F), the row's groups contiguous.
+#include "gm_device.h"
+#include "gm_launch.h"
+
+namespace gm {
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Dot product of two vectors of 8 bf16 with fp32 accumulation (v_dot2_f32_bf16).
+// The bf16 pairs are moved out of the 32-bit lanes with memcpy: a bit_cast of
+// a subscripted vector element inside this unrolled loop was folded to element
+// 0 by the compiler (every step used the first pair).
+__device__ __forceinline__ float dot8_bf16(u32x4 w, u32x4 x) {
+  const uint32_t wa[4] = {w.x, w.y, w.z, w.w};
+  const uint32_t xa[4] = {x.x, x.y, x.z, x.w};
+  float acc = 0.0f;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    bf16x2 a, b;
+    __builtin_memcpy(&a, &wa[q], sizeof(a));
+    __builtin_memcpy(&b, &xa[q], sizeof(b));
+    acc = __builtin_amdgcn_fdot2_f32_bf16(a, b, acc, false);
+  }
+  return acc;
+}
+
+constexpr int kMaxGroupsPerRow = 512;  // G_in limit of the in-place variant's per-wave list
+
+template <int TB, bool PACKED>
+__global__ __launch_bounds__(256) void gemv_kernel(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
+                                                   const float* __restrict__ mask,
+                                                   const uint16_t* __restrict__ Wp, const int* __restrict__ chunk,
+                                                   const float* __restrict__ scale,
+                                                   const int* __restrict__ rowptr, int T, int t0, int d_in,
+                                                   int d_out, int g, uint16_t* __restrict__ Y) {
+  __shared__ int s_v[4][PACKED ? 1 : kMaxGroupsPerRow];
+  __shared__ float s_m[4][PACKED ? 1 : kMaxGroupsPerRow];
+  const int lane = threadIdx.x & 63;
+  const int wv = threadIdx.x >> 6;
+  const int o = blockIdx.x * 4 + wv;
+  if (o >= d_out) return;  // whole wave leaves together; no block barrier below
+  const int G_in = d_in / g;
+  const int lanes_per_group = g >> 3;
+  const int gps = 64 / lanes_per_group;  // groups per wave step (>= 1 for g <= 512)
+  const int slot = lane / lanes_per_group;
+  const int e = (lane % lanes_per_group) * 8;
+  const int ntok = min(TB, T - t0);
+
+  int nk;
+  int64_t pbase = 0;
+  if constexpr (PACKED) {
+    pbase = rowptr[o];
+    nk = rowptr[o + 1] - int(pbase);
+  } else {
+    // Compact this row's kept groups into the wave's LDS list, in column order.
+    nk = 0;
+    for (int vb = 0; vb < G_in; vb += 64) {
+      const int v = vb + lane;
+      const float m = v < G_in ? mask[int64_t(o) * G_in + v] : 0.0f;
+      const uint64_t bal = __ballot(m != 0.0f);
+      if (m != 0.0f) {
+        const int r = nk + __popcll(bal & ((uint64_t(1) << lane) - 1));
+        s_v[wv][r] = v;
+        s_m[wv][r] = m;
+      }
+      nk += __popcll(bal);
+    }
+    // LDS writes of this wave become visible to its other lanes before the list is read.
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+
+  float acc[TB];
+#pragma unroll
+  for (int t = 0; t < TB; ++t) acc[t] = 0.0f;
+
+  for (int k0 = 0; k0 < nk; k0 += 2 * gps) {
+    const int ka = k0 + slot;
+    const int kb = k0 + gps + slot;
+    int va = 0, vb = 0;
+    float ma = 0.0f, mb = 0.0f;
+    u32x4 wa = zero16(), wb = zero16();
+    if (ka < nk) {
+      if constexpr (PACKED) {
+        va = chunk[pbase + ka];
+        ma = scale[pbase + ka];
+        wa = ld16(Wp + (pbase + ka) * g + e);
+      } else {
+        va = s_v[wv][ka];
+        ma = s_m[wv][ka];
+        wa = ld16(W + int64_t(o) * d_in + int64_t(va) * g + e);
+      }
+    }
+    if (kb < nk) {
+      if constexpr (PACKED) {
+        vb = chunk[pbase + kb];
+        mb = scale[pbase + kb];
+        wb = ld16(Wp + (pbase + kb) * g + e);
+      } else {
+        vb = s_v[wv][kb];
+        mb = s_m[wv][kb];
+        wb = ld16(W + int64_t(o) * d_in + int64_t(vb) * g + e);
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < TB; ++t) {
+      if (t < ntok) {
+        const uint16_t* xr = X + int64_t(t0 + t) * d_in + e;
+        float p = 0.0f;
+        if (ka < nk) p += ma * dot8_bf16(wa, ld16(xr + int64_t(va) * g));
+        if (kb < nk) p += mb * dot8_bf16(wb, ld16(xr + int64_t(vb) * g));
+        acc[t] += p;
+      }
+    }
+  }
+
+#pragma unroll
+  for (int t = 0; t < TB; ++t) {
+    float s = acc[t];
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) s += __shfl_xor(s, d);
+    acc[t] = s;
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int t = 0; t < TB; ++t)
+      if (t < ntok) Y[int64_t(t0 + t) * d_out + o] = uint16_t(f32_to_bf16_bits(acc[t]));
+  }
+}
+
+template <bool PACKED>
+static hipError_t gemv_passes(const uint16_t* X, const uint16_t* W, const float* mask, const uint16_t* Wp,
+                              const int* chunk, const float* scale, const int* rowptr, int T, int d_in, int d_out,
+                              int g, uint16_t* Y, hipStream_t s) {
+  const dim3 grid((d_out + 3) / 4), block(256);
+  for (int t0 = 0; t0 < T; t0 += 16) {
+    const int nt = T - t0;
+    if (nt == 1)
+      hipLaunchKernelGGL((gemv_kernel<1, PACKED>), grid, block, 0, s, X, W, mask, Wp, chunk, scale, rowptr, T, t0,
+                         d_in, d_out, g, Y);
+    else if (nt <= 4)
+      hipLaunchKernelGGL((gemv_kernel<4, PACKED>), grid, block, 0, s, X, W, mask, Wp, chunk, scale, rowptr, T, t0,
+                         d_in, d_out, g, Y);
+    else if (nt <= 8)
+      hipLaunchKernelGGL((gemv_kernel<8, PACKED>), grid, block, 0, s, X, W, mask, Wp, chunk, scale, rowptr, T, t0,
+                         d_in, d_out, g, Y);
+    else
+      hipLaunchKernelGGL((gemv_kernel<16, PACKED>), grid, block, 0, s, X, W, mask, Wp, chunk, scale, rowptr, T, t0,
+                         d_in, d_out, g, Y);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_gemv_inplace(const uint16_t* X, const uint16_t* W, const float* mask, int T, int d_in, int d_out,
+                               int g, uint16_t* Y, hipStream_t s) {
+  return gemv_passes<false>(X, W, mask, nullptr, nullptr, nullptr, nullptr, T, d_in, d_out, g, Y, s);
+}
+
+hipError_t launch_gemv_packed(const uint16_t* X, const uint16_t* Wp, const int* chunk, const float* scale,
+                              const int* rowptr, int T, int d_in, int d_out, int g, uint16_t* Y, hipStream_t s) {
+  return gemv_passes<true>(X, nullptr, nullptr, Wp, chunk, scale, rowptr, T, d_in, d_out, g, Y, s);
+}
+
+int gemv_max_groups_per_row() { return kMaxGroupsPerRow; }
+
+}  // namespace gm

@@ -1,0 +1,80 @@
+// Device-side helpers shared by the gfx950 kernels of the group-masked linear layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gm {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------- bf16 <-> fp32
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(uint32_t(h) << 16); }
+
+// Round-to-nearest-even fp32 -> bf16 (finite inputs; NaN kept quiet).
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u) return (u >> 16) | ((u & 0xffffu) ? 0x40u : 0u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+}
+
+// ---------------------------------------------------------------- 16-byte moves
+
+__device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+__device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+__device__ __forceinline__ u32x4 zero16() { return u32x4{0u, 0u, 0u, 0u}; }
+
+// Multiply the 8 bf16 values of a 16-byte vector by s (fp32), rounding back to bf16.
+__device__ __forceinline__ u32x4 scale_bf16x8(u32x4 v, float s) {
+  u32x4 r;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) r[q] = pack_bf16x2(bf16_lo(v[q]) * s, bf16_hi(v[q]) * s);
+  return r;
+}
+
+// Transpose an 8 x 8 block of 16-bit values held as 8 vectors of 8:
+// out[c] element j = in[j] element c.
+__device__ __forceinline__ void transpose8x8_b16(const u32x4 (&in)[8], u32x4 (&out)[8]) {
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    const int q = c >> 1;
+    const bool hi = c & 1;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      uint32_t a = in[2 * p][q];
+      uint32_t b = in[2 * p + 1][q];
+      out[c][p] = hi ? ((a >> 16) | (b & 0xffff0000u)) : ((a & 0xffffu) | (b << 16));
+    }
+  }
+}
+
+// ---------------------------------------------------------------- MFMA
+
+// v_mfma_f32_16x16x32_bf16: C[16x16] += A[16x32] B[32x16].
+// Lane l supplies A row (l % 16), k slice [8 (l/16), 8 (l/16) + 8) and
+// B column (l % 16) over the same k slice; it receives C rows 4 (l/16) + j,
+// j = 0..3, of column (l % 16).
+__device__ __forceinline__ f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+// ---------------------------------------------------------------- LDS tiles
+
+// A K-major bf16 tile of R rows x 64 k (128 bytes per row, eight 16-byte
+// chunks).  Chunk c of row r is stored at chunk position c ^ (r & 7), so eight
+// consecutive rows read at one logical chunk hit eight different bank groups.
+__device__ __forceinline__ int swz64(int row, int chunk) { return row * 8 + (chunk ^ (row & 7)); }
+
+}  // namespace gm

@@ -1,0 +1,126 @@
+"""The C-ABI library loads, exports every declared entry point, and rejects bad
+arguments before touching any device (no compute call here: no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_33977_amd as gm
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "groupmask.h")
+
+FAKE = ctypes.c_void_p(1 << 20)      # non-NULL, 16-byte aligned; never dereferenced on the error paths used
+MISALIGNED = ctypes.c_void_p((1 << 20) + 4)
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gm_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    declared = _declared_functions()
+    assert declared, "no declarations parsed"
+    assert sorted(gm.EXPORTS) == declared
+    for name in declared:
+        assert hasattr(gm.LIB, name), name
+
+
+def test_abi_version_and_status_strings():
+    assert gm.gm_abi_version() == 1
+    for s in range(7):
+        assert gm.status_string(s)
+    assert gm.status_string(99) == "unknown status"
+
+
+def test_workspace_size_host_only():
+    ws = gm.gm_workspace_size(gm.GM_OP_BWD, 4096, 4096, 4096, 256)
+    # col counts + row lists + scales + dY^T, each part rounded to 256 bytes
+    G_in = 4096 // 256
+    expect = 256 + 2 * (G_in * 4096 * 4) + 4096 * 4096 * 2
+    assert ws == expect
+    assert gm.gm_workspace_size(gm.GM_OP_FWD, 4096, 4096, 4096, 256) == 0
+    # ragged T: dY^T rows padded to a multiple of 8 tokens
+    assert gm.gm_workspace_size(gm.GM_OP_BWD, 77, 320, 200, 64) > 200 * 80 * 2
+
+
+@pytest.mark.parametrize("args,code", [
+    ((4096, 4096, 4096, 100), gm.GM_ERR_SHAPE),      # group size not supported
+    ((4096, 4000, 4096, 256), gm.GM_ERR_SHAPE),      # d_in not a multiple of g
+    ((0, 4096, 4096, 256), gm.GM_ERR_SHAPE),         # empty T
+    ((16, 4096, 4092, 256), gm.GM_ERR_SHAPE),        # d_out not a multiple of 8
+    ((16, 64 * 1024, 64, 64), gm.GM_ERR_SHAPE),      # more than 512 group columns
+])
+def test_workspace_size_rejects_bad_shapes(args, code):
+    out = ctypes.c_size_t(0)
+    assert gm.LIB.gm_workspace_size(gm.GM_OP_BWD, *args, ctypes.byref(out)) == code
+
+
+def test_workspace_size_rejects_bad_op_and_null():
+    out = ctypes.c_size_t(0)
+    assert gm.LIB.gm_workspace_size(7, 16, 256, 256, 256, ctypes.byref(out)) == gm.GM_ERR_VALUE
+    assert gm.LIB.gm_workspace_size(gm.GM_OP_FWD, 16, 256, 256, 256, None) == gm.GM_ERR_NULL
+
+
+def test_gate_argument_errors():
+    L = gm.LIB
+    assert L.gm_gate(None, None, 16, 0.5, 1, FAKE, None, None) == gm.GM_ERR_NULL
+    assert L.gm_gate(FAKE, None, 16, 0.5, 1, None, None, None) == gm.GM_ERR_NULL
+    assert L.gm_gate(FAKE, None, -1, 0.5, 1, FAKE, None, None) == gm.GM_ERR_SHAPE
+    assert L.gm_gate(FAKE, None, 16, 0.0, 1, FAKE, None, None) == gm.GM_ERR_VALUE
+    assert L.gm_gate(FAKE, None, 16, -1.0, 1, FAKE, None, None) == gm.GM_ERR_VALUE
+    assert L.gm_gate(FAKE, None, 16, float("nan"), 1, FAKE, None, None) == gm.GM_ERR_VALUE
+    assert L.gm_gate(FAKE, None, 16, float("inf"), 1, FAKE, None, None) == gm.GM_ERR_VALUE
+    assert L.gm_gate(FAKE, None, 16, 0.5, 2, FAKE, None, None) == gm.GM_ERR_VALUE
+    assert L.gm_gate(MISALIGNED, None, 16, 0.5, 1, FAKE, None, None) == gm.GM_ERR_ALIGN
+    assert L.gm_gate(FAKE, MISALIGNED, 16, 0.5, 1, FAKE, None, None) == gm.GM_ERR_ALIGN
+    assert L.gm_gate(FAKE, None, 16, 0.5, 1, FAKE, MISALIGNED, None) == gm.GM_ERR_ALIGN
+    # n == 0 is a no-op that succeeds without a device
+    assert L.gm_gate(FAKE, None, 0, 0.5, 1, FAKE, None, None) == gm.GM_OK
+
+
+def test_gate_bwd_argument_errors():
+    L = gm.LIB
+    assert L.gm_gate_bwd(None, FAKE, 8, 0.4, FAKE, None) == gm.GM_ERR_NULL
+    assert L.gm_gate_bwd(FAKE, None, 8, 0.4, FAKE, None) == gm.GM_ERR_NULL
+    assert L.gm_gate_bwd(FAKE, FAKE, 8, 0.4, None, None) == gm.GM_ERR_NULL
+    assert L.gm_gate_bwd(FAKE, FAKE, -3, 0.4, FAKE, None) == gm.GM_ERR_SHAPE
+    assert L.gm_gate_bwd(FAKE, FAKE, 8, 0.0, FAKE, None) == gm.GM_ERR_VALUE
+    assert L.gm_gate_bwd(FAKE, FAKE, 8, 0.4, MISALIGNED, None) == gm.GM_ERR_ALIGN
+    assert L.gm_gate_bwd(FAKE, FAKE, 0, 0.4, FAKE, None) == gm.GM_OK
+
+
+def test_linear_argument_errors():
+    L = gm.LIB
+    fwd = L.gm_masked_linear_fwd
+    assert fwd(None, FAKE, FAKE, 16, 256, 256, 256, FAKE, None, 0, None) == gm.GM_ERR_NULL
+    assert fwd(FAKE, FAKE, None, 16, 256, 256, 256, FAKE, None, 0, None) == gm.GM_ERR_NULL
+    assert fwd(FAKE, FAKE, FAKE, 16, 256, 256, 96, FAKE, None, 0, None) == gm.GM_ERR_SHAPE
+    assert fwd(FAKE, FAKE, FAKE, 0, 256, 256, 256, FAKE, None, 0, None) == gm.GM_ERR_SHAPE
+    assert fwd(FAKE, FAKE, FAKE, 16, 256, 250, 256, FAKE, None, 0, None) == gm.GM_ERR_SHAPE
+    assert fwd(FAKE, MISALIGNED, FAKE, 16, 256, 256, 256, FAKE, None, 0, None) == gm.GM_ERR_ALIGN
+
+    bwd = L.gm_masked_linear_bwd
+    # dX requested without a mask
+    assert bwd(FAKE, FAKE, FAKE, None, 16, 256, 256, 256, FAKE, None, FAKE, 1 << 30, None) == gm.GM_ERR_NULL
+    assert bwd(None, FAKE, FAKE, FAKE, 16, 256, 256, 256, FAKE, FAKE, FAKE, 1 << 30, None) == gm.GM_ERR_NULL
+    # both outputs NULL: nothing to do
+    assert bwd(FAKE, FAKE, FAKE, FAKE, 16, 256, 256, 256, None, None, None, 0, None) == gm.GM_OK
+    # dX needs the workspace
+    need = gm.gm_workspace_size(gm.GM_OP_BWD, 16, 256, 256, 256)
+    assert bwd(FAKE, FAKE, FAKE, FAKE, 16, 256, 256, 256, FAKE, None, None, 0, None) == gm.GM_ERR_WORKSPACE
+    assert bwd(FAKE, FAKE, FAKE, FAKE, 16, 256, 256, 256, FAKE, None, FAKE, need - 1, None) == gm.GM_ERR_WORKSPACE
+    assert bwd(FAKE, FAKE, FAKE, FAKE, 16, 256, 256, 256, FAKE, None, MISALIGNED, need, None) == gm.GM_ERR_ALIGN
+    assert bwd(FAKE, FAKE, FAKE, FAKE, 16, 256, 512, 256, FAKE, MISALIGNED, FAKE, need, None) == gm.GM_ERR_ALIGN
+
+
+def test_pack_argument_errors():
+    L = gm.LIB
+    assert L.gm_pack_rows(FAKE, FAKE, 256, 16, 256, 16, FAKE, FAKE, None, FAKE, None) == gm.GM_ERR_NULL
+    assert L.gm_pack_rows(FAKE, FAKE, 256, 16, 256, 17, FAKE, FAKE, FAKE, FAKE, None) == gm.GM_ERR_SHAPE
+    assert L.gm_pack_rows(FAKE, FAKE, 256, 16, 256, -1, FAKE, FAKE, FAKE, FAKE, None) == gm.GM_ERR_SHAPE
+    assert L.gm_packed_linear_fwd(FAKE, FAKE, FAKE, FAKE, None, 1, 256, 16, 256, FAKE, None) == gm.GM_ERR_NULL
+    assert L.gm_packed_linear_fwd(FAKE, FAKE, FAKE, FAKE, FAKE, 1, 200, 16, 256, FAKE, None) == gm.GM_ERR_SHAPE

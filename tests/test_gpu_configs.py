@@ -1,0 +1,170 @@
+"""GPU parity at the full sizes of the five workloads, in the launch
+configuration the benchmark times.  The oracle checks whole tensors where it
+finishes in seconds and otherwise sampled rows, columns and groups, computed
+from the same inputs restricted to the sample (row and column slices of a
+product are products of slices)."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from gpu_support import (assert_close, dev_bf16, dev_f32, empty_bf16, empty_f32, host_bits, host_f64_from_bf16, say,
+                         sync, workspace)
+
+pytestmark = pytest.mark.gpu
+
+N_SAMPLE_ROWS = 64
+
+
+def _step(d, g, tau):
+    """gate -> fwd -> bwd -> gate bwd, the benchmark's step, on device tensors."""
+    import paper_2609_33977_amd as gm
+    T, d_in = d["X"].shape
+    d_out = d["W"].shape[0]
+    n = d["logits"].numel()
+    mask, soft = empty_f32(d_out, d_in // g), empty_f32(d_out, d_in // g)
+    gm.gm_gate(d["logits"], d["noise"], tau, True, mask, soft)
+    Y = empty_bf16(T, d_out)
+    gm.gm_masked_linear_fwd(d["X"], d["W"], mask, g, Y)
+    dX, dgate = empty_bf16(T, d_in), empty_f32(d_out, d_in // g)
+    ws = workspace(gm.gm_workspace_size(gm.GM_OP_BWD, T, d_in, d_out, g))
+    gm.gm_masked_linear_bwd(d["dY"], d["X"], d["W"], mask, g, dX, dgate, ws)
+    dlog = empty_f32(n)
+    gm.gm_gate_bwd(dgate, soft, tau, dlog)
+    sync()
+    assert n == d_out * (d_in // g)
+    return mask, soft, Y, dX, dgate, dlog
+
+
+def _device(case):
+    return dict(X=dev_bf16(case.X), W=dev_bf16(case.W), dY=dev_bf16(case.dY),
+                logits=dev_f32(case.logits), noise=dev_f32(case.noise))
+
+
+def _check_sampled(case, mask, Y, dX, dgate, key, n_rows=N_SAMPLE_ROWS):
+    r = workloads.gen.rng_for(300, *key)
+    T, d_in, d_out, g = case.T, case.d_in, case.d_out, case.g
+    X, W, dY = oracle.from_bf16(case.X), oracle.from_bf16(case.W), oracle.from_bf16(case.dY)
+    m = case.mask.astype(np.float64)
+    assert np.array_equal(mask.cpu().numpy(), case.mask), "hard mask differs from the budgeted selection"
+    t_s = np.sort(r.choice(T, size=min(n_rows, T), replace=False))
+    o_s = np.sort(r.choice(d_out, size=min(n_rows, d_out), replace=False))
+    Yg = host_f64_from_bf16(Y)[t_s]
+    assert_close("Y (sampled tokens)", Yg, oracle.linear_fwd(X[t_s], W, m, g))
+    dXg = host_f64_from_bf16(dX)[t_s]
+    assert_close("dX (sampled tokens)", dXg, oracle.linear_bwd_dx(dY[t_s], W, m, g))
+    dgg = dgate.cpu().numpy()[o_s]
+    assert_close("dgate (sampled rows)", dgg, oracle.linear_bwd_dgate(dY[:, o_s], X, W[o_s], g))
+
+
+def test_attention_projection_4096_full_tensors():
+    cfg = workloads.config("attn_4096")
+    T, g, tau = cfg["T"], cfg["g"], cfg["tau"]
+    _, d_out, d_in = cfg["linears"][0]
+    say(f"attn 4096: T={T} {d_out}x{d_in} g={g}")
+    case = workloads.make_linear_case((2, 0, 0), T, d_in, d_out, g, None, tau=tau)
+    mask, soft, Y, dX, dgate, dlog = _step(_device(case), g, tau)
+    m_ref, y_ref = oracle.gate(case.logits, case.noise, tau, True)
+    assert np.array_equal(mask.cpu().numpy(), m_ref)
+    assert int(m_ref.sum()) == d_out * (d_in // g) // 2
+    X, W, dY = oracle.from_bf16(case.X), oracle.from_bf16(case.W), oracle.from_bf16(case.dY)
+    assert_close("Y", host_f64_from_bf16(Y), oracle.linear_fwd(X, W, m_ref, g))
+    dXr, dgr = oracle.linear_bwd(dY, X, W, m_ref, g)
+    assert_close("dX", host_f64_from_bf16(dX), dXr)
+    assert_close("dgate", dgate.cpu().numpy(), dgr)
+    assert_close("dlogits", dlog.cpu().numpy().reshape(dgr.shape), oracle.gate_bwd(dgate.cpu().numpy(), y_ref, tau),
+                 1e-5)
+
+
+def test_mlp_trio_layer_adaptive():
+    cfg = workloads.config("mlp_trio_7b")
+    T, g, tau = cfg["T"], cfg["g"], cfg["tau"]
+    groups = [do * di // g for _, do, di in cfg["linears"]]
+    kept, s = workloads.kept_counts_uniform_law(workloads.gen.rng_for(3, 1), groups, 0.3, 0.7)
+    for j, (name, d_out, d_in) in enumerate(cfg["linears"]):
+        say(f"mlp {name}: T={T} {d_out}x{d_in} sparsity {s[j]:.3f}")
+        case = workloads.make_linear_case((3, 0, j), T, d_in, d_out, g, kept[j], tau=tau)
+        mask, _, Y, dX, dgate, _ = _step(_device(case), g, tau)
+        assert int(mask.sum().item()) == kept[j]
+        _check_sampled(case, mask, Y, dX, dgate, (3, j))
+
+
+def _llama2_7b_budget():
+    cfg = workloads.config("llama2_7b_step")
+    g = cfg["g"]
+    shapes = [(do, di) for _ in range(cfg["layers"]) for _, do, di in cfg["linears"]]
+    groups = [do * di // g for do, di in shapes]
+    kept, _ = workloads.kept_counts_beta_law(workloads.gen.rng_for(4, 0), groups, [do * di for do, di in shapes])
+    return cfg, shapes, groups, kept
+
+
+def test_llama2_7b_batched_gate_meets_global_budget():
+    import paper_2609_33977_amd as gm
+    cfg, shapes, groups, kept = _llama2_7b_budget()
+    assert sum(kept) * 2 == sum(groups)
+    # One batched gate over all 224 selector matrices, as in the mask-learning step.
+    r = workloads.gen.rng_for(4, 1)
+    flat = np.concatenate([workloads.random_kept_mask(r, G, k) for G, k in zip(groups, kept)])
+    logits, noise = workloads.budgeted_gate_inputs(r, flat)
+    say(f"llama2-7b: batched gate over {flat.size} groups")
+    d_m, d_y = empty_f32(flat.size), empty_f32(flat.size)
+    gm.gm_gate(dev_f32(logits), dev_f32(noise), cfg["tau"], True, d_m, d_y)
+    sync()
+    mg = d_m.cpu().numpy()
+    assert np.array_equal(mg, flat)
+    s_layer, s_glob = oracle.sparsity(np.split(mg, np.cumsum(groups)[:-1]), shapes)
+    assert s_glob == pytest.approx(0.5, abs=1e-12)
+    assert min(s_layer) < 0.35 and max(s_layer) > 0.65  # budgets really are layer-adaptive
+
+
+@pytest.mark.parametrize("layer", [0, 31])
+def test_llama2_7b_layer_linears(layer):
+    cfg, shapes, groups, kept = _llama2_7b_budget()
+    T, g, tau = cfg["T"], cfg["g"], cfg["tau"]
+    for j, (name, d_out, d_in) in enumerate(cfg["linears"]):
+        idx = layer * len(cfg["linears"]) + j
+        say(f"llama2-7b layer {layer} {name}: {d_out}x{d_in} kept {kept[idx]}/{groups[idx]}")
+        case = workloads.make_linear_case((4, layer, j), T, d_in, d_out, g, kept[idx], tau=tau)
+        mask, _, Y, dX, dgate, _ = _step(_device(case), g, tau)
+        _check_sampled(case, mask, Y, dX, dgate, (4, layer, j), n_rows=32)
+
+
+@pytest.mark.parametrize("T", [1, 8, 16, 512])
+def test_llama2_13b_inference_path(T):
+    import torch
+    import paper_2609_33977_amd as gm
+    cfg = workloads.config("llama2_13b_infer")
+    g = cfg["g"]
+    for name, d_out, d_in in (cfg["linears"][0], cfg["linears"][4], cfg["linears"][6]):
+        say(f"13b {name}: T={T} {d_out}x{d_in}")
+        case = workloads.make_linear_case((5, T, d_out, d_in), T, d_in, d_out, g, None, tau=cfg["tau"])
+        X, W, mask = dev_bf16(case.X), dev_bf16(case.W), dev_f32(case.mask)
+        Y = empty_bf16(T, d_out)
+        gm.gm_masked_linear_fwd(X, W, mask, g, Y)
+        cap = d_out * (d_in // g)
+        Wp = torch.empty(cap, g, dtype=torch.bfloat16, device="cuda")
+        chunk = torch.empty(cap, dtype=torch.int32, device="cuda")
+        scale = torch.empty(cap, dtype=torch.float32, device="cuda")
+        rowptr = torch.empty(d_out + 1, dtype=torch.int32, device="cuda")
+        gm.gm_pack_rows(W, mask, g, cap, Wp, chunk, scale, rowptr)
+        Yp = empty_bf16(T, d_out)
+        if T <= 16:
+            gm.gm_packed_linear_fwd(X, Wp, chunk, scale, rowptr, d_out, g, Yp)
+        sync()
+        assert int(rowptr[-1].item()) == cap // 2
+        t_s = np.arange(T) if T <= 64 else np.sort(workloads.gen.rng_for(5, T).choice(T, 64, replace=False))
+        ref = oracle.linear_fwd(oracle.from_bf16(case.X)[t_s], oracle.from_bf16(case.W), case.mask, g)
+        assert_close("Y", host_f64_from_bf16(Y)[t_s], ref)
+        if T <= 16:
+            assert np.array_equal(host_bits(Yp), host_bits(Y))
+
+
+@pytest.mark.parametrize("g", [64, 128, 256, 512])
+def test_llama2_13b_group_size_sweep(g):
+    cfg = workloads.config("llama2_13b_infer")
+    T = cfg["T_sweep"]
+    for name, d_out, d_in in (cfg["linears"][0], cfg["linears"][4], cfg["linears"][6]):
+        say(f"13b sweep {name}: T={T} {d_out}x{d_in} g={g}")
+        case = workloads.make_linear_case((5, 99, d_out, g), T, d_in, d_out, g, None, tau=cfg["tau"])
+        mask, _, Y, dX, dgate, _ = _step(_device(case), g, cfg["tau"])
+        _check_sampled(case, mask, Y, dX, dgate, (5, g, d_out), n_rows=32)

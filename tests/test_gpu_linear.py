@@ -1,0 +1,204 @@
+"""GPU parity of the masked linear (forward, dX, dgate, decode and packed paths)
+against the fp64 oracle, on shapes that span several tiles and ragged tails."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from gpu_support import (assert_close, dev_bf16, dev_f32, empty_bf16, empty_f32, host_bits, host_f64_from_bf16, say,
+                         sync, workspace)
+
+pytestmark = pytest.mark.gpu
+
+
+def _dev_case(case, mask=None):
+    m = case.mask if mask is None else mask
+    return dict(X=dev_bf16(case.X), W=dev_bf16(case.W), dY=dev_bf16(case.dY), mask=dev_f32(m))
+
+
+def _fwd(d, g):
+    import paper_2609_33977_amd as gm
+    T = d["X"].shape[0]
+    d_out = d["W"].shape[0]
+    Y = empty_bf16(T, d_out)
+    ws = workspace(gm.gm_workspace_size(gm.GM_OP_FWD, T, d["X"].shape[1], d_out, g))
+    gm.gm_masked_linear_fwd(d["X"], d["W"], d["mask"], g, Y, ws)
+    sync()
+    return Y
+
+
+def _bwd(d, g, want_dx=True, want_dgate=True):
+    import paper_2609_33977_amd as gm
+    T, d_in = d["X"].shape
+    d_out = d["W"].shape[0]
+    dX = empty_bf16(T, d_in) if want_dx else None
+    dgate = empty_f32(d_out, d_in // g) if want_dgate else None
+    ws = workspace(gm.gm_workspace_size(gm.GM_OP_BWD, T, d_in, d_out, g))
+    gm.gm_masked_linear_bwd(d["dY"], d["X"], d["W"], d["mask"], g, dX, dgate, ws)
+    sync()
+    return dX, dgate
+
+
+def _oracle_all(case, mask=None):
+    m = case.mask if mask is None else mask
+    X, W, dY = oracle.from_bf16(case.X), oracle.from_bf16(case.W), oracle.from_bf16(case.dY)
+    Y = oracle.linear_fwd(X, W, m, case.g)
+    dX, dgate = oracle.linear_bwd(dY, X, W, m, case.g)
+    return Y, dX, dgate
+
+
+SHAPES = [  # (T, d_in, d_out, g): several tiles in every dimension plus ragged tails
+    (128, 1024, 1024, 256),   # single masked linear of the smallest workload
+    (77, 320, 200, 64),       # T, d_in and d_out all ragged
+    (300, 1024, 264, 128),
+    (257, 1024, 512, 512),    # a group spans two dgate tiles
+    (33, 2048, 136, 256),
+    (520, 768, 1000, 256),
+]
+
+
+@pytest.mark.parametrize("T,d_in,d_out,g", SHAPES)
+def test_fwd_bwd_parity(T, d_in, d_out, g):
+    say(f"linear fwd+bwd: T={T} d_in={d_in} d_out={d_out} g={g}")
+    case = workloads.make_linear_case((200, T, d_in, d_out, g), T, d_in, d_out, g, None)
+    d = _dev_case(case)
+    Y = _fwd(d, g)
+    dX, dgate = _bwd(d, g)
+    Yr, dXr, dgr = _oracle_all(case)
+    assert_close("Y", host_f64_from_bf16(Y), Yr)
+    assert_close("dX", host_f64_from_bf16(dX), dXr)
+    assert_close("dgate", dgate.cpu().numpy(), dgr)
+
+
+@pytest.mark.parametrize("T,d_in,d_out,g", [(200, 1024, 512, 256), (96, 512, 128, 64)])
+def test_soft_mask_scales_groups(T, d_in, d_out, g):
+    say(f"soft mask: T={T} d_in={d_in} d_out={d_out} g={g}")
+    case = workloads.make_linear_case((201, T), T, d_in, d_out, g, None)
+    r = workloads.gen.rng_for(202, T)
+    soft = r.uniform(0.05, 1.5, size=case.mask.shape).astype(np.float32)
+    soft[r.uniform(size=soft.shape) < 0.4] = 0.0
+    d = _dev_case(case, soft)
+    Y = _fwd(d, g)
+    dX, dgate = _bwd(d, g)
+    Yr, dXr, dgr = _oracle_all(case, soft)
+    assert_close("Y", host_f64_from_bf16(Y), Yr)
+    assert_close("dX", host_f64_from_bf16(dX), dXr)
+    assert_close("dgate", dgate.cpu().numpy(), dgr)
+
+
+def test_all_ones_is_dense_and_all_zeros_is_exact_zero():
+    import torch
+    T, d_in, d_out, g = 256, 1024, 768, 256
+    case = workloads.make_linear_case((203,), T, d_in, d_out, g, None)
+    ones = np.ones_like(case.mask)
+    zeros = np.zeros_like(case.mask)
+    say("all-ones mask")
+    d = _dev_case(case, ones)
+    Y = _fwd(d, g)
+    dX, _ = _bwd(d, g, want_dgate=False)
+    Yr, dXr, _ = _oracle_all(case, ones)
+    assert_close("Y (dense)", host_f64_from_bf16(Y), Yr)
+    assert_close("dX (dense)", host_f64_from_bf16(dX), dXr)
+    # the dense product of the same bf16 values in fp32
+    ref32 = (d["X"].float() @ d["W"].float().t()).cpu().numpy()
+    assert_close("Y vs fp32 dense product", host_f64_from_bf16(Y), ref32)
+    say("all-zeros mask")
+    d = _dev_case(case, zeros)
+    Y = _fwd(d, g)
+    dX, dgate = _bwd(d, g)
+    assert not np.any(host_bits(Y) & 0x7FFF)
+    assert not np.any(host_bits(dX) & 0x7FFF)
+    _, _, dgr = _oracle_all(case, zeros)
+    assert_close("dgate (all pruned)", dgate.cpu().numpy(), dgr)
+    del torch
+
+
+def test_dgate_does_not_depend_on_mask_and_single_outputs():
+    T, d_in, d_out, g = 192, 1024, 512, 128
+    case = workloads.make_linear_case((204,), T, d_in, d_out, g, None)
+    say("dgate mask independence, dgate-only and dX-only calls")
+    d1 = _dev_case(case)
+    d2 = _dev_case(case, np.ones_like(case.mask))
+    _, g1 = _bwd(d1, g)
+    _, g2 = _bwd(d2, g, want_dx=False)
+    assert np.array_equal(g1.cpu().numpy(), g2.cpu().numpy())
+    dX_only, _ = _bwd(d1, g, want_dgate=False)   # dY^T from the standalone transpose
+    dX_both, _ = _bwd(d1, g)                     # dY^T from the dgate side output
+    assert np.array_equal(host_bits(dX_only), host_bits(dX_both))
+
+
+@pytest.mark.parametrize("T", [1, 3, 8, 16])
+@pytest.mark.parametrize("g", [64, 256, 512])
+def test_decode_forward(T, g):
+    d_in, d_out = 2048, 328
+    say(f"decode forward: T={T} g={g}")
+    case = workloads.make_linear_case((205, T, g), T, d_in, d_out, g, None)
+    d = _dev_case(case)
+    Y = _fwd(d, g)
+    Yr, _, _ = _oracle_all(case)
+    assert_close("Y", host_f64_from_bf16(Y), Yr)
+
+
+def _pack(d, g):
+    import torch
+    import paper_2609_33977_amd as gm
+    d_out, d_in = d["W"].shape
+    cap = d_out * (d_in // g)
+    Wp = torch.zeros(cap, g, dtype=torch.bfloat16, device="cuda")
+    chunk = torch.full((cap,), -1, dtype=torch.int32, device="cuda")
+    scale = torch.zeros(cap, dtype=torch.float32, device="cuda")
+    rowptr = torch.zeros(d_out + 1, dtype=torch.int32, device="cuda")
+    gm.gm_pack_rows(d["W"], d["mask"], g, cap, Wp, chunk, scale, rowptr)
+    sync()
+    return Wp, chunk, scale, rowptr
+
+
+@pytest.mark.parametrize("g", [64, 128, 256, 512])
+def test_pack_rows_is_exact(g):
+    d_in, d_out = 2048, 200
+    say(f"pack rows: g={g}")
+    case = workloads.make_linear_case((206, g), 1, d_in, d_out, g, None)
+    soft = case.mask * workloads.gen.rng_for(207, g).uniform(0.5, 1.5, size=case.mask.shape).astype(np.float32)
+    d = _dev_case(case, soft)
+    Wp, chunk, scale, rowptr = _pack(d, g)
+    # expected export, built from the definition (row-major order of the kept groups)
+    keep = soft != 0
+    rp = np.concatenate([[0], np.cumsum(keep.sum(axis=1))]).astype(np.int32)
+    o_idx, v_idx = np.nonzero(keep)
+    k = rp[-1]
+    assert np.array_equal(rowptr.cpu().numpy(), rp)
+    assert np.array_equal(chunk.cpu().numpy()[:k], v_idx.astype(np.int32))
+    assert np.array_equal(scale.cpu().numpy()[:k], soft[o_idx, v_idx])
+    Wg = case.W.reshape(d_out, d_in // g, g)
+    assert np.array_equal(host_bits(Wp)[:k], Wg[o_idx, v_idx])
+
+
+@pytest.mark.parametrize("T", [1, 8, 16, 40])
+def test_packed_forward(T):
+    d_in, d_out, g = 3072, 264, 256
+    import paper_2609_33977_amd as gm
+    say(f"packed forward: T={T}")
+    case = workloads.make_linear_case((208, T), T, d_in, d_out, g, None)
+    d = _dev_case(case)
+    Wp, chunk, scale, rowptr = _pack(d, g)
+    Y = empty_bf16(T, d_out)
+    gm.gm_packed_linear_fwd(d["X"], Wp, chunk, scale, rowptr, d_out, g, Y)
+    sync()
+    Yr, _, _ = _oracle_all(case)
+    assert_close("Y", host_f64_from_bf16(Y), Yr)
+    Y2 = _fwd(d, g)
+    if T <= 16:  # same GEMV kernel over the two layouts: identical results
+        assert np.array_equal(host_bits(Y), host_bits(Y2))
+
+
+def test_workspace_too_small_is_rejected_without_launch():
+    import paper_2609_33977_amd as gm
+    T, d_in, d_out, g = 64, 512, 256, 256
+    case = workloads.make_linear_case((209,), T, d_in, d_out, g, None)
+    d = _dev_case(case)
+    need = gm.gm_workspace_size(gm.GM_OP_BWD, T, d_in, d_out, g)
+    small = workspace(need - 256)
+    dX = empty_bf16(T, d_in)
+    with pytest.raises(gm.GroupMaskError) as ei:
+        gm.gm_masked_linear_bwd(d["dY"], d["X"], d["W"], d["mask"], g, dX, None, small)
+    assert ei.value.status == gm.GM_ERR_WORKSPACE

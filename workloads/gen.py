@@ -10,7 +10,9 @@ import numpy as np
 # stream here is derived from it.
 SEED = 42
 
-_NOISE_BITS = 24  # u = (j + 1/2) / 2^24 is exact in fp32 and never 0 or 1
+# u = (j + 1/2) / 2^23 is a multiple of 2^-24 in (0, 1): exact in fp32, as is 1 - u,
+# and never 0 or 1.
+_NOISE_BITS = 23
 
 
 def _rng(*key: int) -> np.random.Generator:
@@ -30,7 +32,7 @@ def f32_from_bf16_bits(b: np.ndarray) -> np.ndarray:
 
 
 def draw_uniform_noise(rng: np.random.Generator, n: int, half: Optional[str] = None) -> np.ndarray:
-    """Uniform variates u = (j + 1/2) / 2^24, j integer, exact in fp32.
+    """Uniform variates u = (j + 1/2) / 2^23, j integer, exact in fp32.
 
     ``half`` restricts j to the upper ("hi", u > 1/2) or lower ("lo", u < 1/2)
     half of its range; None draws from the whole of (0, 1).
