@@ -52,23 +52,29 @@ gm_status check_linear_shape(int64_t T, int64_t d_in, int64_t d_out, int32_t g) 
 }
 
 // Workspace of the backward, each part 256-byte aligned:
-//   colcount [G_in] int32 | rows [G_in * d_out] int32 | scales [G_in * d_out] fp32 | dYt [d_out * ldt] bf16
+//   colcount [G_in] int32 | colsoft [G_in] int32 | rows [G_in * d_out + 64] int32 |
+//   scales [G_in * d_out + 64] fp32 | dYt [d_out * ldt] bf16
+// The 64 spare entries after the column lists keep the dX kernel's look-ahead
+// reads of the list (up to 31 entries past a column's end) inside the buffer.
 struct BwdLayout {
-  size_t colcount, rows, scales, dyt, total;
+  size_t colcount, colsoft, rows, scales, dyt, total;
   int ldt;
 };
 
 BwdLayout bwd_layout(int64_t T, int64_t d_in, int64_t d_out, int32_t g) {
   BwdLayout L;
   const size_t G_in = size_t(d_in / g);
+  const size_t list = G_in * size_t(d_out) + 64;
   L.ldt = int(round_up(size_t(T), 8));
   size_t off = 0;
   L.colcount = off;
   off = round_up(off + G_in * sizeof(int32_t), 256);
+  L.colsoft = off;
+  off = round_up(off + G_in * sizeof(int32_t), 256);
   L.rows = off;
-  off = round_up(off + G_in * size_t(d_out) * sizeof(int32_t), 256);
+  off = round_up(off + list * sizeof(int32_t), 256);
   L.scales = off;
-  off = round_up(off + G_in * size_t(d_out) * sizeof(float), 256);
+  off = round_up(off + list * sizeof(float), 256);
   L.dyt = off;
   off = round_up(off + size_t(d_out) * size_t(L.ldt) * sizeof(uint16_t), 256);
   L.total = off;
@@ -160,22 +166,21 @@ GM_EXPORT gm_status gm_masked_linear_bwd(const uint16_t* dY, const uint16_t* X, 
   if (gm_status st = check_device()) return st;
 
   const int t = int(T), di = int(d_in), dout = int(d_out), G_in = int(d_in / g);
-  char* base = static_cast<char*>(ws);
-  int* colcount = dX ? reinterpret_cast<int*>(base + L.colcount) : nullptr;
-  int* rows = dX ? reinterpret_cast<int*>(base + L.rows) : nullptr;
-  float* scales = dX ? reinterpret_cast<float*>(base + L.scales) : nullptr;
-  uint16_t* dyt = dX ? reinterpret_cast<uint16_t*>(base + L.dyt) : nullptr;
-
-  if (dX) {
-    if (gm_status st = from_hip(gm::launch_col_lists(mask, dout, G_in, colcount, rows, scales, stream))) return st;
-  }
   if (dgate) {
-    if (gm_status st = from_hip(gm::launch_dgate(dY, X, W, t, di, dout, g, dgate, dyt, L.ldt, stream))) return st;
-  } else {
-    if (gm_status st = from_hip(gm::launch_transpose(dY, t, dout, dyt, L.ldt, stream))) return st;
+    if (gm_status st = from_hip(gm::launch_dgate(dY, X, W, t, di, dout, g, dgate, stream))) return st;
   }
   if (dX) {
-    if (gm_status st = from_hip(gm::launch_dx(dyt, L.ldt, W, colcount, rows, scales, t, di, dout, g, dX, stream)))
+    char* base = static_cast<char*>(ws);
+    int* colcount = reinterpret_cast<int*>(base + L.colcount);
+    int* colsoft = reinterpret_cast<int*>(base + L.colsoft);
+    int* rows = reinterpret_cast<int*>(base + L.rows);
+    float* scales = reinterpret_cast<float*>(base + L.scales);
+    uint16_t* dyt = reinterpret_cast<uint16_t*>(base + L.dyt);
+    if (gm_status st = from_hip(gm::launch_col_lists(mask, dout, G_in, colcount, colsoft, rows, scales, stream)))
+      return st;
+    if (gm_status st = from_hip(gm::launch_transpose(dY, t, dout, dyt, L.ldt, stream))) return st;
+    if (gm_status st = from_hip(gm::launch_dx(dyt, L.ldt, W, colcount, rows, scales, colsoft, t, di, dout, g, dX,
+                                              stream)))
       return st;
   }
   return GM_OK;

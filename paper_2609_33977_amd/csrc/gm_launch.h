@@ -13,8 +13,8 @@ hipError_t launch_gate_fwd(const float* logits, const float* noise, int64_t n, f
 hipError_t launch_gate_bwd(const float* dmask, const float* soft, int64_t n, float tau, float* dlogits,
                            hipStream_t s);
 
-hipError_t launch_col_lists(const float* mask, int d_out, int G_in, int* colcount, int* rows, float* scales,
-                            hipStream_t s);
+hipError_t launch_col_lists(const float* mask, int d_out, int G_in, int* colcount, int* colsoft, int* rows,
+                            float* scales, hipStream_t s);
 hipError_t launch_pack_rows(const uint16_t* W, const float* mask, int d_in, int d_out, int g, int64_t capacity,
                             uint16_t* Wp, int* chunk, float* scale, int* rowptr, hipStream_t s);
 
@@ -27,9 +27,10 @@ int gemv_max_groups_per_row();
 hipError_t launch_fwd(const uint16_t* X, const uint16_t* W, const float* mask, int T, int d_in, int d_out, int g,
                       uint16_t* Y, hipStream_t s);
 hipError_t launch_dgate(const uint16_t* dY, const uint16_t* X, const uint16_t* W, int T, int d_in, int d_out, int g,
-                        float* dgate, uint16_t* dYt, int ldt, hipStream_t s);
+                        float* dgate, hipStream_t s);
 hipError_t launch_transpose(const uint16_t* dY, int T, int d_out, uint16_t* dYt, int ldt, hipStream_t s);
 hipError_t launch_dx(const uint16_t* dYt, int ldt, const uint16_t* W, const int* colcount, const int* rows,
-                     const float* scales, int T, int d_in, int d_out, int g, uint16_t* dX, hipStream_t s);
+                     const float* scales, const int* colsoft, int T, int d_in, int d_out, int g, uint16_t* dX,
+                     hipStream_t s);
 
 }  // namespace gm

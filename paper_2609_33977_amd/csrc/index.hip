@@ -2,7 +2,8 @@
 //
 // Column lists (consumed by the dX GEMM): for every group column v the kept
 // output rows in increasing order, rows[v * d_out + j], with their mask values
-// scales[v * d_out + j] and the count colcount[v].  This is the group-compacted
+// scales[v * d_out + j], the count colcount[v] and colsoft[v] = 1 when some
+// kept value of the column differs from 1.  This is the group-compacted
 // view of W that lets the dX K-loop visit only kept groups.
 //
 // Row-packed export (Appendix F): rowptr / packed values / group column ids,
@@ -15,12 +16,15 @@ namespace gm {
 // One 256-thread block per group column v; scans the rows in blocks of 256 and
 // compacts the kept ones with a wave ballot plus a 4-entry LDS prefix.
 __global__ __launch_bounds__(256) void col_lists_kernel(const float* __restrict__ mask, int d_out, int G_in,
-                                                        int* __restrict__ colcount, int* __restrict__ rows,
-                                                        float* __restrict__ scales) {
+                                                        int* __restrict__ colcount, int* __restrict__ colsoft,
+                                                        int* __restrict__ rows, float* __restrict__ scales) {
   const int v = blockIdx.x;
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   __shared__ int wave_cnt[4];
+  __shared__ int s_soft;
+  if (threadIdx.x == 0) s_soft = 0;
+  __syncthreads();
   int base = 0;
   for (int o0 = 0; o0 < d_out; o0 += 256) {
     const int o = o0 + threadIdx.x;
@@ -35,16 +39,21 @@ __global__ __launch_bounds__(256) void col_lists_kernel(const float* __restrict_
     if (keep) {
       rows[int64_t(v) * d_out + off + rank] = o;
       scales[int64_t(v) * d_out + off + rank] = m;
+      if (m != 1.0f) s_soft = 1;
     }
     base += wave_cnt[0] + wave_cnt[1] + wave_cnt[2] + wave_cnt[3];
     __syncthreads();
   }
-  if (threadIdx.x == 0) colcount[v] = base;
+  if (threadIdx.x == 0) {
+    colcount[v] = base;
+    colsoft[v] = s_soft;
+  }
 }
 
-hipError_t launch_col_lists(const float* mask, int d_out, int G_in, int* colcount, int* rows, float* scales,
-                            hipStream_t s) {
-  hipLaunchKernelGGL(col_lists_kernel, dim3(G_in), dim3(256), 0, s, mask, d_out, G_in, colcount, rows, scales);
+hipError_t launch_col_lists(const float* mask, int d_out, int G_in, int* colcount, int* colsoft, int* rows,
+                            float* scales, hipStream_t s) {
+  hipLaunchKernelGGL(col_lists_kernel, dim3(G_in), dim3(256), 0, s, mask, d_out, G_in, colcount, colsoft, rows,
+                     scales);
   return hipGetLastError();
 }
 
