@@ -115,7 +115,9 @@ gm_status gm_workspace_size(int op, int64_t T, int64_t d_in, int64_t d_out, int3
  *   X    [T, d_in]  bf16       W [d_out, d_in] bf16     mask [d_out, d_in/g] fp32
  *   Y    [T, d_out] bf16, written in full
  *   T >= 1; d_in, d_out >= 1 and multiples of 8; g in {64, 128, 256, 512}
- *   dividing d_in.  Mask values must be finite and >= 0 (not checked).
+ *   dividing d_in, d_in / g <= 512; each of X, W, Y (T rounded up to a
+ *   multiple of 8) below 2^30 - 2^22 elements.  Mask values must be finite
+ *   and >= 0 (not checked).
  *   ws / ws_bytes: workspace of at least gm_workspace_size(GM_OP_FWD, ...)
  *   bytes (ws may be NULL when that size is 0).
  */

@@ -17,6 +17,7 @@ namespace {
 constexpr int64_t kMaxDim = int64_t(1) << 30;  // kernels index rows and columns with 32-bit ints
 constexpr int kMaxGroupCols = 512;             // per-tile group-column list of the forward GEMM
 constexpr int kDecodeTokens = 16;              // forward dispatch: T <= 16 takes the GEMV path
+constexpr int64_t kMaxElems = (int64_t(1) << 30) - (int64_t(1) << 22);  // bf16 elements per matrix (< 2 GiB)
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -48,14 +49,17 @@ gm_status check_linear_shape(int64_t T, int64_t d_in, int64_t d_out, int32_t g) 
   if (g != 64 && g != 128 && g != 256 && g != 512) return GM_ERR_SHAPE;
   if (d_in % g) return GM_ERR_SHAPE;
   if (d_in / g > kMaxGroupCols) return GM_ERR_SHAPE;
+  // The GEMMs address every matrix with 32-bit byte offsets below 2 GiB.
+  const int64_t t8 = (T + 7) / 8 * 8;
+  if (t8 * d_in > kMaxElems || t8 * d_out > kMaxElems || d_out * d_in > kMaxElems) return GM_ERR_SHAPE;
   return GM_OK;
 }
 
 // Workspace of the backward, each part 256-byte aligned:
-//   colcount [G_in] int32 | colsoft [G_in] int32 | rows [G_in * d_out + 64] int32 |
-//   scales [G_in * d_out + 64] fp32 | dYt [d_out * ldt] bf16
-// The 64 spare entries after the column lists keep the dX kernel's look-ahead
-// reads of the list (up to 31 entries past a column's end) inside the buffer.
+//   colcount [G_in] int32 | colsoft [G_in] int32 | rows [G_in * d_out + 128] int32 |
+//   scales [G_in * d_out + 128] fp32 | dYt [d_out * ldt] bf16
+// The 128 spare entries after the column lists keep the dX kernel's look-ahead
+// reads of the list (up to 63 entries past a column's end) inside the buffer.
 struct BwdLayout {
   size_t colcount, colsoft, rows, scales, dyt, total;
   int ldt;
@@ -64,7 +68,7 @@ struct BwdLayout {
 BwdLayout bwd_layout(int64_t T, int64_t d_in, int64_t d_out, int32_t g) {
   BwdLayout L;
   const size_t G_in = size_t(d_in / g);
-  const size_t list = G_in * size_t(d_out) + 64;
+  const size_t list = G_in * size_t(d_out) + 128;
   L.ldt = int(round_up(size_t(T), 8));
   size_t off = 0;
   L.colcount = off;
@@ -166,22 +170,26 @@ GM_EXPORT gm_status gm_masked_linear_bwd(const uint16_t* dY, const uint16_t* X, 
   if (gm_status st = check_device()) return st;
 
   const int t = int(T), di = int(d_in), dout = int(d_out), G_in = int(d_in / g);
-  if (dgate) {
-    if (gm_status st = from_hip(gm::launch_dgate(dY, X, W, t, di, dout, g, dgate, stream))) return st;
-  }
+  char* base = static_cast<char*>(ws);
+  uint16_t* dyt = dX ? reinterpret_cast<uint16_t*>(base + L.dyt) : nullptr;
   if (dX) {
-    char* base = static_cast<char*>(ws);
     int* colcount = reinterpret_cast<int*>(base + L.colcount);
     int* colsoft = reinterpret_cast<int*>(base + L.colsoft);
     int* rows = reinterpret_cast<int*>(base + L.rows);
     float* scales = reinterpret_cast<float*>(base + L.scales);
-    uint16_t* dyt = reinterpret_cast<uint16_t*>(base + L.dyt);
     if (gm_status st = from_hip(gm::launch_col_lists(mask, dout, G_in, colcount, colsoft, rows, scales, stream)))
       return st;
-    if (gm_status st = from_hip(gm::launch_transpose(dY, t, dout, dyt, L.ldt, stream))) return st;
+    // dY^T: a side output of the dgate GEMM, or a transpose pass without it.
+    if (dgate) {
+      if (gm_status st = from_hip(gm::launch_dgate(dY, X, W, t, di, dout, g, dgate, dyt, L.ldt, stream))) return st;
+    } else {
+      if (gm_status st = from_hip(gm::launch_transpose(dY, t, dout, dyt, L.ldt, stream))) return st;
+    }
     if (gm_status st = from_hip(gm::launch_dx(dyt, L.ldt, W, colcount, rows, scales, colsoft, t, di, dout, g, dX,
                                               stream)))
       return st;
+  } else {
+    if (gm_status st = from_hip(gm::launch_dgate(dY, X, W, t, di, dout, g, dgate, nullptr, 0, stream))) return st;
   }
   return GM_OK;
 }

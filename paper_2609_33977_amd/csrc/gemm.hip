@@ -7,26 +7,29 @@
 // Shared machinery (gm_pipe.h): 256 x 256 output tiles (dX: min(g, 256) x 256),
 // four waves of 128 x 128 (dX: g/2 x 128) accumulated in AGPRs with
 // v_mfma_f32_16x16x32_bf16, and a four-stage pipeline of 32-deep K slices
-// copied global -> LDS by global_load_lds (no registers in flight), with one
-// block barrier per slice.  M is always the dimension that is contiguous in
-// the output, so every lane stores 4 adjacent bf16 (8 bytes).
+// copied global -> LDS by buffer loads with the lds modifier (no registers in
+// flight), with one block barrier per slice.  Each lane keeps a fixed 32-bit
+// byte offset per copy; the K advance lives in the scalar buffer resource,
+// and out-of-range offsets read zeros (padding, ragged tails, pruned groups).
+// M is always the dimension that is contiguous in the output, so every lane
+// stores 4 adjacent bf16 (8 bytes).
 //
 // Operand tiles:
 //   fwd   W rows and X rows are K-contiguous: K-major tiles, ds_read_b128.
-//         A pruned group is never read: its DMA lanes copy from a zero chunk.
+//         A pruned group is never read: its copy lanes get an out-of-range offset.
 //         The K-loop visits only group columns that some row of the tile keeps.
 //   dgate X and dY are stored [T, .]: K (= tokens) is the row index, so the
 //         tiles are MN-major and fragments come from ds_read_b64_tr_b16.
 //         Epilogue: the fp32 tile of X^T dY is multiplied by W and summed over
 //         each group in registers and across lanes; dY^T X never reaches HBM.
+//         The transposing reads of dY are 16-byte chunks of dY^T, which the
+//         first row of tiles stores for the dX GEMM.
 //   dX    K = the kept rows of one group column (its column list): whole rows
 //         of W and of dY^T are gathered, MN-major tiles, transposing reads.
 #include "gm_launch.h"
 #include "gm_pipe.h"
 
 namespace gm {
-
-__device__ __attribute__((aligned(16))) uint16_t g_zero_chunk[8];
 
 // Blocks are dealt to the eight XCDs round-robin; renumber them so that each
 // XCD works on a contiguous range of tiles and shares operand panels in its L2.
@@ -44,19 +47,97 @@ __device__ __forceinline__ void zero_acc(f32x4 (&acc)[MB][NB]) {
     for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 }
 
-// One 32-deep K slice: B fragments held, A fragments streamed.
-template <int MB, int NB, bool A_KM, bool B_KM, int CA, int CB>
-__device__ __forceinline__ void mma_slice(const u32x4* __restrict__ As, const u32x4* __restrict__ Bs, int a0, int b0,
-                                          int lane, f32x4 (&acc)[MB][NB]) {
+template <int NB, bool KM, int C>
+__device__ __forceinline__ void load_bfrags(const u32x4* __restrict__ Bs, int b0, int lane, u32x4 (&bf)[NB]) {
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) bf[nb] = KM ? km_frag(Bs, b0 + nb * 16, lane) : mn_frag<C>(Bs, b0 + nb * 16, lane);
+}
+
+template <bool KM, int C>
+__device__ __forceinline__ u32x4 load_afrag(const u32x4* __restrict__ As, int a0, int lane) {
+  return KM ? km_frag(As, a0, lane) : mn_frag<C>(As, a0, lane);
+}
+
+template <int MB, int NB>
+__device__ __forceinline__ void mfma_row(int mb, const u32x4& af, const u32x4 (&bf)[NB], f32x4 (&acc)[MB][NB]) {
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = mfma16x16x32(af, bf[nb], acc[mb][nb]);
+}
+
+// The K-loop shared by the three GEMMs.  `issue(st, p)` starts copy p
+// (0 <= p < PER_STAGE) of K slice st into LDS buffer st % kStages; for
+// st >= nst it must fill zeros without touching memory (a zero-length buffer
+// resource).  `landed(st)` runs after this wave's copies of slice st completed
+// and before the barrier that publishes them (soft-selector rescaling).
+// `bhook(kt, bf)` sees the B fragments of slice kt once they are in registers.
+//
+// Software pipeline: rows 0 .. MB-2 of slice kt run first (A fragments
+// streamed one row ahead); then the wave waits for slice kt+1, meets the
+// others at the barrier (which also frees buffer kt % kStages), and issues the
+// last MFMA row of slice kt interleaved with the copies of slice kt + kStages
+// and the reads of slice kt+1's B fragments into the registers each MFMA has
+// just consumed.  Copies run kStages slices ahead; fragment-read latency and
+// copy issue hide behind MFMA work.  Every iteration issues exactly PER_STAGE
+// copies (slices past the end copy zeros), so the wait count is a constant,
+// and the loop body has no branches around the accumulators; the last slice
+// is peeled off.
+template <int MB, int NB, bool A_KM, bool B_KM, int CA, int CB, int PER_STAGE, int ABUF, int BBUF, class Issue,
+          class Landed, class BHook>
+__device__ __forceinline__ void gemm_mainloop(u32x4 (*As)[ABUF], u32x4 (*Bs)[BBUF], int nst, int a0, int b0, int lane,
+                                              f32x4 (&acc)[MB][NB], Issue&& issue, Landed&& landed, BHook&& bhook) {
+  static_assert(PER_STAGE <= NB, "copies are interleaved with the NB MFMAs of one row");
+  constexpr int AHEAD = PER_STAGE * (kStages - 2);  // copies issued after the slice being waited for
+  if (nst <= 0) return;
+  for (int s = 0; s < kStages - 1; ++s)
+#pragma unroll
+    for (int p = 0; p < PER_STAGE; ++p) issue(s, p);
+  wait_vmcnt<AHEAD>();
+  landed(0);
+  block_sync();
+#pragma unroll
+  for (int p = 0; p < PER_STAGE; ++p) issue(kStages - 1, p);
+
   u32x4 bf[NB];
+  u32x4 af;
+  load_bfrags<NB, B_KM, CB>(Bs[0], b0, lane, bf);
+  af = load_afrag<A_KM, CA>(As[0], a0, lane);
+
+  for (int kt = 0; kt + 1 < nst; ++kt) {
+    bhook(kt, bf);
+    const u32x4* A = As[kt % kStages];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) bf[nb] = B_KM ? km_frag(Bs, b0 + nb * 16, lane) : mn_frag<CB>(Bs, b0 + nb * 16, lane);
+    for (int mb = 0; mb < MB - 1; ++mb) {
+      const u32x4 an = load_afrag<A_KM, CA>(A, a0 + (mb + 1) * 16, lane);
+      mfma_row<MB, NB>(mb, af, bf, acc);
+      af = an;
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's reads of slice kt are done
+    wait_vmcnt<AHEAD>();                                 // ... and its copies of slice kt+1
+    landed(kt + 1);
+    block_sync();
+    const u32x4* Bn = Bs[(kt + 1) % kStages];
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb) {
-    const u32x4 af = A_KM ? km_frag(As, a0 + mb * 16, lane) : mn_frag<CA>(As, a0 + mb * 16, lane);
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = mfma16x16x32(af, bf[nb], acc[mb][nb]);
+    for (int nb = 0; nb < NB; ++nb) {
+      acc[MB - 1][nb] = mfma16x16x32(af, bf[nb], acc[MB - 1][nb]);
+      __builtin_amdgcn_sched_barrier(0);
+      if (nb < PER_STAGE) issue(kt + kStages, nb);
+      bf[nb] = B_KM ? km_frag(Bn, b0 + nb * 16, lane) : mn_frag<CB>(Bn, b0 + nb * 16, lane);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    af = load_afrag<A_KM, CA>(As[(kt + 1) % kStages], a0, lane);
   }
+  {
+    bhook(nst - 1, bf);
+    const u32x4* A = As[(nst - 1) % kStages];
+#pragma unroll
+    for (int mb = 0; mb < MB - 1; ++mb) {
+      const u32x4 an = load_afrag<A_KM, CA>(A, a0 + (mb + 1) * 16, lane);
+      mfma_row<MB, NB>(mb, af, bf, acc);
+      af = an;
+    }
+    mfma_row<MB, NB>(MB - 1, af, bf, acc);
+  }
+  wait_vmcnt<0>();  // zero-fill copies of slices past the end, before the block exits
 }
 
 // Store 4 adjacent bf16 (rows m .. m+3 of the MFMA tile = consecutive output columns).
@@ -97,7 +178,10 @@ __global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X
 
   // Prologue: kept bits of every row of the tile, the columns some row keeps, soft values.
   if (tid < MAXG / 32) s_any[tid] = 0;
-  if (tid == 0) s_soft = 0;
+  if (tid == 0) {
+    s_soft = 0;
+    s_cols[0] = 0;  // read (unused) by the zero-fill copies when no column is kept
+  }
   __syncthreads();
   {
     const int o = m0 + tid;
@@ -131,22 +215,41 @@ __global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X
   const int nst = s_ncols * SUB;
   const bool soft = s_soft != 0;
 
-  // This lane's four DMA rows (the same in both tiles): row = 16 (4 wave + j) + lane / 4.
-  auto issue = [&](int st) {
-    const int v = s_cols[st / SUB];
-    const int k0 = v * G + (st % SUB) * kBK;
-    u32x4* A = As[st % kStages];
-    u32x4* B = Bs[st % kStages];
+  // This lane's four DMA rows (the same in both tiles): row = 16 (4 wave + j) + lane / 4,
+  // and their byte offsets within a K slice (out-of-range rows read zeros).
+  uint32_t offA[4], offB[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int b = wave * 4 + j;
-      int row, c;
-      km_dma_target(b * 64 + lane, row, c);
-      const int o = m0 + row;
-      const bool kept = o < d_out && ((s_bits[row][v >> 5] >> (v & 31)) & 1);
-      dma16(kept ? static_cast<const void*>(W + int64_t(o) * d_in + k0 + 8 * c) : g_zero_chunk, A + b * 64);
-      const int t = n0 + row;
-      dma16(t < T ? static_cast<const void*>(X + int64_t(t) * d_in + k0 + 8 * c) : g_zero_chunk, B + b * 64);
+  for (int j = 0; j < 4; ++j) {
+    int row, c;
+    km_dma_target((wave * 4 + j) * 64 + lane, row, c);
+    offA[j] = uint32_t((m0 + row) * d_in + 8 * c) * 2u;
+    offB[j] = uint32_t((n0 + row) * d_in + 8 * c) * 2u;
+  }
+  const uint32_t bytesW = uint32_t(d_out) * uint32_t(d_in) * 2u;
+  const uint32_t bytesX = uint32_t(T) * uint32_t(d_in) * 2u;
+  uint32_t keptA = 0;  // bit j: row j of this lane keeps the current group column
+  auto issue = [&](int st, int p) {
+    const bool live = st < nst;
+    const int v = s_cols[live ? st / SUB : 0];
+    const int k0 = live ? v * G + (st % SUB) * kBK : 0;
+    if (p == 0) {
+      keptA = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        int row, c;
+        km_dma_target((wave * 4 + j) * 64 + lane, row, c);
+        keptA |= ((s_bits[row][v >> 5] >> (v & 31)) & 1u) << j;
+      }
+    }
+    // copies 0..3 fill this wave's four row blocks of the W tile, 4..7 of the X tile
+    const int j = p & 3;
+    const int b = wave * 4 + j;
+    if (p < 4) {
+      const i32x4_t rA = make_rsrc(W + k0, live ? bytesW - 2u * uint32_t(k0) : 0u);
+      dma16_buf(rA, ((keptA >> j) & 1u) ? offA[j] : kOOB, As[st % kStages] + b * 64);
+    } else {
+      const i32x4_t rB = make_rsrc(X + k0, live ? bytesX - 2u * uint32_t(k0) : 0u);
+      dma16_buf(rB, offB[j], Bs[st % kStages] + b * 64);
     }
   };
   // Soft selectors: scale this lane's freshly landed W chunks by their mask value.
@@ -166,22 +269,17 @@ __global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X
       u32x4* p = A + (wave * 4 + j) * 64 + lane;
       if (m[j] != 0.0f && m[j] != 1.0f) *p = scale_bf16x8(*p, m[j]);
     }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   };
 
   f32x4 acc[MB][NB];
   zero_acc(acc);
-  for (int s = 0; s < kStages - 1; ++s)
-    if (s < nst) issue(s);
-  for (int kt = 0; kt < nst; ++kt) {
-    wait_stages<PER_STAGE>(min(kStages - 2, nst - 1 - kt));
-    if (soft) {
-      rescale(kt);
-      __syncthreads();
-    }
-    block_sync();
-    if (kt + kStages - 1 < nst) issue(kt + kStages - 1);
-    mma_slice<MB, NB, true, true, 0, 0>(As[kt % kStages], Bs[kt % kStages], wm * 128, wn * 128, lane, acc);
-  }
+  gemm_mainloop<MB, NB, true, true, 0, 0, PER_STAGE>(
+      As, Bs, nst, wm * 128, wn * 128, lane, acc, issue,
+      [&](int st) {
+        if (soft) rescale(st);
+      },
+      [](int, const u32x4(&)[NB]) {});
 
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
@@ -202,7 +300,7 @@ __global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X
 template <int G>
 __global__ __launch_bounds__(256) void dgate_kernel(const uint16_t* __restrict__ dY, const uint16_t* __restrict__ X,
                                                     const uint16_t* __restrict__ W, int T, int d_in, int d_out,
-                                                    float* __restrict__ dgate) {
+                                                    float* __restrict__ dgate, uint16_t* __restrict__ dYt, int ldt) {
   constexpr int BM = 256, BN = 256, MB = 8, NB = 8;
   constexpr int PER_STAGE = 8;
   __shared__ u32x4 As[kStages][kBK * BM / 8];
@@ -219,32 +317,54 @@ __global__ __launch_bounds__(256) void dgate_kernel(const uint16_t* __restrict__
   const int m0 = tm * BM, n0 = tn * BN;
   const int nst = (T + kBK - 1) / kBK;
 
-  auto issue = [&](int st) {
-    const int k0 = st * kBK;
-    u32x4* A = As[st % kStages];
-    u32x4* B = Bs[st % kStages];
+  // Byte offsets of this lane's DMA chunks within a K slice (columns past the
+  // matrix read zeros; rows past T fall outside the slice's range).
+  uint32_t offA[4], offB[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int b = wave * 4 + j;
-      int row, c;
-      mn_dma_target<256>(b * 64 + lane, row, c);
-      const int t = k0 + row;
-      const int i = m0 + 8 * c, o = n0 + 8 * c;
-      dma16(t < T && i < d_in ? static_cast<const void*>(X + int64_t(t) * d_in + i) : g_zero_chunk, A + b * 64);
-      dma16(t < T && o < d_out ? static_cast<const void*>(dY + int64_t(t) * d_out + o) : g_zero_chunk, B + b * 64);
+  for (int j = 0; j < 4; ++j) {
+    int row, c;
+    mn_dma_target<256>((wave * 4 + j) * 64 + lane, row, c);
+    offA[j] = m0 + 8 * c < d_in ? uint32_t(row * d_in + m0 + 8 * c) * 2u : kOOB;
+    offB[j] = n0 + 8 * c < d_out ? uint32_t(row * d_out + n0 + 8 * c) * 2u : kOOB;
+  }
+  const uint32_t bytesX = uint32_t(T) * uint32_t(d_in) * 2u;
+  const uint32_t bytesY = uint32_t(T) * uint32_t(d_out) * 2u;
+  auto issue = [&](int st, int p) {
+    const bool live = st < nst;
+    const int k0 = live ? st * kBK : 0;
+    const int j = p & 3;
+    const int b = wave * 4 + j;
+    if (p < 4) {
+      const i32x4_t rA =
+          make_rsrc(X + int64_t(k0) * d_in, live ? bytesX - uint32_t(k0) * uint32_t(d_in) * 2u : 0u);
+      dma16_buf(rA, offA[j], As[st % kStages] + b * 64);
+    } else {
+      const i32x4_t rB =
+          make_rsrc(dY + int64_t(k0) * d_out, live ? bytesY - uint32_t(k0) * uint32_t(d_out) * 2u : 0u);
+      dma16_buf(rB, offB[j], Bs[st % kStages] + b * 64);
+    }
+  };
+
+  // dY^T side output (for the dX GEMM): lane (G, i) of a B fragment holds
+  // dY[k0 + 8 G .. k0 + 8 G + 7, o] for o = n0 + wn*128 + nb*16 + i, which is a
+  // 16-byte chunk of row o of dY^T.  The tiles sharing this dY panel split
+  // the slices between them (slice kt goes to tile row kt * tiles_m / nst), and
+  // within a tile the two wave rows, which hold the same B fragments, alternate.
+  auto bhook = [&](int kt, const u32x4(&bf)[NB]) {
+    if (dYt == nullptr || (kt * tiles_m) / nst != tm || (kt & 1) != wm) return;
+    const int t = kt * kBK + 8 * (lane >> 4);
+    if (t >= ldt) return;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int o = n0 + wn * 128 + nb * 16 + (lane & 15);
+      if (o < d_out) st16(dYt + int64_t(o) * ldt + t, bf[nb]);
     }
   };
 
   f32x4 acc[MB][NB];
   zero_acc(acc);
-  for (int s = 0; s < kStages - 1; ++s)
-    if (s < nst) issue(s);
-  for (int kt = 0; kt < nst; ++kt) {
-    wait_stages<PER_STAGE>(min(kStages - 2, nst - 1 - kt));
-    block_sync();
-    if (kt + kStages - 1 < nst) issue(kt + kStages - 1);
-    mma_slice<MB, NB, false, false, BM, BN>(As[kt % kStages], Bs[kt % kStages], wm * 128, wn * 128, lane, acc);
-  }
+  gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE>(As, Bs, nst, wm * 128, wn * 128, lane, acc, issue,
+                                                        [](int) {}, bhook);
 
   // Epilogue.  Lane (l >> 4, l & 15) holds, for every (mb, nb), rows
   // i = i0 .. i0 + 3 of column o: W[o, i0 .. i0 + 3] is one 8-byte load.
@@ -348,38 +468,36 @@ __global__ __launch_bounds__(256) void dx_kernel(const uint16_t* __restrict__ dY
 
   // Slice st uses k-rows st*32 + r; this wave gathers rows r = 8 wave .. 8 wave + 7.
   int idx[8];
-  auto load_idx = [&](int st) {
+  auto load_idx = [&](int st) {  // st <= nst: at most 31 + 32 entries past the column's end
     const int base = st * kBK + wave * 8;
 #pragma unroll
     for (int q = 0; q < 8; ++q) idx[q] = rl[base + q];  // uniform: scalar loads
   };
-  auto issue = [&](int st) {
-    const int k0 = st * kBK;
-    u32x4* A = As[st % kStages];
-    u32x4* B = Bs[st % kStages];
+  // The gathered k-row of a DMA lane is one of the wave's eight list entries:
+  // instruction j of a tile with CPR chunks per row covers rows
+  // 8 wave + j*64/CPR + lane/CPR.
+  auto row_index = [&](int q) {
+    int o = idx[0];
 #pragma unroll
-    for (int j = 0; j < NA; ++j) {
-      const int b = wave * NA + j;
+    for (int p = 1; p < 8; ++p) o = q == p ? idx[p] : o;
+    return o;
+  };
+  const i32x4_t rA = make_rsrc(W + m0, (uint32_t(d_out) * uint32_t(d_in) - uint32_t(m0)) * 2u);
+  const i32x4_t rB = make_rsrc(dYt + n0, (uint32_t(d_out) * uint32_t(ldt) - uint32_t(n0)) * 2u);
+  auto issue = [&](int st, int p) {  // copies 0 .. NA-1: W tile, NA .. NA+3: dY^T tile
+    const int k0 = st * kBK;          // slices past the end: every k0 + row >= kv reads zeros
+    if (p < NA) {
+      const int b = wave * NA + p;
       int row, c;
       mn_dma_target<BM>(b * 64 + lane, row, c);
-      const int q = row & 7;
-      int o = idx[0];
-#pragma unroll
-      for (int p = 1; p < 8; ++p) o = q == p ? idx[p] : o;
-      const bool ok = k0 + row < kv;
-      dma16(ok ? static_cast<const void*>(W + int64_t(o) * d_in + m0 + 8 * c) : g_zero_chunk, A + b * 64);
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int b = wave * 4 + j;
+      const uint32_t off = uint32_t(row_index(row & 7) * d_in + 8 * c) * 2u;
+      dma16_buf(rA, k0 + row < kv ? off : kOOB, As[st % kStages] + b * 64);
+    } else {
+      const int b = wave * 4 + (p - NA);
       int row, c;
       mn_dma_target<BN>(b * 64 + lane, row, c);
-      const int q = row & 7;
-      int o = idx[0];
-#pragma unroll
-      for (int p = 1; p < 8; ++p) o = q == p ? idx[p] : o;
-      const bool ok = k0 + row < kv && n0 + 8 * c < ldt;
-      dma16(ok ? static_cast<const void*>(dYt + int64_t(o) * ldt + n0 + 8 * c) : g_zero_chunk, B + b * 64);
+      const uint32_t off = uint32_t(row_index(row & 7) * ldt + 8 * c) * 2u;
+      dma16_buf(rB, k0 + row < kv && n0 + 8 * c < ldt ? off : kOOB, Bs[st % kStages] + b * 64);
     }
   };
   // Soft selectors: scale this lane's landed W chunks by the row's mask value.
@@ -397,30 +515,21 @@ __global__ __launch_bounds__(256) void dx_kernel(const uint16_t* __restrict__ dY
         if (s != 1.0f) *p = scale_bf16x8(*p, s);
       }
     }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   };
 
   f32x4 acc[MB][NB];
   zero_acc(acc);
-  for (int s = 0; s < kStages - 1; ++s)
-    if (s < nst) {
-      load_idx(s);
-      issue(s);
-    }
-  if (kStages - 1 < nst) load_idx(kStages - 1);
-  for (int kt = 0; kt < nst; ++kt) {
-    wait_stages<PER_STAGE>(min(kStages - 2, nst - 1 - kt));
-    if (soft) {
-      rescale(kt);
-      __syncthreads();
-    }
-    block_sync();
-    if (kt + kStages - 1 < nst) {
-      issue(kt + kStages - 1);
-      if (kt + kStages < nst) load_idx(kt + kStages);
-    }
-    mma_slice<MB, NB, false, false, BM, BN>(As[kt % kStages], Bs[kt % kStages], wm * (BM / 2), wn * 128, lane,
-                                            acc);
-  }
+  gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE>(As, Bs, nst, wm * (BM / 2), wn * 128, lane, acc,
+                                                        [&](int st, int p) {  // slices are issued in order
+                                                          if (p == 0 && st == 0) load_idx(0);
+                                                          issue(st, p);
+                                                          if (p == PER_STAGE - 1) load_idx(min(st + 1, nst));
+                                                        },
+                                                        [&](int st) {
+                                                          if (soft) rescale(st);
+                                                        },
+                                                        [](int, const u32x4(&)[NB]) {});
 
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
@@ -473,7 +582,7 @@ hipError_t launch_fwd(const uint16_t* X, const uint16_t* W, const float* mask, i
 }
 
 hipError_t launch_dgate(const uint16_t* dY, const uint16_t* X, const uint16_t* W, int T, int d_in, int d_out, int g,
-                        float* dgate, hipStream_t s) {
+                        float* dgate, uint16_t* dYt, int ldt, hipStream_t s) {
   const int tiles = ((d_out + 255) / 256) * ((d_in + 255) / 256);
   if (g == 512) {
     const int64_t n = int64_t(d_out) * (d_in / g);
@@ -482,7 +591,7 @@ hipError_t launch_dgate(const uint16_t* dY, const uint16_t* X, const uint16_t* W
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  GM_LAUNCH_G(dgate_kernel, tiles, dY, X, W, T, d_in, d_out, dgate)
+  GM_LAUNCH_G(dgate_kernel, tiles, dY, X, W, T, d_in, d_out, dgate, dYt, ldt)
   return hipGetLastError();
 }
 

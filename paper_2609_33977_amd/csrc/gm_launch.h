@@ -27,7 +27,7 @@ int gemv_max_groups_per_row();
 hipError_t launch_fwd(const uint16_t* X, const uint16_t* W, const float* mask, int T, int d_in, int d_out, int g,
                       uint16_t* Y, hipStream_t s);
 hipError_t launch_dgate(const uint16_t* dY, const uint16_t* X, const uint16_t* W, int T, int d_in, int d_out, int g,
-                        float* dgate, hipStream_t s);
+                        float* dgate, uint16_t* dYt, int ldt, hipStream_t s);
 hipError_t launch_transpose(const uint16_t* dY, int T, int d_out, uint16_t* dYt, int ldt, hipStream_t s);
 hipError_t launch_dx(const uint16_t* dYt, int ldt, const uint16_t* W, const int* colcount, const int* rows,
                      const float* scales, const int* colsoft, int T, int d_in, int d_out, int g, uint16_t* dX,

@@ -10,10 +10,6 @@ namespace gm {
 typedef __attribute__((address_space(3))) void lds_void;
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 
-// Sixteen zero bytes in global memory: the source of every DMA lane whose
-// element lies outside the matrix or belongs to a pruned group.
-extern __device__ __attribute__((aligned(16))) uint16_t g_zero_chunk[8];
-
 // Pipeline depth (LDS stages) and K per stage.
 constexpr int kStages = 4;
 constexpr int kBK = 32;
@@ -24,14 +20,43 @@ constexpr int kBK = 32;
 // compiler does not add conservative waits for it; completion is tracked
 // with wait_vmcnt() and made visible to the block with block_sync().  M0
 // needs one wait state after it is written.  M0 is a reserved register the
-// compiler cannot be told about; the kernels that use this helper have no
+// compiler cannot be told about; the kernels that use these helpers have no
 // other M0 reader (no GDS, message, move-relative or compiler-issued LDS DMA
-// instructions), which the build's assembly check confirms.
+// instructions).
 __device__ __forceinline__ void dma16(const void* gsrc, const void* lds_wave_base) {
   const uint32_t l = uint32_t(reinterpret_cast<uintptr_t>((lds_void*)lds_wave_base));
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
                :
                : "v"(gsrc), "s"(__builtin_amdgcn_readfirstlane(l))
+               : "memory");
+}
+
+// Buffer resource over a byte range [base, base + bytes): loads at offsets
+// outside it return zeros, which is how the kernels read padding, ragged
+// tails and pruned groups without branches.
+typedef int32_t i32x4_t __attribute__((ext_vector_type(4)));
+constexpr uint32_t kOOB = 0x80000000u;  // an offset past every range (ranges stay below 2 GiB)
+
+__device__ __forceinline__ i32x4_t make_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  i32x4_t r;
+  r[0] = int32_t(uint32_t(b));
+  r[1] = int32_t(uint32_t(b >> 32) & 0xffffu);  // stride 0: raw byte buffer
+  r[2] = int32_t(bytes);
+  r[3] = 0x00020000;
+  r[0] = __builtin_amdgcn_readfirstlane(r[0]);
+  r[1] = __builtin_amdgcn_readfirstlane(r[1]);
+  r[2] = __builtin_amdgcn_readfirstlane(r[2]);
+  return r;
+}
+
+// buffer_load_dwordx4 ... offen lds: 16 bytes at rsrc + voffset into LDS at
+// lds_wave_base + 16 lane (zeros when voffset is out of the resource's range).
+__device__ __forceinline__ void dma16_buf(i32x4_t rsrc, uint32_t voffset, const void* lds_wave_base) {
+  const uint32_t l = uint32_t(reinterpret_cast<uintptr_t>((lds_void*)lds_wave_base));
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+               :
+               : "v"(voffset), "s"(rsrc), "s"(__builtin_amdgcn_readfirstlane(l))
                : "memory");
 }
 
@@ -62,15 +87,19 @@ __device__ __forceinline__ void block_sync() {
 
 // ---------------------------------------------------------------- K-major tile
 // R rows x 32 k, 64 bytes per row.  16-byte chunk c (k = 8c .. 8c+7) of row r
-// sits at slot 4 r + (c ^ ((r >> 1) & 3)): eight consecutive rows read at one
-// chunk cover all banks.
+// sits at slot 4 r + (c ^ ((r >> 2) & 3)).  The LDS has 64 banks (256 bytes):
+// rows r .. r+3 at one chunk already fall on four different bank quarters, and
+// the XOR with bits 2-3 of the row moves rows 4 apart to other chunks, so the
+// 16 rows that one fragment read touches cover all banks once.  The XOR term
+// depends only on the row within its 16-row fragment, so fragment addresses
+// are a per-lane base plus compile-time offsets.
 
-__device__ __forceinline__ int km_slot(int row, int chunk) { return row * 4 + (chunk ^ ((row >> 1) & 3)); }
+__device__ __forceinline__ int km_slot(int row, int chunk) { return row * 4 + (chunk ^ ((row >> 2) & 3)); }
 
 // DMA slot s of the tile (s = 64 b + lane) -> (row, logical chunk).
 __device__ __forceinline__ void km_dma_target(int s, int& row, int& chunk) {
   row = s >> 2;
-  chunk = (s & 3) ^ ((row >> 1) & 3);
+  chunk = (s & 3) ^ ((row >> 2) & 3);
 }
 
 // MFMA fragment (8 consecutive k of one row) for lane l: row0 + (l & 15), k-chunk l >> 4.

@@ -13,20 +13,20 @@
 
 namespace gm {
 
-// One 256-thread block per group column v; scans the rows in blocks of 256 and
-// compacts the kept ones with a wave ballot plus a 4-entry LDS prefix.
-__global__ __launch_bounds__(256) void col_lists_kernel(const float* __restrict__ mask, int d_out, int G_in,
+// One 1024-thread block per group column v; scans the rows in blocks of 1024
+// and compacts the kept ones with a wave ballot plus a 16-entry LDS prefix.
+__global__ __launch_bounds__(1024) void col_lists_kernel(const float* __restrict__ mask, int d_out, int G_in,
                                                         int* __restrict__ colcount, int* __restrict__ colsoft,
                                                         int* __restrict__ rows, float* __restrict__ scales) {
   const int v = blockIdx.x;
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
-  __shared__ int wave_cnt[4];
+  __shared__ int wave_cnt[16];
   __shared__ int s_soft;
   if (threadIdx.x == 0) s_soft = 0;
   __syncthreads();
   int base = 0;
-  for (int o0 = 0; o0 < d_out; o0 += 256) {
+  for (int o0 = 0; o0 < d_out; o0 += 1024) {
     const int o = o0 + threadIdx.x;
     const float m = o < d_out ? mask[int64_t(o) * G_in + v] : 0.0f;
     const bool keep = m != 0.0f;
@@ -41,7 +41,7 @@ __global__ __launch_bounds__(256) void col_lists_kernel(const float* __restrict_
       scales[int64_t(v) * d_out + off + rank] = m;
       if (m != 1.0f) s_soft = 1;
     }
-    base += wave_cnt[0] + wave_cnt[1] + wave_cnt[2] + wave_cnt[3];
+    for (int q = 0; q < 16; ++q) base += wave_cnt[q];
     __syncthreads();
   }
   if (threadIdx.x == 0) {
@@ -52,7 +52,7 @@ __global__ __launch_bounds__(256) void col_lists_kernel(const float* __restrict_
 
 hipError_t launch_col_lists(const float* mask, int d_out, int G_in, int* colcount, int* colsoft, int* rows,
                             float* scales, hipStream_t s) {
-  hipLaunchKernelGGL(col_lists_kernel, dim3(G_in), dim3(256), 0, s, mask, d_out, G_in, colcount, colsoft, rows,
+  hipLaunchKernelGGL(col_lists_kernel, dim3(G_in), dim3(1024), 0, s, mask, d_out, G_in, colcount, colsoft, rows,
                      scales);
   return hipGetLastError();
 }
