@@ -32,11 +32,26 @@
 namespace gm {
 
 // Blocks are dealt to the eight XCDs round-robin; renumber them so that each
-// XCD works on a contiguous range of tiles and shares operand panels in its L2.
+// XCD works on a contiguous range of tile indices, then walk the tile grid in
+// groups of kGroupM tile rows (column-major inside a group): an XCD's range is
+// then a kGroupM-row rectangle of tiles, which shares both operand panels in
+// its L2 instead of streaming every panel of one operand.
+constexpr int kGroupM = 4;
+
 __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
   const int per = nblocks / 8;
   if (per == 0 || bid >= per * 8) return bid;
   return (bid % 8) * per + bid / 8;
+}
+
+__device__ __forceinline__ void tile_coords(int nblocks, int tiles_m, int tiles_n, int& tm, int& tn) {
+  const int t = xcd_remap(blockIdx.x, nblocks);
+  const int group = t / (kGroupM * tiles_n);
+  const int first_m = group * kGroupM;
+  const int gm = min(tiles_m - first_m, kGroupM);
+  const int r = t - group * kGroupM * tiles_n;
+  tm = first_m + r % gm;
+  tn = r / gm;
 }
 
 template <int MB, int NB>
@@ -171,9 +186,9 @@ __global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X
   const int wm = wave >> 1, wn = wave & 1;
   const int G_in = d_in / G;
   const int words = (G_in + 31) / 32;
-  const int tiles_m = (d_out + BM - 1) / BM;
-  const int bid = xcd_remap(blockIdx.x, gridDim.x);
-  const int tm = bid % tiles_m, tn = bid / tiles_m;  // consecutive blocks share the X panel
+  const int tiles_m = (d_out + BM - 1) / BM, tiles_n = (T + BN - 1) / BN;
+  int tm, tn;
+  tile_coords(gridDim.x, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
 
   // Prologue: kept bits of every row of the tile, the columns some row keeps, soft values.
@@ -311,9 +326,9 @@ __global__ __launch_bounds__(256) void dgate_kernel(const uint16_t* __restrict__
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   const int G_in = d_in / G;
-  const int tiles_m = (d_in + BM - 1) / BM;
-  const int bid = xcd_remap(blockIdx.x, gridDim.x);
-  const int tm = bid % tiles_m, tn = bid / tiles_m;
+  const int tiles_m = (d_in + BM - 1) / BM, tiles_n = (d_out + BN - 1) / BN;
+  int tm, tn;
+  tile_coords(gridDim.x, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int nst = (T + kBK - 1) / kBK;
 
@@ -455,9 +470,9 @@ __global__ __launch_bounds__(256) void dx_kernel(const uint16_t* __restrict__ dY
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
-  const int tiles_m = d_in / BM;
-  const int bid = xcd_remap(blockIdx.x, gridDim.x);
-  const int tm = bid % tiles_m, tn = bid / tiles_m;
+  const int tiles_m = d_in / BM, tiles_n = (T + BN - 1) / BN;
+  int tm, tn;
+  tile_coords(gridDim.x, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int v = m0 / g;
   const int kv = colcount[v];

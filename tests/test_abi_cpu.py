@@ -38,9 +38,12 @@ def test_abi_version_and_status_strings():
 
 def test_workspace_size_host_only():
     ws = gm.gm_workspace_size(gm.GM_OP_BWD, 4096, 4096, 4096, 256)
-    # col counts + row lists + scales + dY^T, each part rounded to 256 bytes
+    # per-column counts and soft flags, then row lists and scales (each with
+    # 128 entries of look-ahead padding), then dY^T; every part rounded up to
+    # 256 bytes
     G_in = 4096 // 256
-    expect = 256 + 2 * (G_in * 4096 * 4) + 4096 * 4096 * 2
+    r256 = lambda x: (x + 255) // 256 * 256
+    expect = 2 * r256(G_in * 4) + 2 * r256((G_in * 4096 + 128) * 4) + r256(4096 * 4096 * 2)
     assert ws == expect
     assert gm.gm_workspace_size(gm.GM_OP_FWD, 4096, 4096, 4096, 256) == 0
     # ragged T: dY^T rows padded to a multiple of 8 tokens
