@@ -79,12 +79,16 @@ __device__ __forceinline__ void mfma_row(int mb, const u32x4& af, const u32x4 (&
   for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = mfma16x16x32(af, bf[nb], acc[mb][nb]);
 }
 
-// The K-loop shared by the three GEMMs.  `issue(st, p)` starts copy p
-// (0 <= p < PER_STAGE) of K slice st into LDS buffer st % kStages; for
-// st >= nst it must fill zeros without touching memory (a zero-length buffer
-// resource).  `landed(st)` runs after this wave's copies of slice st completed
-// and before the barrier that publishes them (soft-selector rescaling).
-// `bhook(kt, bf)` sees the B fragments of slice kt once they are in registers.
+// The K-loop shared by the three GEMMs.  `prepare(st)` computes whatever the
+// copies of K slice st need (buffer resources, per-lane offsets); it is called
+// once per slice, in increasing st, at a point where this wave has no LDS read
+// in flight, so any LDS or scalar loads it makes cost only their own latency.
+// `issue(st, p)` then starts copy p (0 <= p < PER_STAGE) of slice st into LDS
+// buffer st % kStages; slices st >= nst are never consumed, so their copies
+// only need to stay inside their buffer resources.  `landed(st)` runs after
+// this wave's copies of slice st completed and before the barrier that
+// publishes them (soft-selector rescaling).  `bhook(kt, bf)` sees the B
+// fragments of slice kt once they are in registers.
 //
 // Software pipeline: rows 0 .. MB-2 of slice kt run first (A fragments
 // streamed one row ahead); then the wave waits for slice kt+1, meets the
@@ -96,16 +100,20 @@ __device__ __forceinline__ void mfma_row(int mb, const u32x4& af, const u32x4 (&
 // copies (slices past the end copy zeros), so the wait count is a constant,
 // and the loop body has no branches around the accumulators; the last slice
 // is peeled off.
-template <int MB, int NB, bool A_KM, bool B_KM, int CA, int CB, int PER_STAGE, int ABUF, int BBUF, class Issue,
-          class Landed, class BHook>
+template <int MB, int NB, bool A_KM, bool B_KM, int CA, int CB, int PER_STAGE, int ABUF, int BBUF, class Prepare,
+          class Issue, class Landed, class BHook>
 __device__ __forceinline__ void gemm_mainloop(u32x4 (*As)[ABUF], u32x4 (*Bs)[BBUF], int nst, int a0, int b0, int lane,
-                                              f32x4 (&acc)[MB][NB], Issue&& issue, Landed&& landed, BHook&& bhook) {
+                                              f32x4 (&acc)[MB][NB], Prepare&& prepare, Issue&& issue,
+                                              Landed&& landed, BHook&& bhook) {
   static_assert(PER_STAGE <= NB, "copies are interleaved with the NB MFMAs of one row");
   constexpr int AHEAD = PER_STAGE * (kStages - 2);  // copies issued after the slice being waited for
   if (nst <= 0) return;
-  for (int s = 0; s < kStages - 1; ++s)
+  for (int s = 0; s < kStages - 1; ++s) {
+    prepare(s);
 #pragma unroll
     for (int p = 0; p < PER_STAGE; ++p) issue(s, p);
+  }
+  prepare(kStages - 1);
   wait_vmcnt<AHEAD>();
   landed(0);
   block_sync();
@@ -127,6 +135,7 @@ __device__ __forceinline__ void gemm_mainloop(u32x4 (*As)[ABUF], u32x4 (*Bs)[BBU
       af = an;
     }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's reads of slice kt are done
+    prepare(kt + kStages);
     wait_vmcnt<AHEAD>();                                 // ... and its copies of slice kt+1
     landed(kt + 1);
     block_sync();
@@ -228,44 +237,55 @@ __global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X
   }
   __syncthreads();
   const int nst = s_ncols * SUB;
-  const bool soft = s_soft != 0;
 
   // This lane's four DMA rows (the same in both tiles): row = 16 (4 wave + j) + lane / 4,
   // and their byte offsets within a K slice (out-of-range rows read zeros).
+  int rowj[4];
   uint32_t offA[4], offB[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    int row, c;
-    km_dma_target((wave * 4 + j) * 64 + lane, row, c);
-    offA[j] = uint32_t((m0 + row) * d_in + 8 * c) * 2u;
-    offB[j] = uint32_t((n0 + row) * d_in + 8 * c) * 2u;
+    int c;
+    km_dma_target((wave * 4 + j) * 64 + lane, rowj[j], c);
+    offA[j] = uint32_t((m0 + rowj[j]) * d_in + 8 * c) * 2u;
+    offB[j] = uint32_t((n0 + rowj[j]) * d_in + 8 * c) * 2u;
   }
   const uint32_t bytesW = uint32_t(d_out) * uint32_t(d_in) * 2u;
   const uint32_t bytesX = uint32_t(T) * uint32_t(d_in) * 2u;
-  uint32_t keptA = 0;  // bit j: row j of this lane keeps the current group column
-  auto issue = [&](int st, int p) {
-    const bool live = st < nst;
-    const int v = s_cols[live ? st / SUB : 0];
-    const int k0 = live ? v * G + (st % SUB) * kBK : 0;
-    if (p == 0) {
-      keptA = 0;
+
+  // Per-slice copy state, set by prepare(): the buffer resources of the
+  // slice's K range and the W offsets for its group column (pruned rows get
+  // an out-of-range offset).  prepare() has no branches: the column of the
+  // next slice and the kept bits of this lane's rows for it are read from LDS
+  // one slice ahead, so their latency is hidden.
+  const uint32_t ldsA = lds_addr(As), ldsB = lds_addr(Bs);
+  auto col_of = [&](int st) { return st < nst ? st / SUB : 0; };  // slices past the end reuse column 0
+  int v_cur = __builtin_amdgcn_readfirstlane(s_cols[0]);
+  int v_nxt = __builtin_amdgcn_readfirstlane(s_cols[col_of(1)]);
+  uint32_t bits_cur[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        int row, c;
-        km_dma_target((wave * 4 + j) * 64 + lane, row, c);
-        keptA |= ((s_bits[row][v >> 5] >> (v & 31)) & 1u) << j;
-      }
-    }
-    // copies 0..3 fill this wave's four row blocks of the W tile, 4..7 of the X tile
+  for (int j = 0; j < 4; ++j) bits_cur[j] = s_bits[rowj[j]][v_cur >> 5];
+  uint32_t curA[4];
+  i32x4_t rA, rB;
+  auto prepare = [&](int st) {
+    const bool live = st < nst;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) curA[j] = offA[j] | (((~bits_cur[j] >> (v_cur & 31)) & 1u) << 31);
+    const int k0 = live ? v_cur * G + (st % SUB) * kBK : 0;
+    rA = make_rsrc(W + k0, live ? bytesW - 2u * uint32_t(k0) : 0u);
+    rB = make_rsrc(X + k0, live ? bytesX - 2u * uint32_t(k0) : 0u);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) bits_cur[j] = s_bits[rowj[j]][v_nxt >> 5];
+    v_cur = v_nxt;
+    v_nxt = __builtin_amdgcn_readfirstlane(s_cols[col_of(st + 2)]);
+  };
+  // copies 0..3 fill this wave's four row blocks of the W tile, 4..7 of the X tile
+  auto issue = [&](int st, int p) {
     const int j = p & 3;
-    const int b = wave * 4 + j;
-    if (p < 4) {
-      const i32x4_t rA = make_rsrc(W + k0, live ? bytesW - 2u * uint32_t(k0) : 0u);
-      dma16_buf(rA, ((keptA >> j) & 1u) ? offA[j] : kOOB, As[st % kStages] + b * 64);
-    } else {
-      const i32x4_t rB = make_rsrc(X + k0, live ? bytesX - 2u * uint32_t(k0) : 0u);
-      dma16_buf(rB, offB[j], Bs[st % kStages] + b * 64);
-    }
+    const uint32_t dst = (st % kStages) * (BM * 64) + (wave * 4 + j) * 1024;
+    if (p < 4)
+      dma16_buf(rA, curA[j], ldsA + dst);
+    else
+      dma16_buf(rB, offB[j], ldsB + dst);
   };
   // Soft selectors: scale this lane's freshly landed W chunks by their mask value.
   auto rescale = [&](int st) {
@@ -273,11 +293,7 @@ __global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X
     u32x4* A = As[st % kStages];
     float m[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      int row, c;
-      km_dma_target((wave * 4 + j) * 64 + lane, row, c);
-      m[j] = m0 + row < d_out ? mask[int64_t(m0 + row) * G_in + v] : 0.0f;
-    }
+    for (int j = 0; j < 4; ++j) m[j] = m0 + rowj[j] < d_out ? mask[int64_t(m0 + rowj[j]) * G_in + v] : 0.0f;
     wait_vmcnt<0>();
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -287,14 +303,15 @@ __global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   };
 
+  // Hard masks (the common case) run a loop without the rescaling step.
   f32x4 acc[MB][NB];
   zero_acc(acc);
-  gemm_mainloop<MB, NB, true, true, 0, 0, PER_STAGE>(
-      As, Bs, nst, wm * 128, wn * 128, lane, acc, issue,
-      [&](int st) {
-        if (soft) rescale(st);
-      },
-      [](int, const u32x4(&)[NB]) {});
+  if (s_soft)
+    gemm_mainloop<MB, NB, true, true, 0, 0, PER_STAGE>(As, Bs, nst, wm * 128, wn * 128, lane, acc, prepare, issue,
+                                                       rescale, [](int, const u32x4(&)[NB]) {});
+  else
+    gemm_mainloop<MB, NB, true, true, 0, 0, PER_STAGE>(As, Bs, nst, wm * 128, wn * 128, lane, acc, prepare, issue,
+                                                       [](int) {}, [](int, const u32x4(&)[NB]) {});
 
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
@@ -344,20 +361,21 @@ __global__ __launch_bounds__(256) void dgate_kernel(const uint16_t* __restrict__
   }
   const uint32_t bytesX = uint32_t(T) * uint32_t(d_in) * 2u;
   const uint32_t bytesY = uint32_t(T) * uint32_t(d_out) * 2u;
-  auto issue = [&](int st, int p) {
+  i32x4_t rA, rB;  // buffer resources of the slice being copied (zero length past the end)
+  auto prepare = [&](int st) {
     const bool live = st < nst;
     const int k0 = live ? st * kBK : 0;
+    rA = make_rsrc(X + int64_t(k0) * d_in, live ? bytesX - uint32_t(k0) * uint32_t(d_in) * 2u : 0u);
+    rB = make_rsrc(dY + int64_t(k0) * d_out, live ? bytesY - uint32_t(k0) * uint32_t(d_out) * 2u : 0u);
+  };
+  const uint32_t ldsA = lds_addr(As), ldsB = lds_addr(Bs);
+  auto issue = [&](int st, int p) {
     const int j = p & 3;
-    const int b = wave * 4 + j;
-    if (p < 4) {
-      const i32x4_t rA =
-          make_rsrc(X + int64_t(k0) * d_in, live ? bytesX - uint32_t(k0) * uint32_t(d_in) * 2u : 0u);
-      dma16_buf(rA, offA[j], As[st % kStages] + b * 64);
-    } else {
-      const i32x4_t rB =
-          make_rsrc(dY + int64_t(k0) * d_out, live ? bytesY - uint32_t(k0) * uint32_t(d_out) * 2u : 0u);
-      dma16_buf(rB, offB[j], Bs[st % kStages] + b * 64);
-    }
+    const uint32_t dst = (st % kStages) * (kBK * BM * 2) + (wave * 4 + j) * 1024;
+    if (p < 4)
+      dma16_buf(rA, offA[j], ldsA + dst);
+    else
+      dma16_buf(rB, offB[j], ldsB + dst);
   };
 
   // dY^T side output (for the dX GEMM): lane (G, i) of a B fragment holds
@@ -378,8 +396,8 @@ __global__ __launch_bounds__(256) void dgate_kernel(const uint16_t* __restrict__
 
   f32x4 acc[MB][NB];
   zero_acc(acc);
-  gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE>(As, Bs, nst, wm * 128, wn * 128, lane, acc, issue,
-                                                        [](int) {}, bhook);
+  gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE>(As, Bs, nst, wm * 128, wn * 128, lane, acc, prepare,
+                                                        issue, [](int) {}, bhook);
 
   // Epilogue.  Lane (l >> 4, l & 15) holds, for every (mb, nb), rows
   // i = i0 .. i0 + 3 of column o: W[o, i0 .. i0 + 3] is one 8-byte load.
@@ -481,39 +499,50 @@ __global__ __launch_bounds__(256) void dx_kernel(const uint16_t* __restrict__ dY
   const float* __restrict__ sl = scales + int64_t(v) * d_out;
   const int nst = (kv + kBK - 1) / kBK;
 
-  // Slice st uses k-rows st*32 + r; this wave gathers rows r = 8 wave .. 8 wave + 7.
+  // Slice st uses k-rows st*32 + r; this wave gathers rows r = 8 wave .. 8 wave + 7,
+  // whose list entries are read with scalar loads one slice ahead.
   int idx[8];
   auto load_idx = [&](int st) {  // st <= nst: at most 31 + 32 entries past the column's end
     const int base = st * kBK + wave * 8;
 #pragma unroll
     for (int q = 0; q < 8; ++q) idx[q] = rl[base + q];  // uniform: scalar loads
   };
-  // The gathered k-row of a DMA lane is one of the wave's eight list entries:
-  // instruction j of a tile with CPR chunks per row covers rows
-  // 8 wave + j*64/CPR + lane/CPR.
-  auto row_index = [&](int q) {
-    int o = idx[0];
-#pragma unroll
-    for (int p = 1; p < 8; ++p) o = q == p ? idx[p] : o;
+  // Copy j of a tile with C columns (CPR = C / 8 chunks per k-row) covers
+  // k-rows 8 wave + j * RPI + lane / CPR, RPI = 64 / CPR: the lane's row is
+  // one of RPI consecutive list entries.
+  auto pick = [&](int j, int rpi, int u) {
+    int o = idx[j * rpi];
+    for (int q = 1; q < rpi; ++q) o = u == q ? idx[j * rpi + q] : o;
     return o;
   };
+  constexpr int RPI_A = 512 / BM, RPI_B = 512 / BN;
   const i32x4_t rA = make_rsrc(W + m0, (uint32_t(d_out) * uint32_t(d_in) - uint32_t(m0)) * 2u);
   const i32x4_t rB = make_rsrc(dYt + n0, (uint32_t(d_out) * uint32_t(ldt) - uint32_t(n0)) * 2u);
-  auto issue = [&](int st, int p) {  // copies 0 .. NA-1: W tile, NA .. NA+3: dY^T tile
-    const int k0 = st * kBK;          // slices past the end: every k0 + row >= kv reads zeros
-    if (p < NA) {
-      const int b = wave * NA + p;
+  uint32_t offA[NA], offB[4];  // this slice's per-lane offsets (rows past the list read zeros)
+  auto prepare = [&](int st) {
+    const int k0 = st * kBK;
+#pragma unroll
+    for (int j = 0; j < NA; ++j) {
       int row, c;
-      mn_dma_target<BM>(b * 64 + lane, row, c);
-      const uint32_t off = uint32_t(row_index(row & 7) * d_in + 8 * c) * 2u;
-      dma16_buf(rA, k0 + row < kv ? off : kOOB, As[st % kStages] + b * 64);
-    } else {
-      const int b = wave * 4 + (p - NA);
-      int row, c;
-      mn_dma_target<BN>(b * 64 + lane, row, c);
-      const uint32_t off = uint32_t(row_index(row & 7) * ldt + 8 * c) * 2u;
-      dma16_buf(rB, k0 + row < kv && n0 + 8 * c < ldt ? off : kOOB, Bs[st % kStages] + b * 64);
+      mn_dma_target<BM>((wave * NA + j) * 64 + lane, row, c);
+      const int o = pick(j, RPI_A, lane / (BM / 8));
+      offA[j] = uint32_t(o * d_in + 8 * c) * 2u | uint32_t(k0 + row >= kv) << 31;
     }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      int row, c;
+      mn_dma_target<BN>((wave * 4 + j) * 64 + lane, row, c);
+      const int o = pick(j, RPI_B, lane / (BN / 8));
+      offB[j] = uint32_t(o * ldt + 8 * c) * 2u | uint32_t(k0 + row >= kv || n0 + 8 * c >= ldt) << 31;
+    }
+    load_idx(min(st + 1, nst));
+  };
+  const uint32_t ldsA = lds_addr(As), ldsB = lds_addr(Bs);
+  auto issue = [&](int st, int p) {  // copies 0 .. NA-1: W tile, NA .. NA+3: dY^T tile
+    if (p < NA)
+      dma16_buf(rA, offA[p], ldsA + (st % kStages) * (kBK * BM * 2) + (wave * NA + p) * 1024);
+    else
+      dma16_buf(rB, offB[p - NA], ldsB + (st % kStages) * (kBK * BN * 2) + (wave * 4 + p - NA) * 1024);
   };
   // Soft selectors: scale this lane's landed W chunks by the row's mask value.
   auto rescale = [&](int st) {
@@ -533,18 +562,17 @@ __global__ __launch_bounds__(256) void dx_kernel(const uint16_t* __restrict__ dY
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   };
 
+  // Columns whose kept selectors are all exactly 1 run a loop without the rescaling step.
   f32x4 acc[MB][NB];
   zero_acc(acc);
-  gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE>(As, Bs, nst, wm * (BM / 2), wn * 128, lane, acc,
-                                                        [&](int st, int p) {  // slices are issued in order
-                                                          if (p == 0 && st == 0) load_idx(0);
-                                                          issue(st, p);
-                                                          if (p == PER_STAGE - 1) load_idx(min(st + 1, nst));
-                                                        },
-                                                        [&](int st) {
-                                                          if (soft) rescale(st);
-                                                        },
-                                                        [](int, const u32x4(&)[NB]) {});
+  load_idx(0);
+  if (soft)
+    gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE>(As, Bs, nst, wm * (BM / 2), wn * 128, lane, acc,
+                                                          prepare, issue, rescale, [](int, const u32x4(&)[NB]) {});
+  else
+    gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE>(As, Bs, nst, wm * (BM / 2), wn * 128, lane, acc,
+                                                          prepare, issue, [](int) {},
+                                                          [](int, const u32x4(&)[NB]) {});
 
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)

@@ -14,22 +14,14 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 constexpr int kStages = 4;
 constexpr int kBK = 32;
 
-// 16 bytes from global memory straight into LDS (global_load_lds_dwordx4):
-// lane l of the wave writes lds_wave_base + 16 l.  lds_wave_base must be the
-// same for the whole wave.  Issued through inline assembly so that the
-// compiler does not add conservative waits for it; completion is tracked
-// with wait_vmcnt() and made visible to the block with block_sync().  M0
-// needs one wait state after it is written.  M0 is a reserved register the
-// compiler cannot be told about; the kernels that use these helpers have no
-// other M0 reader (no GDS, message, move-relative or compiler-issued LDS DMA
-// instructions).
-__device__ __forceinline__ void dma16(const void* gsrc, const void* lds_wave_base) {
-  const uint32_t l = uint32_t(reinterpret_cast<uintptr_t>((lds_void*)lds_wave_base));
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-               :
-               : "v"(gsrc), "s"(__builtin_amdgcn_readfirstlane(l))
-               : "memory");
-}
+// Copies go from global memory straight into LDS with buffer loads (below),
+// issued through inline assembly so that the compiler does not add
+// conservative waits for them; completion is tracked with wait_vmcnt() and
+// made visible to the block with block_sync().  The LDS destination is taken
+// from M0, which needs one wait state after it is written.  M0 is a reserved
+// register the compiler cannot be told about; the kernels that use these
+// helpers have no other M0 reader (no GDS, message, move-relative or
+// compiler-issued LDS DMA instructions).
 
 // Buffer resource over a byte range [base, base + bytes): loads at offsets
 // outside it return zeros, which is how the kernels read padding, ragged
@@ -50,13 +42,20 @@ __device__ __forceinline__ i32x4_t make_rsrc(const void* base, uint32_t bytes) {
   return r;
 }
 
+// 32-bit LDS byte address of a __shared__ object (computed once per kernel:
+// the generic -> LDS conversion checks for null).
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return __builtin_amdgcn_readfirstlane(uint32_t(reinterpret_cast<uintptr_t>((lds_void*)p)));
+}
+
 // buffer_load_dwordx4 ... offen lds: 16 bytes at rsrc + voffset into LDS at
-// lds_wave_base + 16 lane (zeros when voffset is out of the resource's range).
-__device__ __forceinline__ void dma16_buf(i32x4_t rsrc, uint32_t voffset, const void* lds_wave_base) {
-  const uint32_t l = uint32_t(reinterpret_cast<uintptr_t>((lds_void*)lds_wave_base));
+// lds_wave_base + 16 lane (zeros when voffset is out of the resource's range;
+// ranges stay below 2 GiB, so setting bit 31 of an offset marks it out of range).
+// lds_wave_base is an LDS byte address, uniform across the wave.
+__device__ __forceinline__ void dma16_buf(i32x4_t rsrc, uint32_t voffset, uint32_t lds_wave_base) {
   asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
                :
-               : "v"(voffset), "s"(rsrc), "s"(__builtin_amdgcn_readfirstlane(l))
+               : "v"(voffset), "s"(rsrc), "s"(lds_wave_base)
                : "memory");
 }
 
