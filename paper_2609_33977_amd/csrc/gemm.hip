@@ -29,6 +29,8 @@
 #include "gm_launch.h"
 #include "gm_pipe.h"
 
+#include <type_traits>
+
 namespace gm {
 
 // Blocks are dealt to the eight XCDs round-robin; renumber them so that each
@@ -54,13 +56,9 @@ __device__ __forceinline__ void tile_coords(int nblocks, int tiles_m, int tiles_
   tn = r / gm;
 }
 
-template <int MB, int NB>
-__device__ __forceinline__ void zero_acc(f32x4 (&acc)[MB][NB]) {
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-}
+// Accumulator rows mb < kAgprRows<MB> live in AGPRs, the others in arch VGPRs.
+template <int MB>
+constexpr int kAgprRows = MB - (MB + 3) / 4;
 
 template <int NB, bool KM, int C>
 __device__ __forceinline__ void load_bfrags(const u32x4* __restrict__ Bs, int b0, int lane, u32x4 (&bf)[NB]) {
@@ -73,10 +71,20 @@ __device__ __forceinline__ u32x4 load_afrag(const u32x4* __restrict__ As, int a0
   return KM ? km_frag(As, a0, lane) : mn_frag<C>(As, a0, lane);
 }
 
-template <int MB, int NB>
+// One MFMA of accumulator (mb, nb); FIRST starts it from zero.
+template <bool FIRST, int MB, int NB>
+__device__ __forceinline__ void mfma_at(int mb, int nb, const u32x4& af, const u32x4& b, f32x4 (&acc)[MB][NB]) {
+  if (mb < kAgprRows<MB>) {
+    if constexpr (FIRST) mfma_init<true>(acc[mb][nb], af, b); else mfma_acc<true>(acc[mb][nb], af, b);
+  } else {
+    if constexpr (FIRST) mfma_init<false>(acc[mb][nb], af, b); else mfma_acc<false>(acc[mb][nb], af, b);
+  }
+}
+
+template <bool FIRST, int MB, int NB>
 __device__ __forceinline__ void mfma_row(int mb, const u32x4& af, const u32x4 (&bf)[NB], f32x4 (&acc)[MB][NB]) {
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = mfma16x16x32(af, bf[nb], acc[mb][nb]);
+  for (int nb = 0; nb < NB; ++nb) mfma_at<FIRST>(mb, nb, af, bf[nb], acc);
 }
 
 // The K-loop shared by the three GEMMs.  `prepare(st)` computes whatever the
@@ -88,7 +96,8 @@ __device__ __forceinline__ void mfma_row(int mb, const u32x4& af, const u32x4 (&
 // only need to stay inside their buffer resources.  `landed(st)` runs after
 // this wave's copies of slice st completed and before the barrier that
 // publishes them (soft-selector rescaling).  `bhook(kt, bf)` sees the B
-// fragments of slice kt once they are in registers.
+// fragments of slice kt once they are in registers.  The accumulators are
+// written by the first slice's MFMAs (zero when nst is 0).
 //
 // Software pipeline: rows 0 .. MB-2 of slice kt run first (A fragments
 // streamed one row ahead); then the wave waits for slice kt+1, meets the
@@ -98,8 +107,8 @@ __device__ __forceinline__ void mfma_row(int mb, const u32x4& af, const u32x4 (&
 // just consumed.  Copies run kStages slices ahead; fragment-read latency and
 // copy issue hide behind MFMA work.  Every iteration issues exactly PER_STAGE
 // copies (slices past the end copy zeros), so the wait count is a constant,
-// and the loop body has no branches around the accumulators; the last slice
-// is peeled off.
+// and the loop body has no branches around the accumulators; the first and
+// the last slice are peeled off.
 template <int MB, int NB, bool A_KM, bool B_KM, int CA, int CB, int PER_STAGE, int ABUF, int BBUF, class Prepare,
           class Issue, class Landed, class BHook>
 __device__ __forceinline__ void gemm_mainloop(u32x4 (*As)[ABUF], u32x4 (*Bs)[BBUF], int nst, int a0, int b0, int lane,
@@ -107,7 +116,13 @@ __device__ __forceinline__ void gemm_mainloop(u32x4 (*As)[ABUF], u32x4 (*Bs)[BBU
                                               Landed&& landed, BHook&& bhook) {
   static_assert(PER_STAGE <= NB, "copies are interleaved with the NB MFMAs of one row");
   constexpr int AHEAD = PER_STAGE * (kStages - 2);  // copies issued after the slice being waited for
-  if (nst <= 0) return;
+  if (nst <= 0) {
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    return;
+  }
   for (int s = 0; s < kStages - 1; ++s) {
     prepare(s);
 #pragma unroll
@@ -125,13 +140,16 @@ __device__ __forceinline__ void gemm_mainloop(u32x4 (*As)[ABUF], u32x4 (*Bs)[BBU
   load_bfrags<NB, B_KM, CB>(Bs[0], b0, lane, bf);
   af = load_afrag<A_KM, CA>(As[0], a0, lane);
 
-  for (int kt = 0; kt + 1 < nst; ++kt) {
+  // One slice that is followed by another: rows 0 .. MB-2, the barrier, then
+  // the last row interleaved with the next slice's copies and fragment reads.
+  auto slice = [&](int kt, auto first) {
+    constexpr bool FIRST = decltype(first)::value;
     bhook(kt, bf);
     const u32x4* A = As[kt % kStages];
 #pragma unroll
     for (int mb = 0; mb < MB - 1; ++mb) {
       const u32x4 an = load_afrag<A_KM, CA>(A, a0 + (mb + 1) * 16, lane);
-      mfma_row<MB, NB>(mb, af, bf, acc);
+      mfma_row<FIRST, MB, NB>(mb, af, bf, acc);
       af = an;
     }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's reads of slice kt are done
@@ -142,26 +160,37 @@ __device__ __forceinline__ void gemm_mainloop(u32x4 (*As)[ABUF], u32x4 (*Bs)[BBU
     const u32x4* Bn = Bs[(kt + 1) % kStages];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      acc[MB - 1][nb] = mfma16x16x32(af, bf[nb], acc[MB - 1][nb]);
+      mfma_at<FIRST, MB, NB>(MB - 1, nb, af, bf[nb], acc);
       __builtin_amdgcn_sched_barrier(0);
       if (nb < PER_STAGE) issue(kt + kStages, nb);
       bf[nb] = B_KM ? km_frag(Bn, b0 + nb * 16, lane) : mn_frag<CB>(Bn, b0 + nb * 16, lane);
       __builtin_amdgcn_sched_barrier(0);
     }
     af = load_afrag<A_KM, CA>(As[(kt + 1) % kStages], a0, lane);
-  }
-  {
+  };
+  // The last slice: all rows, no further copies.
+  auto last = [&](auto first) {
+    constexpr bool FIRST = decltype(first)::value;
     bhook(nst - 1, bf);
     const u32x4* A = As[(nst - 1) % kStages];
 #pragma unroll
     for (int mb = 0; mb < MB - 1; ++mb) {
       const u32x4 an = load_afrag<A_KM, CA>(A, a0 + (mb + 1) * 16, lane);
-      mfma_row<MB, NB>(mb, af, bf, acc);
+      mfma_row<FIRST, MB, NB>(mb, af, bf, acc);
       af = an;
     }
-    mfma_row<MB, NB>(MB - 1, af, bf, acc);
+    mfma_row<FIRST, MB, NB>(MB - 1, af, bf, acc);
+  };
+
+  if (nst == 1) {
+    last(std::true_type{});
+  } else {
+    slice(0, std::true_type{});
+    for (int kt = 1; kt + 1 < nst; ++kt) slice(kt, std::false_type{});
+    last(std::false_type{});
   }
   wait_vmcnt<0>();  // zero-fill copies of slices past the end, before the block exits
+  acc_drain<kAgprRows<MB> * NB>(reinterpret_cast<f32x4(&)[MB * NB]>(acc));
 }
 
 // Store 4 adjacent bf16 (rows m .. m+3 of the MFMA tile = consecutive output columns).
@@ -305,7 +334,6 @@ __global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X
 
   // Hard masks (the common case) run a loop without the rescaling step.
   f32x4 acc[MB][NB];
-  zero_acc(acc);
   if (s_soft)
     gemm_mainloop<MB, NB, true, true, 0, 0, PER_STAGE>(As, Bs, nst, wm * 128, wn * 128, lane, acc, prepare, issue,
                                                        rescale, [](int, const u32x4(&)[NB]) {});
@@ -395,7 +423,6 @@ __global__ __launch_bounds__(256) void dgate_kernel(const uint16_t* __restrict__
   };
 
   f32x4 acc[MB][NB];
-  zero_acc(acc);
   gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE>(As, Bs, nst, wm * 128, wn * 128, lane, acc, prepare,
                                                         issue, [](int) {}, bhook);
 
@@ -564,7 +591,6 @@ __global__ __launch_bounds__(256) void dx_kernel(const uint16_t* __restrict__ dY
 
   // Columns whose kept selectors are all exactly 1 run a loop without the rescaling step.
   f32x4 acc[MB][NB];
-  zero_acc(acc);
   load_idx(0);
   if (soft)
     gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE>(As, Bs, nst, wm * (BM / 2), wn * 128, lane, acc,

@@ -70,6 +70,54 @@ __device__ __forceinline__ f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c) {
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
+// The same MFMA accumulating in place, written in assembly with the
+// accumulator as one tied operand.  With the builtin, this clang often gives
+// the result a different register from the accumulator input and moves it
+// back (up to one move per MFMA with 64 live accumulators), which cuts the
+// issue rate of a 128 x 128 wave tile by a third.  AGPR selects the register
+// file of the accumulator: a wave tile keeps most accumulators in AGPRs and
+// the rest in arch VGPRs, which leaves the register allocator room in both.
+// mfma_init starts an accumulator (C input 0), so no accumulator is written
+// by other instructions before the K-loop.  The compiler does not see these
+// instructions as MFMAs, so its hazard padding does not cover them; readers
+// of the accumulators wait for acc_drain().
+template <bool AGPR>
+__device__ __forceinline__ void mfma_acc(f32x4& acc, const u32x4& a, const u32x4& b) {
+  if constexpr (AGPR)
+    asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+  else
+    asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(a), "v"(b));
+}
+
+template <bool AGPR>
+__device__ __forceinline__ void mfma_init(f32x4& acc, const u32x4& a, const u32x4& b) {
+  if constexpr (AGPR)
+    asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, 0" : "=a"(acc) : "v"(a), "v"(b));
+  else
+    asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, 0" : "=&v"(acc) : "v"(a), "v"(b));
+}
+
+template <bool AGPR>
+__device__ __forceinline__ void acc_pin(f32x4& acc) {
+  if constexpr (AGPR)
+    asm volatile("" : "+a"(acc));
+  else
+    asm volatile("" : "+v"(acc));
+}
+
+// After the last MFMA: 24 wait states (more than the longest MFMA write ->
+// VALU read dependency), then every accumulator passes through an empty
+// statement that orders its readers after the wait.  Accumulator i lives in
+// AGPRs when i < N_AGPR.
+template <int N_AGPR, int N>
+__device__ __forceinline__ void acc_drain(f32x4 (&acc)[N]) {
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    if (i < N_AGPR) acc_pin<true>(acc[i]); else acc_pin<false>(acc[i]);
+  }
+}
+
 // ---------------------------------------------------------------- LDS tiles
 
 // A K-major bf16 tile of R rows x 64 k (128 bytes per row, eight 16-byte
