@@ -56,6 +56,11 @@ __device__ __forceinline__ void tile_coords(int nblocks, int tiles_m, int tiles_
   tn = r / gm;
 }
 
+// LDS pipeline depth (K slices of kBK) per GEMM; the forward also keeps the
+// tile's kept bits in LDS.
+constexpr int kStagesDgate = 4;
+constexpr int kStagesDx = 4;
+
 // Accumulator rows mb < kAgprRows<MB> live in AGPRs, the others in arch VGPRs.
 template <int MB>
 constexpr int kAgprRows = MB - (MB + 3) / 4;
@@ -92,7 +97,7 @@ __device__ __forceinline__ void mfma_row(int mb, const u32x4& af, const u32x4 (&
 // once per slice, in increasing st, at a point where this wave has no LDS read
 // in flight, so any LDS or scalar loads it makes cost only their own latency.
 // `issue(st, p)` then starts copy p (0 <= p < PER_STAGE) of slice st into LDS
-// buffer st % kStages; slices st >= nst are never consumed, so their copies
+// buffer st % STAGES; slices st >= nst are never consumed, so their copies
 // only need to stay inside their buffer resources.  `landed(st)` runs after
 // this wave's copies of slice st completed and before the barrier that
 // publishes them (soft-selector rescaling).  `bhook(kt, bf)` sees the B
@@ -101,21 +106,21 @@ __device__ __forceinline__ void mfma_row(int mb, const u32x4& af, const u32x4 (&
 //
 // Software pipeline: rows 0 .. MB-2 of slice kt run first (A fragments
 // streamed one row ahead); then the wave waits for slice kt+1, meets the
-// others at the barrier (which also frees buffer kt % kStages), and issues the
-// last MFMA row of slice kt interleaved with the copies of slice kt + kStages
+// others at the barrier (which also frees buffer kt % STAGES), and issues the
+// last MFMA row of slice kt interleaved with the copies of slice kt + STAGES
 // and the reads of slice kt+1's B fragments into the registers each MFMA has
-// just consumed.  Copies run kStages slices ahead; fragment-read latency and
+// just consumed.  Copies run STAGES slices ahead; fragment-read latency and
 // copy issue hide behind MFMA work.  Every iteration issues exactly PER_STAGE
 // copies (slices past the end copy zeros), so the wait count is a constant,
 // and the loop body has no branches around the accumulators; the first and
 // the last slice are peeled off.
-template <int MB, int NB, bool A_KM, bool B_KM, int CA, int CB, int PER_STAGE, int ABUF, int BBUF, class Prepare,
-          class Issue, class Landed, class BHook>
+template <int MB, int NB, bool A_KM, bool B_KM, int CA, int CB, int PER_STAGE, int STAGES, int ABUF, int BBUF,
+          class Prepare, class Issue, class Landed, class BHook>
 __device__ __forceinline__ void gemm_mainloop(u32x4 (*As)[ABUF], u32x4 (*Bs)[BBUF], int nst, int a0, int b0, int lane,
                                               f32x4 (&acc)[MB][NB], Prepare&& prepare, Issue&& issue,
                                               Landed&& landed, BHook&& bhook) {
   static_assert(PER_STAGE <= NB, "copies are interleaved with the NB MFMAs of one row");
-  constexpr int AHEAD = PER_STAGE * (kStages - 2);  // copies issued after the slice being waited for
+  constexpr int AHEAD = PER_STAGE * (STAGES - 2);  // copies issued after the slice being waited for
   if (nst <= 0) {
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
@@ -123,17 +128,17 @@ __device__ __forceinline__ void gemm_mainloop(u32x4 (*As)[ABUF], u32x4 (*Bs)[BBU
       for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
     return;
   }
-  for (int s = 0; s < kStages - 1; ++s) {
+  for (int s = 0; s < STAGES - 1; ++s) {
     prepare(s);
 #pragma unroll
     for (int p = 0; p < PER_STAGE; ++p) issue(s, p);
   }
-  prepare(kStages - 1);
+  prepare(STAGES - 1);
   wait_vmcnt<AHEAD>();
   landed(0);
   block_sync();
 #pragma unroll
-  for (int p = 0; p < PER_STAGE; ++p) issue(kStages - 1, p);
+  for (int p = 0; p < PER_STAGE; ++p) issue(STAGES - 1, p);
 
   u32x4 bf[NB];
   u32x4 af;
@@ -145,7 +150,7 @@ __device__ __forceinline__ void gemm_mainloop(u32x4 (*As)[ABUF], u32x4 (*Bs)[BBU
   auto slice = [&](int kt, auto first) {
     constexpr bool FIRST = decltype(first)::value;
     bhook(kt, bf);
-    const u32x4* A = As[kt % kStages];
+    const u32x4* A = As[kt % STAGES];
 #pragma unroll
     for (int mb = 0; mb < MB - 1; ++mb) {
       const u32x4 an = load_afrag<A_KM, CA>(A, a0 + (mb + 1) * 16, lane);
@@ -153,26 +158,26 @@ __device__ __forceinline__ void gemm_mainloop(u32x4 (*As)[ABUF], u32x4 (*Bs)[BBU
       af = an;
     }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's reads of slice kt are done
-    prepare(kt + kStages);
+    prepare(kt + STAGES);
     wait_vmcnt<AHEAD>();                                 // ... and its copies of slice kt+1
     landed(kt + 1);
     block_sync();
-    const u32x4* Bn = Bs[(kt + 1) % kStages];
+    const u32x4* Bn = Bs[(kt + 1) % STAGES];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       mfma_at<FIRST, MB, NB>(MB - 1, nb, af, bf[nb], acc);
       __builtin_amdgcn_sched_barrier(0);
-      if (nb < PER_STAGE) issue(kt + kStages, nb);
+      if (nb < PER_STAGE) issue(kt + STAGES, nb);
       bf[nb] = B_KM ? km_frag(Bn, b0 + nb * 16, lane) : mn_frag<CB>(Bn, b0 + nb * 16, lane);
       __builtin_amdgcn_sched_barrier(0);
     }
-    af = load_afrag<A_KM, CA>(As[(kt + 1) % kStages], a0, lane);
+    af = load_afrag<A_KM, CA>(As[(kt + 1) % STAGES], a0, lane);
   };
   // The last slice: all rows, no further copies.
   auto last = [&](auto first) {
     constexpr bool FIRST = decltype(first)::value;
     bhook(nst - 1, bf);
-    const u32x4* A = As[(nst - 1) % kStages];
+    const u32x4* A = As[(nst - 1) % STAGES];
 #pragma unroll
     for (int mb = 0; mb < MB - 1; ++mb) {
       const u32x4 an = load_afrag<A_KM, CA>(A, a0 + (mb + 1) * 16, lane);
@@ -212,8 +217,9 @@ __global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X
   constexpr int SUB = G / kBK;          // K slices per group column
   constexpr int MAXG = 512;             // group-column limit (checked by the host)
   constexpr int PER_STAGE = 8;          // DMA instructions per wave per slice
-  __shared__ u32x4 As[kStages][BM * 4];
-  __shared__ u32x4 Bs[kStages][BN * 4];
+  constexpr int STAGES = 4;
+  __shared__ u32x4 As[STAGES][BM * 4];
+  __shared__ u32x4 Bs[STAGES][BN * 4];
   __shared__ uint32_t s_bits[BM][MAXG / 32];  // kept bits of the tile's rows
   __shared__ uint32_t s_any[MAXG / 32];       // column kept by some row of the tile
   __shared__ int s_cols[MAXG];
@@ -275,8 +281,8 @@ __global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X
   for (int j = 0; j < 4; ++j) {
     int c;
     km_dma_target((wave * 4 + j) * 64 + lane, rowj[j], c);
-    offA[j] = uint32_t((m0 + rowj[j]) * d_in + 8 * c) * 2u;
-    offB[j] = uint32_t((n0 + rowj[j]) * d_in + 8 * c) * 2u;
+    offA[j] = group_voffset(uint32_t((m0 + rowj[j]) * d_in + 8 * c) * 2u, j);
+    offB[j] = group_voffset(uint32_t((n0 + rowj[j]) * d_in + 8 * c) * 2u, j);
   }
   const uint32_t bytesW = uint32_t(d_out) * uint32_t(d_in) * 2u;
   const uint32_t bytesX = uint32_t(T) * uint32_t(d_in) * 2u;
@@ -300,8 +306,8 @@ __global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X
 #pragma unroll
     for (int j = 0; j < 4; ++j) curA[j] = offA[j] | (((~bits_cur[j] >> (v_cur & 31)) & 1u) << 31);
     const int k0 = live ? v_cur * G + (st % SUB) * kBK : 0;
-    rA = make_rsrc(W + k0, live ? bytesW - 2u * uint32_t(k0) : 0u);
-    rB = make_rsrc(X + k0, live ? bytesX - 2u * uint32_t(k0) : 0u);
+    rA = make_rsrc_grouped(W + k0, live ? bytesW - 2u * uint32_t(k0) : 0u);
+    rB = make_rsrc_grouped(X + k0, live ? bytesX - 2u * uint32_t(k0) : 0u);
 #pragma unroll
     for (int j = 0; j < 4; ++j) bits_cur[j] = s_bits[rowj[j]][v_nxt >> 5];
     v_cur = v_nxt;
@@ -310,16 +316,16 @@ __global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X
   // copies 0..3 fill this wave's four row blocks of the W tile, 4..7 of the X tile
   auto issue = [&](int st, int p) {
     const int j = p & 3;
-    const uint32_t dst = (st % kStages) * (BM * 64) + (wave * 4 + j) * 1024;
+    const uint32_t dst = (st % STAGES) * (BM * 64) + wave * 4 * 1024;
     if (p < 4)
-      dma16_buf(rA, curA[j], ldsA + dst);
+      dma16_group(j, rA, curA[j], ldsA + dst);
     else
-      dma16_buf(rB, offB[j], ldsB + dst);
+      dma16_group(j, rB, offB[j], ldsB + dst);
   };
   // Soft selectors: scale this lane's freshly landed W chunks by their mask value.
   auto rescale = [&](int st) {
     const int v = s_cols[st / SUB];
-    u32x4* A = As[st % kStages];
+    u32x4* A = As[st % STAGES];
     float m[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) m[j] = m0 + rowj[j] < d_out ? mask[int64_t(m0 + rowj[j]) * G_in + v] : 0.0f;
@@ -335,10 +341,10 @@ __global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X
   // Hard masks (the common case) run a loop without the rescaling step.
   f32x4 acc[MB][NB];
   if (s_soft)
-    gemm_mainloop<MB, NB, true, true, 0, 0, PER_STAGE>(As, Bs, nst, wm * 128, wn * 128, lane, acc, prepare, issue,
+    gemm_mainloop<MB, NB, true, true, 0, 0, PER_STAGE, STAGES>(As, Bs, nst, wm * 128, wn * 128, lane, acc, prepare, issue,
                                                        rescale, [](int, const u32x4(&)[NB]) {});
   else
-    gemm_mainloop<MB, NB, true, true, 0, 0, PER_STAGE>(As, Bs, nst, wm * 128, wn * 128, lane, acc, prepare, issue,
+    gemm_mainloop<MB, NB, true, true, 0, 0, PER_STAGE, STAGES>(As, Bs, nst, wm * 128, wn * 128, lane, acc, prepare, issue,
                                                        [](int) {}, [](int, const u32x4(&)[NB]) {});
 
 #pragma unroll
@@ -363,9 +369,9 @@ __global__ __launch_bounds__(256) void dgate_kernel(const uint16_t* __restrict__
                                                     float* __restrict__ dgate, uint16_t* __restrict__ dYt, int ldt) {
   constexpr int BM = 256, BN = 256, MB = 8, NB = 8;
   constexpr int PER_STAGE = 8;
-  __shared__ u32x4 As[kStages][kBK * BM / 8];
-  __shared__ u32x4 Bs[kStages][kBK * BN / 8];
-  __shared__ float s_part[2][BN];
+  constexpr int STAGES = kStagesDgate;
+  __shared__ u32x4 As[STAGES][kBK * BM / 8];
+  __shared__ u32x4 Bs[STAGES][kBK * BN / 8];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -384,8 +390,8 @@ __global__ __launch_bounds__(256) void dgate_kernel(const uint16_t* __restrict__
   for (int j = 0; j < 4; ++j) {
     int row, c;
     mn_dma_target<256>((wave * 4 + j) * 64 + lane, row, c);
-    offA[j] = m0 + 8 * c < d_in ? uint32_t(row * d_in + m0 + 8 * c) * 2u : kOOB;
-    offB[j] = n0 + 8 * c < d_out ? uint32_t(row * d_out + n0 + 8 * c) * 2u : kOOB;
+    offA[j] = group_voffset(m0 + 8 * c < d_in ? uint32_t(row * d_in + m0 + 8 * c) * 2u : kOOB, j);
+    offB[j] = group_voffset(n0 + 8 * c < d_out ? uint32_t(row * d_out + n0 + 8 * c) * 2u : kOOB, j);
   }
   const uint32_t bytesX = uint32_t(T) * uint32_t(d_in) * 2u;
   const uint32_t bytesY = uint32_t(T) * uint32_t(d_out) * 2u;
@@ -393,17 +399,17 @@ __global__ __launch_bounds__(256) void dgate_kernel(const uint16_t* __restrict__
   auto prepare = [&](int st) {
     const bool live = st < nst;
     const int k0 = live ? st * kBK : 0;
-    rA = make_rsrc(X + int64_t(k0) * d_in, live ? bytesX - uint32_t(k0) * uint32_t(d_in) * 2u : 0u);
-    rB = make_rsrc(dY + int64_t(k0) * d_out, live ? bytesY - uint32_t(k0) * uint32_t(d_out) * 2u : 0u);
+    rA = make_rsrc_grouped(X + int64_t(k0) * d_in, live ? bytesX - uint32_t(k0) * uint32_t(d_in) * 2u : 0u);
+    rB = make_rsrc_grouped(dY + int64_t(k0) * d_out, live ? bytesY - uint32_t(k0) * uint32_t(d_out) * 2u : 0u);
   };
   const uint32_t ldsA = lds_addr(As), ldsB = lds_addr(Bs);
   auto issue = [&](int st, int p) {
     const int j = p & 3;
-    const uint32_t dst = (st % kStages) * (kBK * BM * 2) + (wave * 4 + j) * 1024;
+    const uint32_t dst = (st % STAGES) * (kBK * BM * 2) + wave * 4 * 1024;
     if (p < 4)
-      dma16_buf(rA, offA[j], ldsA + dst);
+      dma16_group(j, rA, offA[j], ldsA + dst);
     else
-      dma16_buf(rB, offB[j], ldsB + dst);
+      dma16_group(j, rB, offB[j], ldsB + dst);
   };
 
   // dY^T side output (for the dX GEMM): lane (G, i) of a B fragment holds
@@ -423,7 +429,7 @@ __global__ __launch_bounds__(256) void dgate_kernel(const uint16_t* __restrict__
   };
 
   f32x4 acc[MB][NB];
-  gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE>(As, Bs, nst, wm * 128, wn * 128, lane, acc, prepare,
+  gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE, STAGES>(As, Bs, nst, wm * 128, wn * 128, lane, acc, prepare,
                                                         issue, [](int) {}, bhook);
 
   // Epilogue.  Lane (l >> 4, l & 15) holds, for every (mb, nb), rows
@@ -472,6 +478,10 @@ __global__ __launch_bounds__(256) void dgate_kernel(const uint16_t* __restrict__
       }
     }
   } else {
+    // The two wave rows combine through LDS, reusing the first stage buffer
+    // once every wave has finished its K-loop (their copies have drained).
+    float(*s_part)[BN] = reinterpret_cast<float(*)[BN]>(&As[0][0]);
+    __syncthreads();
     if (lane < 16) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) s_part[wm][wn * 128 + nb * 16 + lane] = part[nb][0] + part[nb][1];
@@ -509,8 +519,9 @@ __global__ __launch_bounds__(256) void dx_kernel(const uint16_t* __restrict__ dY
   constexpr int BN = 256, MB = BM / 32, NB = 8;
   constexpr int NA = BM / 64;            // A DMA instructions per wave per slice
   constexpr int PER_STAGE = NA + 4;
-  __shared__ u32x4 As[kStages][kBK * BM / 8];
-  __shared__ u32x4 Bs[kStages][kBK * BN / 8];
+  constexpr int STAGES = kStagesDx;
+  __shared__ u32x4 As[STAGES][kBK * BM / 8];
+  __shared__ u32x4 Bs[STAGES][kBK * BN / 8];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -543,8 +554,8 @@ __global__ __launch_bounds__(256) void dx_kernel(const uint16_t* __restrict__ dY
     return o;
   };
   constexpr int RPI_A = 512 / BM, RPI_B = 512 / BN;
-  const i32x4_t rA = make_rsrc(W + m0, (uint32_t(d_out) * uint32_t(d_in) - uint32_t(m0)) * 2u);
-  const i32x4_t rB = make_rsrc(dYt + n0, (uint32_t(d_out) * uint32_t(ldt) - uint32_t(n0)) * 2u);
+  const i32x4_t rA = make_rsrc_grouped(W + m0, (uint32_t(d_out) * uint32_t(d_in) - uint32_t(m0)) * 2u);
+  const i32x4_t rB = make_rsrc_grouped(dYt + n0, (uint32_t(d_out) * uint32_t(ldt) - uint32_t(n0)) * 2u);
   uint32_t offA[NA], offB[4];  // this slice's per-lane offsets (rows past the list read zeros)
   auto prepare = [&](int st) {
     const int k0 = st * kBK;
@@ -553,28 +564,28 @@ __global__ __launch_bounds__(256) void dx_kernel(const uint16_t* __restrict__ dY
       int row, c;
       mn_dma_target<BM>((wave * NA + j) * 64 + lane, row, c);
       const int o = pick(j, RPI_A, lane / (BM / 8));
-      offA[j] = uint32_t(o * d_in + 8 * c) * 2u | uint32_t(k0 + row >= kv) << 31;
+      offA[j] = group_voffset(uint32_t(o * d_in + 8 * c) * 2u | uint32_t(k0 + row >= kv) << 31, j);
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       int row, c;
       mn_dma_target<BN>((wave * 4 + j) * 64 + lane, row, c);
       const int o = pick(j, RPI_B, lane / (BN / 8));
-      offB[j] = uint32_t(o * ldt + 8 * c) * 2u | uint32_t(k0 + row >= kv || n0 + 8 * c >= ldt) << 31;
+      offB[j] = group_voffset(uint32_t(o * ldt + 8 * c) * 2u | uint32_t(k0 + row >= kv || n0 + 8 * c >= ldt) << 31, j);
     }
     load_idx(min(st + 1, nst));
   };
   const uint32_t ldsA = lds_addr(As), ldsB = lds_addr(Bs);
   auto issue = [&](int st, int p) {  // copies 0 .. NA-1: W tile, NA .. NA+3: dY^T tile
     if (p < NA)
-      dma16_buf(rA, offA[p], ldsA + (st % kStages) * (kBK * BM * 2) + (wave * NA + p) * 1024);
+      dma16_group(p, rA, offA[p], ldsA + (st % STAGES) * (kBK * BM * 2) + wave * NA * 1024);
     else
-      dma16_buf(rB, offB[p - NA], ldsB + (st % kStages) * (kBK * BN * 2) + (wave * 4 + p - NA) * 1024);
+      dma16_group(p - NA, rB, offB[p - NA], ldsB + (st % STAGES) * (kBK * BN * 2) + wave * 4 * 1024);
   };
   // Soft selectors: scale this lane's landed W chunks by the row's mask value.
   auto rescale = [&](int st) {
     const int k0 = st * kBK;
-    u32x4* A = As[st % kStages];
+    u32x4* A = As[st % STAGES];
 #pragma unroll
     for (int j = 0; j < NA; ++j) {
       const int b = wave * NA + j;
@@ -593,10 +604,10 @@ __global__ __launch_bounds__(256) void dx_kernel(const uint16_t* __restrict__ dY
   f32x4 acc[MB][NB];
   load_idx(0);
   if (soft)
-    gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE>(As, Bs, nst, wm * (BM / 2), wn * 128, lane, acc,
+    gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE, STAGES>(As, Bs, nst, wm * (BM / 2), wn * 128, lane, acc,
                                                           prepare, issue, rescale, [](int, const u32x4(&)[NB]) {});
   else
-    gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE>(As, Bs, nst, wm * (BM / 2), wn * 128, lane, acc,
+    gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE, STAGES>(As, Bs, nst, wm * (BM / 2), wn * 128, lane, acc,
                                                           prepare, issue, [](int) {},
                                                           [](int, const u32x4(&)[NB]) {});
 

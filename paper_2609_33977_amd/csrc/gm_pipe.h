@@ -10,8 +10,7 @@ namespace gm {
 typedef __attribute__((address_space(3))) void lds_void;
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 
-// Pipeline depth (LDS stages) and K per stage.
-constexpr int kStages = 4;
+// K per LDS pipeline stage.
 constexpr int kBK = 32;
 
 // Copies go from global memory straight into LDS with buffer loads (below),
@@ -57,6 +56,43 @@ __device__ __forceinline__ void dma16_buf(i32x4_t rsrc, uint32_t voffset, uint32
                :
                : "v"(voffset), "s"(rsrc), "s"(lds_wave_base)
                : "memory");
+}
+
+// Grouped copies: up to four copies J = 0..3 of a wave share one M0 value.
+// The instruction offset of buffer_load ... lds adds to both the memory
+// offset and the LDS address, so copy J uses offset 1024 J and lands at
+// m0 + 1024 J + 16 lane.  To keep every lane's memory offset non-negative,
+// the buffer resource starts kDmaBias bytes early (make_rsrc_grouped) and
+// copy J's lane offset is biased by kDmaBias - 1024 J (group_voffset); the
+// range check is unchanged, and an offset with bit 31 set stays out of range.
+constexpr uint32_t kDmaBias = 3072;
+
+__device__ __forceinline__ i32x4_t make_rsrc_grouped(const void* base, uint32_t bytes) {
+  return make_rsrc(static_cast<const char*>(base) - kDmaBias, bytes + kDmaBias);
+}
+
+__device__ __forceinline__ uint32_t group_voffset(uint32_t off, int j) { return off + kDmaBias - 1024u * uint32_t(j); }
+
+// Copy J of a group; J == 0 sets M0 to the group's LDS base (uniform).
+template <int J>
+__device__ __forceinline__ void dma16_group(i32x4_t rsrc, uint32_t voffset, uint32_t lds_group_base) {
+  static_assert(J >= 0 && J < 4, "four copies per M0 value");
+  if constexpr (J == 0)
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+                 :
+                 : "v"(voffset), "s"(rsrc), "s"(lds_group_base)
+                 : "memory");
+  else
+    asm volatile("buffer_load_dwordx4 %0, %1, 0 offen offset:%2 lds" : : "v"(voffset), "s"(rsrc), "n"(J * 1024) : "memory");
+}
+
+__device__ __forceinline__ void dma16_group(int j, i32x4_t rsrc, uint32_t voffset, uint32_t lds_group_base) {
+  switch (j) {
+    case 0: dma16_group<0>(rsrc, voffset, lds_group_base); break;
+    case 1: dma16_group<1>(rsrc, voffset, lds_group_base); break;
+    case 2: dma16_group<2>(rsrc, voffset, lds_group_base); break;
+    default: dma16_group<3>(rsrc, voffset, lds_group_base); break;
+  }
 }
 
 template <int N>
