@@ -122,19 +122,20 @@ __device__ __forceinline__ void block_sync() {
 
 // ---------------------------------------------------------------- K-major tile
 // R rows x 32 k, 64 bytes per row.  16-byte chunk c (k = 8c .. 8c+7) of row r
-// sits at slot 4 r + (c ^ ((r >> 2) & 3)).  The LDS has 64 banks (256 bytes):
-// rows r .. r+3 at one chunk already fall on four different bank quarters, and
-// the XOR with bits 2-3 of the row moves rows 4 apart to other chunks, so the
-// 16 rows that one fragment read touches cover all banks once.  The XOR term
+// sits at slot 4 r + (c ^ ((r >> 1) & 3)).  A 16-byte-per-lane LDS read is
+// served eight lanes (128 bytes) per cycle: the eight consecutive rows that
+// eight lanes of one fragment read touch occupy two 64-byte row pairs, and the
+// XOR with bits 1-2 of the row moves rows of equal parity to four different
+// 16-byte columns, so the eight lanes cover the 128 bytes once.  The XOR term
 // depends only on the row within its 16-row fragment, so fragment addresses
 // are a per-lane base plus compile-time offsets.
 
-__device__ __forceinline__ int km_slot(int row, int chunk) { return row * 4 + (chunk ^ ((row >> 2) & 3)); }
+__device__ __forceinline__ int km_slot(int row, int chunk) { return row * 4 + (chunk ^ ((row >> 1) & 3)); }
 
 // DMA slot s of the tile (s = 64 b + lane) -> (row, logical chunk).
 __device__ __forceinline__ void km_dma_target(int s, int& row, int& chunk) {
   row = s >> 2;
-  chunk = (s & 3) ^ ((row >> 2) & 3);
+  chunk = (s & 3) ^ ((row >> 1) & 3);
 }
 
 // MFMA fragment (8 consecutive k of one row) for lane l: row0 + (l & 15), k-chunk l >> 4.
