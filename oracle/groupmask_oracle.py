@@ -27,6 +27,10 @@ design notes of the repository):
   (Sec. 2.1 with g_out = 1, g_in = g).  ``expand_mask`` also takes g_out > 1.
 * dgate is produced for every group, pruned or kept, because the STE passes a
   gradient to every selector; it does not depend on the mask values.
+* Budget regulariser (Sec. 2.3): a selector counts as kept when its mask value
+  is nonzero (the discrete B).  Its gradient is the derivative of the loss
+  with B taken as continuous (what the STE hands to the relaxation), with
+  sign(0) = 0 at s = s_t; the uniform variant sums the per-layer terms.
 """
 from __future__ import annotations
 
@@ -35,7 +39,7 @@ import numpy as np
 __all__ = [
     "from_bf16", "logistic_noise", "gate", "gate_bwd", "expand_mask", "masked_weight",
     "linear_fwd", "linear_bwd_dx", "linear_bwd_dgate", "linear_bwd", "sparsity",
-    "preserved_rate", "near_threshold", "kept_count",
+    "preserved_rate", "near_threshold", "kept_count", "budget_loss",
 ]
 
 
@@ -161,3 +165,40 @@ def preserved_rate(B, g_in: int, g_out: int = 1) -> float:
     """Active weights / total weights after applying the binary mask (Appendix F)."""
     M = expand_mask((np.asarray(B) != 0).astype(np.float64), g_in, g_out)
     return float(M.sum() / M.size)
+
+
+# ------------------------------------------ sparsity-budget regulariser (Sec. 2.3)
+
+def budget_loss(selectors, params, s_target: float, lam: float, uniform: bool = False):
+    """Sparsity-budget regulariser of Sec. 2.3 and its gradient per selector.
+
+    selectors: list of B^l arrays (nonzero = kept); params: list of P^l, the
+    weight count d_out^l d_in^l of each layer.  With G^l = B^l.size groups and
+    s^l, s from Eq. 2:
+
+      global  : L = lam |log(s / s_t)|
+                dL/dB^l = lam sgn(log(s/s_t)) (1/s) ds/dB^l,  ds/dB^l = -(P^l / G^l) / sum_k P^k
+      uniform : L = sum_l lam |log(s^l / s_t)|
+                dL/dB^l = lam sgn(log(s^l/s_t)) (1/s^l) (-1 / G^l)
+
+    Every selector of layer l receives the same derivative coeff[l].  s = 0
+    (every group kept) makes L and the derivative infinite.
+    Returns (L, coeff, kept) with coeff a float64 array over layers and kept
+    the integer kept counts.
+    """
+    kept = np.array([np.count_nonzero(np.asarray(B)) for B in selectors], dtype=np.int64)
+    G = np.array([np.asarray(B).size for B in selectors], dtype=np.float64)
+    P = np.array(params, dtype=np.float64)
+    s_layer = 1.0 - kept / G
+    with np.errstate(divide="ignore"):
+        if uniform:
+            logs = np.log(s_layer / s_target)
+            L = float(np.sum(lam * np.abs(logs)))
+            coeff = lam * np.sign(logs) / s_layer * (-1.0 / G)
+        else:
+            s = float(np.sum(s_layer * P) / np.sum(P))
+            logr = np.log(s / s_target)
+            L = float(lam * abs(logr))
+            coeff = lam * np.sign(logr) / s * (-(P / G) / np.sum(P))
+    return L, coeff, kept
+

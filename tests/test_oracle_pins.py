@@ -329,6 +329,80 @@ def test_preserved_rate_counts_active_weights():
     assert (d_out * d_in) / B.size == gold["reduction_factor"]
 
 
+# ------------------------------------------- sparsity-budget regulariser (Sec. 2.3)
+
+def _budget_layers():
+    """Three layers of different shapes and group sizes, about half of the groups kept."""
+    r = workloads.gen.rng_for(902)
+    shapes = [(48, 512, 256), (96, 1024, 256), (40, 768, 128)]  # (d_out, d_in, g)
+    B = [(r.uniform(size=(do, di // g)) < p).astype(np.float64) for (do, di, g), p in zip(shapes, (0.3, 0.55, 0.7))]
+    params = [do * di for do, di, _ in shapes]
+    return shapes, B, params
+
+
+def _with_pruned(B, target_pruned):
+    """Copy of a single selector matrix with exactly target_pruned zeros (first in row-major order)."""
+    flat = np.ones(np.asarray(B).size)
+    flat[:target_pruned] = 0.0
+    return flat.reshape(np.asarray(B).shape)
+
+
+def test_budget_loss_vanishes_at_the_target():
+    B = _with_pruned(np.zeros((40, 25)), 400)  # s = 0.4 exactly
+    for uniform in (False, True):
+        L, coeff, kept = oracle.budget_loss([B], [40 * 25 * 256], 0.4, 16.0, uniform)
+        assert L == 0.0 and np.all(coeff == 0.0) and kept[0] == 600
+
+
+def test_budget_loss_depends_only_on_the_ratio():
+    # Sec. 2.3: s = c s_t and s = s_t / c get the same penalty.
+    s_t, c, G = 0.4, 1.25, 1000
+    Lhi, _, _ = oracle.budget_loss([_with_pruned(np.zeros(G), int(round(c * s_t * G)))], [G * 256], s_t, 16.0)
+    Llo, _, _ = oracle.budget_loss([_with_pruned(np.zeros(G), int(round(s_t / c * G)))], [G * 256], s_t, 16.0)
+    assert Lhi > 0 and abs(Lhi - Llo) <= 1e-12 * Lhi
+    assert abs(Lhi - 16.0 * math.log(c)) <= 1e-12
+
+
+def test_budget_global_sparsity_is_the_fraction_of_pruned_weights():
+    # Eq. 2 weights s^l by d_out d_in: the result is the fraction of zero
+    # weights over every element of every layer, counted after expansion.
+    shapes, B, params = _budget_layers()
+    zeros = sum(float(np.sum(oracle.expand_mask(b, g) == 0)) for b, (_, _, g) in zip(B, shapes))
+    total = float(sum(params))
+    s_elem = zeros / total
+    L, _, _ = oracle.budget_loss(B, params, 0.5, 16.0)
+    assert abs(L - 16.0 * abs(math.log(s_elem / 0.5))) <= 1e-12
+
+
+@pytest.mark.parametrize("uniform", [False, True])
+def test_budget_gradient_matches_selector_flips(uniform):
+    # Central difference in the kept count: one selector of layer l goes from
+    # 1 to 0 (B-) and another from 0 to 1 (B+); (L(B+) - L(B-)) / 2 is dL/dB^l
+    # up to the curvature of the log over one flip, relative (ds/s)^2 / 3 with
+    # ds/s below 5e-3 for these layers, so 1e-4 is a safe bound.
+    shapes, B, params = _budget_layers()
+    _, coeff, _ = oracle.budget_loss(B, params, 0.5, 16.0, uniform)
+    for l in range(len(B)):
+        flat = B[l].ravel()
+        on, off = int(np.flatnonzero(flat)[0]), int(np.flatnonzero(flat == 0)[0])
+        Bp = [b.copy() for b in B]
+        Bm = [b.copy() for b in B]
+        Bp[l].ravel()[off] = 1.0
+        Bm[l].ravel()[on] = 0.0
+        Lp, _, _ = oracle.budget_loss(Bp, params, 0.5, 16.0, uniform)
+        Lm, _, _ = oracle.budget_loss(Bm, params, 0.5, 16.0, uniform)
+        fd = (Lp - Lm) / 2.0
+        assert abs(fd - coeff[l]) <= 1e-4 * abs(coeff[l]) + 1e-15, (l, fd, coeff[l])
+
+
+def test_budget_uniform_variant_is_the_sum_of_single_layer_losses():
+    shapes, B, params = _budget_layers()
+    Lu, cu, _ = oracle.budget_loss(B, params, 0.5, 16.0, uniform=True)
+    singles = [oracle.budget_loss([b], [p], 0.5, 16.0) for b, p in zip(B, params)]
+    assert abs(Lu - sum(x[0] for x in singles)) <= 1e-12 * Lu
+    assert np.allclose(cu, [x[1][0] for x in singles], rtol=1e-12, atol=0)
+
+
 # ------------------------------------------------------- the pins catch mistakes
 
 def _mutant_fwd_strided_groups(X, W, B, g):
@@ -379,6 +453,26 @@ def _mutant_sparsity_unweighted(selectors, shapes):
     return s_l, float(np.mean(s_l))
 
 
+_ORIG_BUDGET = oracle.budget_loss
+
+
+def _mutant_budget_unweighted(selectors, params, s_target, lam, uniform=False):
+    return _ORIG_BUDGET(selectors, [1] * len(params), s_target, lam, uniform)
+
+
+def _mutant_budget_grad_sign(selectors, params, s_target, lam, uniform=False):
+    L, c, k = _ORIG_BUDGET(selectors, params, s_target, lam, uniform)
+    return L, -c, k
+
+
+def _mutant_budget_grad_no_inv_s(selectors, params, s_target, lam, uniform=False):
+    L, c, k = _ORIG_BUDGET(selectors, params, s_target, lam, uniform)
+    G = np.array([np.asarray(B).size for B in selectors], float)
+    s_l = 1.0 - k / G
+    s = float(np.sum(s_l * np.array(params, float)) / np.sum(np.array(params, float)))
+    return L, c * (s_l if uniform else s), k
+
+
 MUTANTS = [
     ("linear_fwd", _mutant_fwd_strided_groups),
     ("linear_bwd_dgate", _mutant_dgate_no_weight),
@@ -388,6 +482,9 @@ MUTANTS = [
     ("gate", _mutant_gate_ge),
     ("gate_bwd", _mutant_ste_no_tau),
     ("sparsity", _mutant_sparsity_unweighted),
+    ("budget_loss", _mutant_budget_unweighted),
+    ("budget_loss", _mutant_budget_grad_sign),
+    ("budget_loss", _mutant_budget_grad_no_inv_s),
 ]
 
 PIN_TESTS = [
@@ -402,6 +499,10 @@ PIN_TESTS = [
     test_ste_derivative_matches_finite_difference_of_relaxation,
     test_paper_category_rates_reproduce_global_rate,
     test_budgeted_inputs_give_exact_kept_count,
+    test_budget_loss_depends_only_on_the_ratio,
+    test_budget_global_sparsity_is_the_fraction_of_pruned_weights,
+    lambda: test_budget_gradient_matches_selector_flips(False),
+    lambda: test_budget_gradient_matches_selector_flips(True),
 ]
 
 
