@@ -220,6 +220,46 @@ def _gemv_bandwidth(n_layers, reps):
             "bytes_per_pass": total, "ms_per_pass": ms, "launches_per_pass": len(mats)}
 
 
+# ------------------------------------------------------------------ budget regulariser
+
+def _budget_bandwidth(reps):
+    """Sparsity-budget regulariser over the 224 selector matrices of LLaMA-2-7B (one flat array)."""
+    import torch
+    import paper_2609_33977_amd as gm
+    import workloads
+    cfg = workloads.config("llama2_7b_step")
+    g = cfg["g"]
+    shapes = [(do, di) for _ in range(cfg["layers"]) for _, do, di in cfg["linears"]]
+    sizes = [do * di // g for do, di in shapes]
+    n = sum(sizes)
+    offsets = torch.tensor(np.concatenate([[0], np.cumsum(sizes)]), dtype=torch.int64, device="cuda")
+    params = torch.tensor([do * di for do, di in shapes], dtype=torch.int64, device="cuda")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(workloads.SEED)
+    mask = (torch.rand(n, device="cuda", generator=gen) < 0.5).float()
+    y = torch.rand(n, device="cuda", generator=gen) * 0.98 + 0.01
+    dgate = torch.randn(n, device="cuda", generator=gen)
+    dlog = torch.empty_like(dgate)
+    L = len(sizes)
+    kept = torch.empty(L, dtype=torch.int64, device="cuda")
+    loss = torch.empty(1, dtype=torch.float64, device="cuda")
+    coeff = torch.empty(L, dtype=torch.float32, device="cuda")
+
+    def reg():
+        gm.gm_budget_loss(mask, offsets, params, 0.5, 16.0, False, kept, loss, coeff)
+
+    def bwd():
+        gm.gm_gate_bwd_budget(dgate, y, cfg["tau"], offsets, coeff, dlog)
+
+    reg(); bwd()
+    torch.cuda.synchronize()
+    t_reg = _events_ms(reg, reps)
+    t_bwd = _events_ms(bwd, reps)
+    return {"workload": f"LLaMA-2-7B: {L} selector matrices, {n} selectors in one flat array, lambda 16, s_t 0.5",
+            "loss_ms": t_reg, "loss_GB/s": 4.0 * n / (t_reg / 1e3) / 1e9,
+            "gate_bwd_budget_ms": t_bwd, "gate_bwd_budget_GB/s": 12.0 * n / (t_bwd / 1e3) / 1e9}
+
+
 # ------------------------------------------------------------------ main
 
 def main():
@@ -275,6 +315,8 @@ def main():
     if not args.no_gemv:
         gemv = _gemv_bandwidth(args.gemv_layers, max(3, args.steps // 4))
 
+    budget = _budget_bandwidth(max(5, args.steps))
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = _cpu_baseline(case, flops_step, args.cpu_seconds)
@@ -305,6 +347,7 @@ def main():
                     "fwd_kept_tflops": fwd_tflops, "breakdown_ms": breakdown},
         "cpu_baseline": cpu,
         "gemv": gemv,
+        "budget": budget,
     }
     print(json.dumps(out), flush=True)
 

@@ -15,7 +15,9 @@
  *     convention: X [T, d_in], W [d_out, d_in], Y / dY [T, d_out],
  *     mask / dgate [d_out, G_in].
  *   - Every pointer argument is a DEVICE pointer unless stated otherwise, and
- *     must be 16-byte aligned.  The caller owns every buffer; the library never
+ *     must be 16-byte aligned unless stated otherwise (the per-layer arrays of
+ *     the budget calls need only their element alignment).  The caller owns
+ *     every buffer; the library never
  *     allocates or frees device memory.  Scratch space is passed in as a
  *     caller-owned workspace sized by gm_workspace_size().
  *   - Every call validates its arguments before launching anything and returns
@@ -96,6 +98,50 @@ gm_status gm_gate(const float* logits, const float* noise, int64_t n, float tau,
  */
 gm_status gm_gate_bwd(const float* dmask, const float* soft, int64_t n, float tau, float* dlogits,
                       gm_stream_t stream);
+
+/*
+ * gm_budget_loss -- sparsity-budget regulariser (Sec. 2.3) of L layers on
+ * their discrete selectors, with Eq. 2's layer-wise and parameter-weighted
+ * sparsity.  The selectors of all layers lie back to back in one flat array
+ * (the layout gm_gate accepts): layer l owns mask[offsets[l] .. offsets[l+1]).
+ *   kept[l] = number of selectors of layer l with mask != 0 (exact)
+ *   s^l = 1 - kept[l] / G^l (G^l = offsets[l+1] - offsets[l]),
+ *   s   = sum_l s^l params[l] / sum_l params[l]
+ *   uniform == 0:  loss = lambda |log(s / s_target)|
+ *                  coeff[l] = lambda sgn(log(s/s_target)) / s * (-(params[l] / G^l) / sum_k params[k])
+ *   uniform == 1:  loss = sum_l lambda |log(s^l / s_target)|
+ *                  coeff[l] = lambda sgn(log(s^l/s_target)) / s^l * (-1 / G^l)
+ * coeff[l] is d loss / d selector for every selector of layer l (sgn(0) = 0);
+ * gm_gate_bwd_budget folds it into the logit gradient.  A sparsity of 0
+ * makes the loss and coefficient infinite.  loss and the sums are fp64.
+ *   mask    [n] fp32 (device), n >= 1, 16-byte aligned
+ *   offsets [L + 1] int64 (device, 8-byte aligned): offsets[0] = 0, strictly
+ *           increasing, offsets[L] = n (not checked: wrong offsets give wrong
+ *           sums, never an access outside mask)
+ *   params  [L] int64 (device, 8-byte aligned): weights per layer, d_out * d_in, >= 1
+ *   L >= 1; 0 < s_target < 1; lambda >= 0 and finite; uniform in {0, 1}
+ *   kept  [L] uint64 (device, 8-byte aligned, output; cleared by the call)
+ *   loss  [1] fp64 (device, 8-byte aligned, output)
+ *   coeff [L] fp32 (device, 4-byte aligned, output)
+ * Three launches on `stream`: clear kept, count (HBM bound, 4 bytes per
+ * selector), finalize (one block).
+ */
+gm_status gm_budget_loss(const float* mask, int64_t n, const int64_t* offsets, const int64_t* params, int32_t L,
+                         float s_target, float lambda, int uniform, uint64_t* kept, double* loss, float* coeff,
+                         gm_stream_t stream);
+
+/*
+ * gm_gate_bwd_budget -- gm_gate_bwd with the regulariser's gradient added to
+ * the selector gradient (Sec. 2.2 and 2.3):
+ *   dlogits[j] = (dgate[j] + coeff[l(j)]) * y[j] * (1 - y[j]) / tau,
+ * with l(j) the layer owning selector j under `offsets` (as in gm_budget_loss).
+ *   dgate, soft, dlogits: [n] fp32 (device), 16-byte aligned, n >= 1;
+ *   dlogits may alias dgate.  offsets [L + 1] int64 (device, 8-byte aligned),
+ *   coeff [L] fp32 (device, 4-byte aligned).
+ *   L >= 1; tau > 0 and finite.
+ */
+gm_status gm_gate_bwd_budget(const float* dgate, const float* soft, int64_t n, float tau, const int64_t* offsets,
+                             int32_t L, const float* coeff, float* dlogits, gm_stream_t stream);
 
 /*
  * gm_workspace_size -- host-only query of the workspace (bytes) that

@@ -17,7 +17,8 @@ GM_OK, GM_ERR_NULL, GM_ERR_SHAPE, GM_ERR_VALUE, GM_ERR_ALIGN, GM_ERR_WORKSPACE, 
 GM_OP_FWD, GM_OP_BWD = 0, 1
 
 EXPORTS = (
-    "gm_abi_version", "gm_status_string", "gm_gate", "gm_gate_bwd", "gm_workspace_size",
+    "gm_abi_version", "gm_status_string", "gm_gate", "gm_gate_bwd", "gm_budget_loss", "gm_gate_bwd_budget",
+    "gm_workspace_size",
     "gm_masked_linear_fwd", "gm_masked_linear_bwd", "gm_pack_rows", "gm_packed_linear_fwd",
 )
 
@@ -38,6 +39,8 @@ def _load() -> ctypes.CDLL:
         "gm_status_string": ([ctypes.c_int], ctypes.c_char_p),
         "gm_gate": ([P, P, I64, F32, ctypes.c_int, P, P, P], ctypes.c_int),
         "gm_gate_bwd": ([P, P, I64, F32, P, P], ctypes.c_int),
+        "gm_budget_loss": ([P, I64, P, P, I32, F32, F32, ctypes.c_int, P, P, P, P], ctypes.c_int),
+        "gm_gate_bwd_budget": ([P, P, I64, F32, P, I32, P, P, P], ctypes.c_int),
         "gm_workspace_size": ([ctypes.c_int, I64, I64, I64, I32, ctypes.POINTER(SZ)], ctypes.c_int),
         "gm_masked_linear_fwd": ([P, P, P, I64, I64, I64, I32, P, P, SZ, P], ctypes.c_int),
         "gm_masked_linear_bwd": ([P, P, P, P, I64, I64, I64, I32, P, P, P, SZ, P], ctypes.c_int),
@@ -91,6 +94,19 @@ def gm_gate(logits, noise, tau: float, hard: bool, mask_out, soft_out=None, stre
 def gm_gate_bwd(dmask, soft, tau: float, dlogits, stream=None) -> None:
     _check(LIB.gm_gate_bwd(_ptr(dmask), _ptr(soft), dmask.numel(), float(tau), _ptr(dlogits), _stream(stream)),
            "gm_gate_bwd")
+
+
+def gm_budget_loss(mask, offsets, params, s_target: float, lam: float, uniform: bool, kept, loss, coeff,
+                   stream=None) -> None:
+    """Sparsity-budget regulariser over the layers of a flat selector array (see gm_budget_loss in the header)."""
+    _check(LIB.gm_budget_loss(_ptr(mask), mask.numel(), _ptr(offsets), _ptr(params), params.numel(), float(s_target),
+                              float(lam), int(bool(uniform)), _ptr(kept), _ptr(loss), _ptr(coeff), _stream(stream)),
+           "gm_budget_loss")
+
+
+def gm_gate_bwd_budget(dgate, soft, tau: float, offsets, coeff, dlogits, stream=None) -> None:
+    _check(LIB.gm_gate_bwd_budget(_ptr(dgate), _ptr(soft), dgate.numel(), float(tau), _ptr(offsets), coeff.numel(),
+                                  _ptr(coeff), _ptr(dlogits), _stream(stream)), "gm_gate_bwd_budget")
 
 
 def gm_workspace_size(op: int, T: int, d_in: int, d_out: int, g: int) -> int:

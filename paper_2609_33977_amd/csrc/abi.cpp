@@ -20,6 +20,8 @@ constexpr int kDecodeTokens = 16;              // forward dispatch: T <= 16 take
 constexpr int64_t kMaxElems = (int64_t(1) << 30) - (int64_t(1) << 22);  // bf16 elements per matrix (< 2 GiB)
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned8(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -125,6 +127,34 @@ GM_EXPORT gm_status gm_gate_bwd(const float* dmask, const float* soft, int64_t n
   if (n == 0) return GM_OK;
   if (gm_status st = check_device()) return st;
   return from_hip(gm::launch_gate_bwd(dmask, soft, n, tau, dlogits, stream));
+}
+
+GM_EXPORT gm_status gm_budget_loss(const float* mask, int64_t n, const int64_t* offsets, const int64_t* params,
+                                   int32_t L, float s_target, float lambda, int uniform, uint64_t* kept, double* loss,
+                                   float* coeff, gm_stream_t stream) {
+  if (!mask || !offsets || !params || !kept || !loss || !coeff) return GM_ERR_NULL;
+  if (n < 1 || L < 1) return GM_ERR_SHAPE;
+  if (!(std::isfinite(s_target) && s_target > 0.0f && s_target < 1.0f)) return GM_ERR_VALUE;
+  if (!(std::isfinite(lambda) && lambda >= 0.0f)) return GM_ERR_VALUE;
+  if (uniform != 0 && uniform != 1) return GM_ERR_VALUE;
+  if (!aligned16(mask) || !aligned8(offsets) || !aligned8(params) || !aligned8(kept) || !aligned8(loss) ||
+      !aligned4(coeff))
+    return GM_ERR_ALIGN;
+  if (gm_status st = check_device()) return st;
+  return from_hip(gm::launch_budget_loss(mask, n, offsets, params, L, s_target, lambda, uniform,
+                                         reinterpret_cast<unsigned long long*>(kept), loss, coeff, stream));
+}
+
+GM_EXPORT gm_status gm_gate_bwd_budget(const float* dgate, const float* soft, int64_t n, float tau,
+                                       const int64_t* offsets, int32_t L, const float* coeff, float* dlogits,
+                                       gm_stream_t stream) {
+  if (!dgate || !soft || !offsets || !coeff || !dlogits) return GM_ERR_NULL;
+  if (n < 1 || L < 1) return GM_ERR_SHAPE;
+  if (gm_status st = check_tau(tau)) return st;
+  if (!aligned16(dgate) || !aligned16(soft) || !aligned16(dlogits) || !aligned8(offsets) || !aligned4(coeff))
+    return GM_ERR_ALIGN;
+  if (gm_status st = check_device()) return st;
+  return from_hip(gm::launch_gate_bwd_budget(dgate, soft, n, tau, offsets, L, coeff, dlogits, stream));
 }
 
 GM_EXPORT gm_status gm_workspace_size(int op, int64_t T, int64_t d_in, int64_t d_out, int32_t g, size_t* bytes) {

@@ -13,6 +13,12 @@ hipError_t launch_gate_fwd(const float* logits, const float* noise, int64_t n, f
 hipError_t launch_gate_bwd(const float* dmask, const float* soft, int64_t n, float tau, float* dlogits,
                            hipStream_t s);
 
+hipError_t launch_budget_loss(const float* mask, int64_t n, const int64_t* offsets, const int64_t* params, int L,
+                              float s_target, float lambda, int uniform, unsigned long long* kept, double* loss,
+                              float* coeff, hipStream_t s);
+hipError_t launch_gate_bwd_budget(const float* dgate, const float* soft, int64_t n, float tau,
+                                  const int64_t* offsets, int L, const float* coeff, float* dlogits, hipStream_t s);
+
 hipError_t launch_col_lists(const float* mask, int d_out, int G_in, int* colcount, int* colsoft, int* rows,
                             float* scales, hipStream_t s);
 hipError_t launch_pack_rows(const uint16_t* W, const float* mask, int d_in, int d_out, int g, int64_t capacity,

@@ -96,6 +96,41 @@ def test_gate_bwd_argument_errors():
     assert L.gm_gate_bwd(FAKE, FAKE, 0, 0.4, FAKE, None) == gm.GM_OK
 
 
+def test_budget_argument_errors():
+    L = gm.LIB
+    ODD8 = ctypes.c_void_p(FAKE.value + 4)  # 4-byte but not 8-byte aligned
+    ok = (FAKE, 64, FAKE, FAKE, 3, 0.5, 16.0, 0, FAKE, FAKE, FAKE, None)
+
+    def call(**kw):
+        names = ("mask", "n", "offsets", "params", "L", "s_t", "lam", "uniform", "kept", "loss", "coeff", "stream")
+        args = dict(zip(names, ok))
+        args.update(kw)
+        return L.gm_budget_loss(*[args[k] for k in names])
+
+    for k in ("mask", "offsets", "params", "kept", "loss", "coeff"):
+        assert call(**{k: None}) == gm.GM_ERR_NULL, k
+    assert call(n=0) == gm.GM_ERR_SHAPE
+    assert call(L=0) == gm.GM_ERR_SHAPE
+    for st in (0.0, 1.0, -0.2, float("nan")):
+        assert call(s_t=st) == gm.GM_ERR_VALUE, st
+    for lam in (-1.0, float("inf"), float("nan")):
+        assert call(lam=lam) == gm.GM_ERR_VALUE, lam
+    assert call(uniform=2) == gm.GM_ERR_VALUE
+    assert call(mask=MISALIGNED) == gm.GM_ERR_ALIGN
+    for k in ("offsets", "params", "kept", "loss"):
+        assert call(**{k: ODD8}) == gm.GM_ERR_ALIGN, k
+
+    bwd = L.gm_gate_bwd_budget
+    assert bwd(None, FAKE, 8, 0.4, FAKE, 2, FAKE, FAKE, None) == gm.GM_ERR_NULL
+    assert bwd(FAKE, FAKE, 8, 0.4, None, 2, FAKE, FAKE, None) == gm.GM_ERR_NULL
+    assert bwd(FAKE, FAKE, 8, 0.4, FAKE, 2, None, FAKE, None) == gm.GM_ERR_NULL
+    assert bwd(FAKE, FAKE, 0, 0.4, FAKE, 2, FAKE, FAKE, None) == gm.GM_ERR_SHAPE
+    assert bwd(FAKE, FAKE, 8, 0.4, FAKE, 0, FAKE, FAKE, None) == gm.GM_ERR_SHAPE
+    assert bwd(FAKE, FAKE, 8, 0.0, FAKE, 2, FAKE, FAKE, None) == gm.GM_ERR_VALUE
+    assert bwd(FAKE, FAKE, 8, 0.4, FAKE, 2, FAKE, MISALIGNED, None) == gm.GM_ERR_ALIGN
+    assert bwd(FAKE, FAKE, 8, 0.4, ODD8, 2, FAKE, FAKE, None) == gm.GM_ERR_ALIGN
+
+
 def test_linear_argument_errors():
     L = gm.LIB
     fwd = L.gm_masked_linear_fwd
