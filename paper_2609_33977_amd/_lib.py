@@ -32,6 +32,11 @@ class GroupMaskError(RuntimeError):
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: build it first (python -m paper_2609_33977_amd.build)")
+    # torch carries its own copy of the HIP runtime and names it without the
+    # version suffix, so the dynamic linker would load the system copy for
+    # this library if it came first; a second runtime in the process sees no
+    # device.  Loading torch first makes this library bind to torch's runtime.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(LIB_PATH)
     P, I64, I32, F32, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float, ctypes.c_size_t
     sigs = {

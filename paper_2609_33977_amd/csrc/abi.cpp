@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 
@@ -25,22 +27,31 @@ bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// With the environment variable GM_DEBUG set, the HIP error behind a
+// GM_ERR_DEVICE status is printed to stderr.
+gm_status device_error(const char* what, hipError_t e) {
+  static const bool debug = std::getenv("GM_DEBUG") != nullptr;
+  if (debug) std::fprintf(stderr, "libgroupmask: %s: HIP error %d (%s)\n", what, int(e), hipGetErrorName(e));
+  return GM_ERR_DEVICE;
+}
+
 // gfx950 check, cached per device.
 gm_status check_device() {
   static std::mutex mu;
   static signed char ok[256];  // 0 unknown, 1 yes, -1 no
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 256) return GM_ERR_DEVICE;
+  if (hipError_t e = hipGetDevice(&dev)) return device_error("hipGetDevice", e);
+  if (dev < 0 || dev >= 256) return device_error("device index", hipErrorInvalidDevice);
   std::lock_guard<std::mutex> lock(mu);
   if (ok[dev] == 0) {
     hipDeviceProp_t prop;
-    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return GM_ERR_DEVICE;
+    if (hipError_t e = hipGetDeviceProperties(&prop, dev)) return device_error("hipGetDeviceProperties", e);
     ok[dev] = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : -1;
   }
-  return ok[dev] == 1 ? GM_OK : GM_ERR_DEVICE;
+  return ok[dev] == 1 ? GM_OK : device_error("not a gfx950 device", hipErrorInvalidDevice);
 }
 
-gm_status from_hip(hipError_t e) { return e == hipSuccess ? GM_OK : GM_ERR_DEVICE; }
+gm_status from_hip(hipError_t e) { return e == hipSuccess ? GM_OK : device_error("kernel launch", e); }
 
 gm_status check_tau(float tau) { return (std::isfinite(tau) && tau > 0.0f) ? GM_OK : GM_ERR_VALUE; }
 

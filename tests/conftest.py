@@ -27,3 +27,21 @@ def pytest_collection_modifyitems(config, items):
     for item in items:
         if "gpu" in item.keywords:
             item.add_marker(skip)
+
+
+@pytest.hookimpl(hookwrapper=True)
+def pytest_runtest_makereport(item, call):
+    # On a failing GPU test, report the HIP runtime's pending error (if any) by name.
+    outcome = yield
+    rep = outcome.get_result()
+    if rep.when == "call" and rep.failed and "gpu" in item.keywords:
+        try:
+            import ctypes
+            hip = ctypes.CDLL("libamdhip64.so")
+            hip.hipGetLastError.restype = ctypes.c_int
+            hip.hipGetErrorName.restype = ctypes.c_char_p
+            code = hip.hipGetLastError()
+            rep.sections.append(("hip", f"pending HIP error after the failure: {code} {hip.hipGetErrorName(code).decode()}"))
+        except OSError:
+            pass
+
