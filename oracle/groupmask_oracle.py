@@ -174,7 +174,7 @@ def budget_loss(selectors, params, s_target: float, lam: float, uniform: bool = 
 
     selectors: list of B^l arrays (nonzero = kept); params: list of P^l, the
     weight count d_out^l d_in^l of each layer.  With G^l = B^l.size groups and
-    s^l, s from Eq. 2:
+    s^l, s from Eq. 2 (evaluated exactly in rationals, then rounded once):
 
       global  : L = lam |log(s / s_t)|
                 dL/dB^l = lam sgn(log(s/s_t)) (1/s) ds/dB^l,  ds/dB^l = -(P^l / G^l) / sum_k P^k
@@ -186,19 +186,22 @@ def budget_loss(selectors, params, s_target: float, lam: float, uniform: bool = 
     Returns (L, coeff, kept) with coeff a float64 array over layers and kept
     the integer kept counts.
     """
+    from fractions import Fraction
     kept = np.array([np.count_nonzero(np.asarray(B)) for B in selectors], dtype=np.int64)
-    G = np.array([np.asarray(B).size for B in selectors], dtype=np.float64)
-    P = np.array(params, dtype=np.float64)
-    s_layer = 1.0 - kept / G
+    Gi = [int(np.asarray(B).size) for B in selectors]
+    Pi = [int(p) for p in params]
+    G = np.array(Gi, dtype=np.float64)
+    P = np.array(Pi, dtype=np.float64)
+    s_layer_exact = [Fraction(g - int(k), g) for g, k in zip(Gi, kept)]
     with np.errstate(divide="ignore"):
         if uniform:
+            s_layer = np.array([float(x) for x in s_layer_exact])
             logs = np.log(s_layer / s_target)
             L = float(np.sum(lam * np.abs(logs)))
             coeff = lam * np.sign(logs) / s_layer * (-1.0 / G)
         else:
-            s = float(np.sum(s_layer * P) / np.sum(P))
+            s = float(sum(x * p for x, p in zip(s_layer_exact, Pi)) / sum(Pi))
             logr = np.log(s / s_target)
             L = float(lam * abs(logr))
             coeff = lam * np.sign(logr) / s * (-(P / G) / np.sum(P))
     return L, coeff, kept
-
