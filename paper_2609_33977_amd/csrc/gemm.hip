@@ -56,6 +56,15 @@ __device__ __forceinline__ void tile_coords(int nblocks, int tiles_m, int tiles_
   tn = r / gm;
 }
 
+// Waves per block of the forward and dgate GEMMs (wave tiles 128 x 128 with 4,
+// 128 x 64 with 8: two waves per SIMD hide each other's copy and barrier time).
+constexpr int kFwdWaves = 8;
+constexpr int kDgateWaves = 8;
+constexpr int kDxWaves = 8;
+// dX: 8 waves for tiles of 128 and 256 rows; the 64-row tile keeps 4 (its W
+// slice is four copies, one per wave).
+constexpr int dx_waves(int bm) { return bm >= 128 ? kDxWaves : 4; }
+
 // LDS pipeline depth (K slices of kBK) per GEMM; the forward also keeps the
 // tile's kept bits in LDS.
 constexpr int kStagesDgate = 4;
@@ -210,13 +219,15 @@ __device__ __forceinline__ void store4_bf16(uint16_t* p, const f32x4& v) {
 
 // C[o, t] over K = d_in, tile 256 (o) x 256 (t); waves 2 (o) x 2 (t).
 template <int G>
-__global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
+__global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
                                                   const float* __restrict__ mask, int T, int d_in, int d_out,
                                                   uint16_t* __restrict__ Y) {
-  constexpr int BM = 256, BN = 256, MB = 8, NB = 8;
-  constexpr int SUB = G / kBK;          // K slices per group column
-  constexpr int MAXG = 512;             // group-column limit (checked by the host)
-  constexpr int PER_STAGE = 8;          // DMA instructions per wave per slice
+  constexpr int NW = kFwdWaves, WN = NW / 2;  // waves per block; wave grid 2 (M) x WN (N)
+  constexpr int BM = 256, BN = 256, MB = 8, NB = BN / WN / 16;
+  constexpr int SUB = G / kBK;                // K slices per group column
+  constexpr int MAXG = 512;                   // group-column limit (checked by the host)
+  constexpr int PER_STAGE = 32 / NW;          // DMA instructions per wave per slice
+  constexpr int CA = PER_STAGE / 2;           // of which copies of the W tile (the rest: X tile)
   constexpr int STAGES = 4;
   __shared__ u32x4 As[STAGES][BM * 4];
   __shared__ u32x4 Bs[STAGES][BN * 4];
@@ -227,7 +238,7 @@ __global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
   const int G_in = d_in / G;
   const int words = (G_in + 31) / 32;
   const int tiles_m = (d_out + BM - 1) / BM, tiles_n = (T + BN - 1) / BN;
@@ -242,7 +253,7 @@ __global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X
     s_cols[0] = 0;  // read (unused) by the zero-fill copies when no column is kept
   }
   __syncthreads();
-  {
+  if (tid < BM) {
     const int o = m0 + tid;
     bool soft = false;
     for (int w = 0; w < words; ++w) {
@@ -273,14 +284,14 @@ __global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X
   __syncthreads();
   const int nst = s_ncols * SUB;
 
-  // This lane's four DMA rows (the same in both tiles): row = 16 (4 wave + j) + lane / 4,
+  // This lane's CA DMA rows (the same in both tiles): row = 16 (CA wave + j) + lane / 4,
   // and their byte offsets within a K slice (out-of-range rows read zeros).
-  int rowj[4];
-  uint32_t offA[4], offB[4];
+  int rowj[CA];
+  uint32_t offA[CA], offB[CA];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < CA; ++j) {
     int c;
-    km_dma_target((wave * 4 + j) * 64 + lane, rowj[j], c);
+    km_dma_target((wave * CA + j) * 64 + lane, rowj[j], c);
     offA[j] = group_voffset(uint32_t((m0 + rowj[j]) * d_in + 8 * c) * 2u, j);
     offB[j] = group_voffset(uint32_t((n0 + rowj[j]) * d_in + 8 * c) * 2u, j);
   }
@@ -296,28 +307,28 @@ __global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X
   auto col_of = [&](int st) { return st < nst ? st / SUB : 0; };  // slices past the end reuse column 0
   int v_cur = __builtin_amdgcn_readfirstlane(s_cols[0]);
   int v_nxt = __builtin_amdgcn_readfirstlane(s_cols[col_of(1)]);
-  uint32_t bits_cur[4];
+  uint32_t bits_cur[CA];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) bits_cur[j] = s_bits[rowj[j]][v_cur >> 5];
-  uint32_t curA[4];
+  for (int j = 0; j < CA; ++j) bits_cur[j] = s_bits[rowj[j]][v_cur >> 5];
+  uint32_t curA[CA];
   i32x4_t rA, rB;
   auto prepare = [&](int st) {
     const bool live = st < nst;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) curA[j] = offA[j] | (((~bits_cur[j] >> (v_cur & 31)) & 1u) << 31);
+    for (int j = 0; j < CA; ++j) curA[j] = offA[j] | (((~bits_cur[j] >> (v_cur & 31)) & 1u) << 31);
     const int k0 = live ? v_cur * G + (st % SUB) * kBK : 0;
     rA = make_rsrc_grouped(W + k0, live ? bytesW - 2u * uint32_t(k0) : 0u);
     rB = make_rsrc_grouped(X + k0, live ? bytesX - 2u * uint32_t(k0) : 0u);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) bits_cur[j] = s_bits[rowj[j]][v_nxt >> 5];
+    for (int j = 0; j < CA; ++j) bits_cur[j] = s_bits[rowj[j]][v_nxt >> 5];
     v_cur = v_nxt;
     v_nxt = __builtin_amdgcn_readfirstlane(s_cols[col_of(st + 2)]);
   };
-  // copies 0..3 fill this wave's four row blocks of the W tile, 4..7 of the X tile
+  // copies 0..CA-1 fill this wave's row blocks of the W tile, CA..2CA-1 of the X tile
   auto issue = [&](int st, int p) {
-    const int j = p & 3;
-    const uint32_t dst = (st % STAGES) * (BM * 64) + wave * 4 * 1024;
-    if (p < 4)
+    const int j = p % CA;
+    const uint32_t dst = (st % STAGES) * (BM * 64) + wave * CA * 1024;
+    if (p < CA)
       dma16_group(j, rA, curA[j], ldsA + dst);
     else
       dma16_group(j, rB, offB[j], ldsB + dst);
@@ -326,13 +337,13 @@ __global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X
   auto rescale = [&](int st) {
     const int v = s_cols[st / SUB];
     u32x4* A = As[st % STAGES];
-    float m[4];
+    float m[CA];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) m[j] = m0 + rowj[j] < d_out ? mask[int64_t(m0 + rowj[j]) * G_in + v] : 0.0f;
+    for (int j = 0; j < CA; ++j) m[j] = m0 + rowj[j] < d_out ? mask[int64_t(m0 + rowj[j]) * G_in + v] : 0.0f;
     wait_vmcnt<0>();
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      u32x4* p = A + (wave * 4 + j) * 64 + lane;
+    for (int j = 0; j < CA; ++j) {
+      u32x4* p = A + (wave * CA + j) * 64 + lane;
       if (m[j] != 0.0f && m[j] != 1.0f) *p = scale_bf16x8(*p, m[j]);
     }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
@@ -341,18 +352,18 @@ __global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X
   // Hard masks (the common case) run a loop without the rescaling step.
   f32x4 acc[MB][NB];
   if (s_soft)
-    gemm_mainloop<MB, NB, true, true, 0, 0, PER_STAGE, STAGES>(As, Bs, nst, wm * 128, wn * 128, lane, acc, prepare, issue,
-                                                       rescale, [](int, const u32x4(&)[NB]) {});
+    gemm_mainloop<MB, NB, true, true, 0, 0, PER_STAGE, STAGES>(As, Bs, nst, wm * 128, wn * NB * 16, lane, acc, prepare,
+                                                              issue, rescale, [](int, const u32x4(&)[NB]) {});
   else
-    gemm_mainloop<MB, NB, true, true, 0, 0, PER_STAGE, STAGES>(As, Bs, nst, wm * 128, wn * 128, lane, acc, prepare, issue,
-                                                       [](int) {}, [](int, const u32x4(&)[NB]) {});
+    gemm_mainloop<MB, NB, true, true, 0, 0, PER_STAGE, STAGES>(As, Bs, nst, wm * 128, wn * NB * 16, lane, acc, prepare,
+                                                              issue, [](int) {}, [](int, const u32x4(&)[NB]) {});
 
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       const int o = m0 + wm * 128 + mb * 16 + 4 * (lane >> 4);
-      const int t = n0 + wn * 128 + nb * 16 + (lane & 15);
+      const int t = n0 + wn * NB * 16 + nb * 16 + (lane & 15);
       if (t < T && o < d_out) store4_bf16(Y + int64_t(t) * d_out + o, acc[mb][nb]);
     }
 }
@@ -364,18 +375,20 @@ __global__ __launch_bounds__(256) void fwd_kernel(const uint16_t* __restrict__ X
 // group spans two tiles, each adding its half onto a zeroed dgate (two
 // addends onto zero: the same sum whichever lands first).
 template <int G>
-__global__ __launch_bounds__(256) void dgate_kernel(const uint16_t* __restrict__ dY, const uint16_t* __restrict__ X,
+__global__ __launch_bounds__(64 * kDgateWaves) void dgate_kernel(const uint16_t* __restrict__ dY, const uint16_t* __restrict__ X,
                                                     const uint16_t* __restrict__ W, int T, int d_in, int d_out,
                                                     float* __restrict__ dgate, uint16_t* __restrict__ dYt, int ldt) {
-  constexpr int BM = 256, BN = 256, MB = 8, NB = 8;
-  constexpr int PER_STAGE = 8;
+  constexpr int NW = kDgateWaves, WN = NW / 2;  // waves per block; wave grid 2 (i) x WN (o)
+  constexpr int BM = 256, BN = 256, MB = 8, NB = BN / WN / 16;
+  constexpr int PER_STAGE = 32 / NW;
+  constexpr int CA = PER_STAGE / 2;  // copies of the X tile per wave (the rest: dY tile)
   constexpr int STAGES = kStagesDgate;
   __shared__ u32x4 As[STAGES][kBK * BM / 8];
   __shared__ u32x4 Bs[STAGES][kBK * BN / 8];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
   const int G_in = d_in / G;
   const int tiles_m = (d_in + BM - 1) / BM, tiles_n = (d_out + BN - 1) / BN;
   int tm, tn;
@@ -385,11 +398,11 @@ __global__ __launch_bounds__(256) void dgate_kernel(const uint16_t* __restrict__
 
   // Byte offsets of this lane's DMA chunks within a K slice (columns past the
   // matrix read zeros; rows past T fall outside the slice's range).
-  uint32_t offA[4], offB[4];
+  uint32_t offA[CA], offB[CA];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < CA; ++j) {
     int row, c;
-    mn_dma_target<256>((wave * 4 + j) * 64 + lane, row, c);
+    mn_dma_target<256>((wave * CA + j) * 64 + lane, row, c);
     offA[j] = group_voffset(m0 + 8 * c < d_in ? uint32_t(row * d_in + m0 + 8 * c) * 2u : kOOB, j);
     offB[j] = group_voffset(n0 + 8 * c < d_out ? uint32_t(row * d_out + n0 + 8 * c) * 2u : kOOB, j);
   }
@@ -404,16 +417,16 @@ __global__ __launch_bounds__(256) void dgate_kernel(const uint16_t* __restrict__
   };
   const uint32_t ldsA = lds_addr(As), ldsB = lds_addr(Bs);
   auto issue = [&](int st, int p) {
-    const int j = p & 3;
-    const uint32_t dst = (st % STAGES) * (kBK * BM * 2) + wave * 4 * 1024;
-    if (p < 4)
+    const int j = p % CA;
+    const uint32_t dst = (st % STAGES) * (kBK * BM * 2) + wave * CA * 1024;
+    if (p < CA)
       dma16_group(j, rA, offA[j], ldsA + dst);
     else
       dma16_group(j, rB, offB[j], ldsB + dst);
   };
 
   // dY^T side output (for the dX GEMM): lane (G, i) of a B fragment holds
-  // dY[k0 + 8 G .. k0 + 8 G + 7, o] for o = n0 + wn*128 + nb*16 + i, which is a
+  // dY[k0 + 8 G .. k0 + 8 G + 7, o] for o = n0 + wn*NB*16 + nb*16 + i, which is a
   // 16-byte chunk of row o of dY^T.  The tiles sharing this dY panel split
   // the slices between them (slice kt goes to tile row kt * tiles_m / nst), and
   // within a tile the two wave rows, which hold the same B fragments, alternate.
@@ -423,14 +436,14 @@ __global__ __launch_bounds__(256) void dgate_kernel(const uint16_t* __restrict__
     if (t >= ldt) return;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      const int o = n0 + wn * 128 + nb * 16 + (lane & 15);
+      const int o = n0 + wn * NB * 16 + nb * 16 + (lane & 15);
       if (o < d_out) st16(dYt + int64_t(o) * ldt + t, bf[nb]);
     }
   };
 
   f32x4 acc[MB][NB];
-  gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE, STAGES>(As, Bs, nst, wm * 128, wn * 128, lane, acc, prepare,
-                                                        issue, [](int) {}, bhook);
+  gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE, STAGES>(As, Bs, nst, wm * 128, wn * NB * 16, lane, acc,
+                                                                 prepare, issue, [](int) {}, bhook);
 
   // Epilogue.  Lane (l >> 4, l & 15) holds, for every (mb, nb), rows
   // i = i0 .. i0 + 3 of column o: W[o, i0 .. i0 + 3] is one 8-byte load.
@@ -438,7 +451,7 @@ __global__ __launch_bounds__(256) void dgate_kernel(const uint16_t* __restrict__
   float part[NB][2];  // per o column: group sums over this wave's first / second 64 rows of i
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
-    const int o = n0 + wn * 128 + nb * 16 + (lane & 15);
+    const int o = n0 + wn * NB * 16 + nb * 16 + (lane & 15);
     float s0 = 0.0f, s1 = 0.0f;
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
@@ -462,7 +475,7 @@ __global__ __launch_bounds__(256) void dgate_kernel(const uint16_t* __restrict__
     if (lane < 16) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
-        const int o = n0 + wn * 128 + nb * 16 + lane;
+        const int o = n0 + wn * NB * 16 + nb * 16 + lane;
         const int v = (m0 + wm * 128) / 64;
         if (o < d_out && v < G_in) dgate[int64_t(o) * G_in + v] = part[nb][0];
         if (o < d_out && v + 1 < G_in) dgate[int64_t(o) * G_in + v + 1] = part[nb][1];
@@ -472,7 +485,7 @@ __global__ __launch_bounds__(256) void dgate_kernel(const uint16_t* __restrict__
     if (lane < 16) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
-        const int o = n0 + wn * 128 + nb * 16 + lane;
+        const int o = n0 + wn * NB * 16 + nb * 16 + lane;
         const int v = (m0 + wm * 128) / 128;
         if (o < d_out && v < G_in) dgate[int64_t(o) * G_in + v] = part[nb][0] + part[nb][1];
       }
@@ -484,11 +497,11 @@ __global__ __launch_bounds__(256) void dgate_kernel(const uint16_t* __restrict__
     __syncthreads();
     if (lane < 16) {
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) s_part[wm][wn * 128 + nb * 16 + lane] = part[nb][0] + part[nb][1];
+      for (int nb = 0; nb < NB; ++nb) s_part[wm][wn * NB * 16 + nb * 16 + lane] = part[nb][0] + part[nb][1];
     }
     __syncthreads();
     const int o = n0 + tid;
-    if (o < d_out) {
+    if (tid < BN && o < d_out) {
       const float h = s_part[0][tid] + s_part[1][tid];
       if constexpr (G == 256)
         dgate[int64_t(o) * G_in + m0 / 256] = h;
@@ -511,21 +524,24 @@ __global__ __launch_bounds__(256) void zero_f32_kernel(float* __restrict__ p, in
 // list is read with scalar loads (eight entries per wave per slice), one slice
 // ahead of its DMA.
 template <int BM>
-__global__ __launch_bounds__(256) void dx_kernel(const uint16_t* __restrict__ dYt, int ldt,
+__global__ __launch_bounds__(64 * dx_waves(BM)) void dx_kernel(const uint16_t* __restrict__ dYt, int ldt,
                                                  const uint16_t* __restrict__ W, const int* __restrict__ colcount,
                                                  const int* __restrict__ rows, const float* __restrict__ scales,
                                                  const int* __restrict__ colsoft, int T, int d_in, int d_out, int g,
                                                  uint16_t* __restrict__ dX) {
-  constexpr int BN = 256, MB = BM / 32, NB = 8;
-  constexpr int NA = BM / 64;            // A DMA instructions per wave per slice
-  constexpr int PER_STAGE = NA + 4;
+  constexpr int NW = dx_waves(BM), WN = NW / 2;  // waves per block; wave grid 2 (i) x WN (t)
+  constexpr int BN = 256, MB = BM / 32, NB = BN / WN / 16;
+  constexpr int KR = kBK / NW;               // k-rows of a slice gathered by one wave
+  constexpr int NA = BM / 16 / NW;           // A DMA instructions per wave per slice
+  constexpr int NBC = BN / 16 / NW;          // B DMA instructions per wave per slice
+  constexpr int PER_STAGE = NA + NBC;
   constexpr int STAGES = kStagesDx;
   __shared__ u32x4 As[STAGES][kBK * BM / 8];
   __shared__ u32x4 Bs[STAGES][kBK * BN / 8];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
   const int tiles_m = d_in / BM, tiles_n = (T + BN - 1) / BN;
   int tm, tn;
   tile_coords(gridDim.x, tiles_m, tiles_n, tm, tn);
@@ -537,17 +553,17 @@ __global__ __launch_bounds__(256) void dx_kernel(const uint16_t* __restrict__ dY
   const float* __restrict__ sl = scales + int64_t(v) * d_out;
   const int nst = (kv + kBK - 1) / kBK;
 
-  // Slice st uses k-rows st*32 + r; this wave gathers rows r = 8 wave .. 8 wave + 7,
+  // Slice st uses k-rows st*32 + r; this wave gathers rows r = KR wave .. KR wave + KR - 1,
   // whose list entries are read with scalar loads one slice ahead.
-  int idx[8];
+  int idx[KR];
   auto load_idx = [&](int st) {  // st <= nst: at most 31 + 32 entries past the column's end
-    const int base = st * kBK + wave * 8;
+    const int base = st * kBK + wave * KR;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) idx[q] = rl[base + q];  // uniform: scalar loads
+    for (int q = 0; q < KR; ++q) idx[q] = rl[base + q];  // uniform: scalar loads
   };
-  // Copy j of a tile with C columns (CPR = C / 8 chunks per k-row) covers
-  // k-rows 8 wave + j * RPI + lane / CPR, RPI = 64 / CPR: the lane's row is
-  // one of RPI consecutive list entries.
+  // Copy j of a wave in a tile with C columns (CPR = C / 8 chunks per k-row)
+  // covers k-rows KR wave + j * RPI + lane / CPR, RPI = 64 / CPR: the lane's
+  // row is one of RPI consecutive list entries of the wave.
   auto pick = [&](int j, int rpi, int u) {
     int o = idx[j * rpi];
     for (int q = 1; q < rpi; ++q) o = u == q ? idx[j * rpi + q] : o;
@@ -556,7 +572,7 @@ __global__ __launch_bounds__(256) void dx_kernel(const uint16_t* __restrict__ dY
   constexpr int RPI_A = 512 / BM, RPI_B = 512 / BN;
   const i32x4_t rA = make_rsrc_grouped(W + m0, (uint32_t(d_out) * uint32_t(d_in) - uint32_t(m0)) * 2u);
   const i32x4_t rB = make_rsrc_grouped(dYt + n0, (uint32_t(d_out) * uint32_t(ldt) - uint32_t(n0)) * 2u);
-  uint32_t offA[NA], offB[4];  // this slice's per-lane offsets (rows past the list read zeros)
+  uint32_t offA[NA], offB[NBC];  // this slice's per-lane offsets (rows past the list read zeros)
   auto prepare = [&](int st) {
     const int k0 = st * kBK;
 #pragma unroll
@@ -567,20 +583,20 @@ __global__ __launch_bounds__(256) void dx_kernel(const uint16_t* __restrict__ dY
       offA[j] = group_voffset(uint32_t(o * d_in + 8 * c) * 2u | uint32_t(k0 + row >= kv) << 31, j);
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < NBC; ++j) {
       int row, c;
-      mn_dma_target<BN>((wave * 4 + j) * 64 + lane, row, c);
+      mn_dma_target<BN>((wave * NBC + j) * 64 + lane, row, c);
       const int o = pick(j, RPI_B, lane / (BN / 8));
       offB[j] = group_voffset(uint32_t(o * ldt + 8 * c) * 2u | uint32_t(k0 + row >= kv || n0 + 8 * c >= ldt) << 31, j);
     }
     load_idx(min(st + 1, nst));
   };
   const uint32_t ldsA = lds_addr(As), ldsB = lds_addr(Bs);
-  auto issue = [&](int st, int p) {  // copies 0 .. NA-1: W tile, NA .. NA+3: dY^T tile
+  auto issue = [&](int st, int p) {  // copies 0 .. NA-1: W tile, NA .. NA+NBC-1: dY^T tile
     if (p < NA)
       dma16_group(p, rA, offA[p], ldsA + (st % STAGES) * (kBK * BM * 2) + wave * NA * 1024);
     else
-      dma16_group(p - NA, rB, offB[p - NA], ldsB + (st % STAGES) * (kBK * BN * 2) + wave * 4 * 1024);
+      dma16_group(p - NA, rB, offB[p - NA], ldsB + (st % STAGES) * (kBK * BN * 2) + wave * NBC * 1024);
   };
   // Soft selectors: scale this lane's landed W chunks by the row's mask value.
   auto rescale = [&](int st) {
@@ -604,10 +620,10 @@ __global__ __launch_bounds__(256) void dx_kernel(const uint16_t* __restrict__ dY
   f32x4 acc[MB][NB];
   load_idx(0);
   if (soft)
-    gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE, STAGES>(As, Bs, nst, wm * (BM / 2), wn * 128, lane, acc,
+    gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE, STAGES>(As, Bs, nst, wm * (BM / 2), wn * NB * 16, lane, acc,
                                                           prepare, issue, rescale, [](int, const u32x4(&)[NB]) {});
   else
-    gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE, STAGES>(As, Bs, nst, wm * (BM / 2), wn * 128, lane, acc,
+    gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE, STAGES>(As, Bs, nst, wm * (BM / 2), wn * NB * 16, lane, acc,
                                                           prepare, issue, [](int) {},
                                                           [](int, const u32x4(&)[NB]) {});
 
@@ -616,7 +632,7 @@ __global__ __launch_bounds__(256) void dx_kernel(const uint16_t* __restrict__ dY
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       const int i = m0 + wm * (BM / 2) + mb * 16 + 4 * (lane >> 4);
-      const int t = n0 + wn * 128 + nb * 16 + (lane & 15);
+      const int t = n0 + wn * NB * 16 + nb * 16 + (lane & 15);
       if (t < T) store4_bf16(dX + int64_t(t) * d_in + i, acc[mb][nb]);
     }
 }
@@ -645,19 +661,19 @@ __global__ __launch_bounds__(256) void transpose_kernel(const uint16_t* __restri
 
 // ============================================================================ launchers
 
-#define GM_LAUNCH_G(KERNEL, GRID, ...)                                                        \
-  switch (g) {                                                                                \
-    case 64: hipLaunchKernelGGL(KERNEL<64>, dim3(GRID), dim3(256), 0, s, __VA_ARGS__); break;   \
-    case 128: hipLaunchKernelGGL(KERNEL<128>, dim3(GRID), dim3(256), 0, s, __VA_ARGS__); break; \
-    case 256: hipLaunchKernelGGL(KERNEL<256>, dim3(GRID), dim3(256), 0, s, __VA_ARGS__); break; \
-    case 512: hipLaunchKernelGGL(KERNEL<512>, dim3(GRID), dim3(256), 0, s, __VA_ARGS__); break; \
-    default: return hipErrorInvalidValue;                                                     \
+#define GM_LAUNCH_G(KERNEL, GRID, THREADS, ...)                                                       \
+  switch (g) {                                                                                        \
+    case 64: hipLaunchKernelGGL(KERNEL<64>, dim3(GRID), dim3(THREADS), 0, s, __VA_ARGS__); break;   \
+    case 128: hipLaunchKernelGGL(KERNEL<128>, dim3(GRID), dim3(THREADS), 0, s, __VA_ARGS__); break; \
+    case 256: hipLaunchKernelGGL(KERNEL<256>, dim3(GRID), dim3(THREADS), 0, s, __VA_ARGS__); break; \
+    case 512: hipLaunchKernelGGL(KERNEL<512>, dim3(GRID), dim3(THREADS), 0, s, __VA_ARGS__); break; \
+    default: return hipErrorInvalidValue;                                                             \
   }
 
 hipError_t launch_fwd(const uint16_t* X, const uint16_t* W, const float* mask, int T, int d_in, int d_out, int g,
                       uint16_t* Y, hipStream_t s) {
   const int tiles = ((T + 255) / 256) * ((d_out + 255) / 256);
-  GM_LAUNCH_G(fwd_kernel, tiles, X, W, mask, T, d_in, d_out, Y)
+  GM_LAUNCH_G(fwd_kernel, tiles, 64 * kFwdWaves, X, W, mask, T, d_in, d_out, Y)
   return hipGetLastError();
 }
 
@@ -671,7 +687,7 @@ hipError_t launch_dgate(const uint16_t* dY, const uint16_t* X, const uint16_t* W
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  GM_LAUNCH_G(dgate_kernel, tiles, dY, X, W, T, d_in, d_out, dgate, dYt, ldt)
+  GM_LAUNCH_G(dgate_kernel, tiles, 64 * kDgateWaves, dY, X, W, T, d_in, d_out, dgate, dYt, ldt)
   return hipGetLastError();
 }
 
@@ -687,9 +703,9 @@ hipError_t launch_dx(const uint16_t* dYt, int ldt, const uint16_t* W, const int*
   const int bm = g < 256 ? g : 256;
   const int tiles = (d_in / bm) * ((T + 255) / 256);
   switch (bm) {
-    case 64: hipLaunchKernelGGL(dx_kernel<64>, dim3(tiles), dim3(256), 0, s, dYt, ldt, W, colcount, rows, scales, colsoft, T, d_in, d_out, g, dX); break;
-    case 128: hipLaunchKernelGGL(dx_kernel<128>, dim3(tiles), dim3(256), 0, s, dYt, ldt, W, colcount, rows, scales, colsoft, T, d_in, d_out, g, dX); break;
-    case 256: hipLaunchKernelGGL(dx_kernel<256>, dim3(tiles), dim3(256), 0, s, dYt, ldt, W, colcount, rows, scales, colsoft, T, d_in, d_out, g, dX); break;
+    case 64: hipLaunchKernelGGL(dx_kernel<64>, dim3(tiles), dim3(64 * dx_waves(64)), 0, s, dYt, ldt, W, colcount, rows, scales, colsoft, T, d_in, d_out, g, dX); break;
+    case 128: hipLaunchKernelGGL(dx_kernel<128>, dim3(tiles), dim3(64 * dx_waves(128)), 0, s, dYt, ldt, W, colcount, rows, scales, colsoft, T, d_in, d_out, g, dX); break;
+    case 256: hipLaunchKernelGGL(dx_kernel<256>, dim3(tiles), dim3(64 * dx_waves(256)), 0, s, dYt, ldt, W, colcount, rows, scales, colsoft, T, d_in, d_out, g, dX); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
