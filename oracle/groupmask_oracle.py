@@ -23,8 +23,8 @@ design notes of the repository):
 * Soft selectors: a fractional mask value scales its group; only exact zeros
   prune.  The paper's forward is binary; this generalisation keeps the soft
   output usable.
-* Groups are 1 x g blocks of consecutive input columns of one output row
-  (Sec. 2.1 with g_out = 1, g_in = g).  ``expand_mask`` also takes g_out > 1.
+* Groups are g_out x g blocks (Sec. 2.1): g consecutive input columns of
+  g_out consecutive output rows; the default 1 x 256 has g_out = 1.
 * dgate is produced for every group, pruned or kept, because the STE passes a
   gradient to every selector; it does not depend on the mask values.
 * Budget regulariser (Sec. 2.3): a selector counts as kept when its mask value
@@ -107,36 +107,39 @@ def masked_weight(W, B, g_in: int, g_out: int = 1) -> np.ndarray:
 
 # ------------------------------------------------------------ masked linear layer
 
-def linear_fwd(X, W, B, g: int) -> np.ndarray:
-    """Student forward of one target linear: Y = X W_hat^T (Eq. 1 applied to nn.Linear)."""
+def linear_fwd(X, W, B, g: int, g_out: int = 1) -> np.ndarray:
+    """Student forward of one target linear: Y = X W_hat^T (Eq. 1 applied to nn.Linear).
+
+    Groups are g_out x g (rows x input columns); B is [d_out / g_out, d_in / g].
+    """
     X = np.asarray(X, dtype=np.float64)
-    return X @ masked_weight(W, B, g).T
+    return X @ masked_weight(W, B, g, g_out).T
 
 
-def linear_bwd_dx(dY, W, B, g: int) -> np.ndarray:
+def linear_bwd_dx(dY, W, B, g: int, g_out: int = 1) -> np.ndarray:
     """Input gradient through the frozen masked weight: dX = dY W_hat."""
-    return np.asarray(dY, dtype=np.float64) @ masked_weight(W, B, g)
+    return np.asarray(dY, dtype=np.float64) @ masked_weight(W, B, g, g_out)
 
 
-def linear_bwd_dgate(dY, X, W, g: int) -> np.ndarray:
-    """Selector gradient: dgate[o, v] = sum over the group's entries of W * (dY^T X).
+def linear_bwd_dgate(dY, X, W, g: int, g_out: int = 1) -> np.ndarray:
+    """Selector gradient: dgate[u, v] = sum over the group's entries of W * (dY^T X).
 
-    Y is linear in each selector, so d<dY, Y>/dB[o, v] = sum_{i in group v} W[o, i] (dY^T X)[o, i];
+    Y is linear in each selector, so d<dY, Y>/dB[u, v] = sum_{o in block u, i in block v} W[o, i] (dY^T X)[o, i];
     the weight itself gets no gradient (frozen, Sec. 2.4).
     """
     dY = np.asarray(dY, dtype=np.float64)
     X = np.asarray(X, dtype=np.float64)
     W = np.asarray(W, dtype=np.float64)
     d_out, d_in = W.shape
-    if d_in % g:
-        raise ValueError("d_in must be a multiple of g")
+    if d_in % g or d_out % g_out:
+        raise ValueError("d_in must be a multiple of g and d_out of g_out")
     G = dY.T @ X
-    return (W * G).reshape(d_out, d_in // g, g).sum(axis=2)
+    return (W * G).reshape(d_out // g_out, g_out, d_in // g, g).sum(axis=(1, 3))
 
 
-def linear_bwd(dY, X, W, B, g: int):
+def linear_bwd(dY, X, W, B, g: int, g_out: int = 1):
     """(dX, dgate) of one masked linear."""
-    return linear_bwd_dx(dY, W, B, g), linear_bwd_dgate(dY, X, W, g)
+    return linear_bwd_dx(dY, W, B, g, g_out), linear_bwd_dgate(dY, X, W, g, g_out)
 
 
 # ------------------------------------------------------ sparsity ratios (Eq. 2)

@@ -34,7 +34,7 @@ def _soft_mask(shape, key, p_zero=0.4):
 
 # ----------------------------------------------------------- brute force (loops)
 
-def _brute_fwd(X, W, B, g):
+def _brute_fwd(X, W, B, g, g_out=1):
     T, d_in = X.shape
     d_out = W.shape[0]
     Y = [[0.0] * d_out for _ in range(T)]
@@ -42,12 +42,12 @@ def _brute_fwd(X, W, B, g):
         for o in range(d_out):
             acc = 0.0
             for i in range(d_in):
-                acc += X[t][i] * W[o][i] * B[o][i // g]
+                acc += X[t][i] * W[o][i] * B[o // g_out][i // g]
             Y[t][o] = acc
     return np.array(Y)
 
 
-def _brute_dx(dY, W, B, g):
+def _brute_dx(dY, W, B, g, g_out=1):
     T, d_out = dY.shape
     d_in = W.shape[1]
     dX = [[0.0] * d_in for _ in range(T)]
@@ -55,49 +55,87 @@ def _brute_dx(dY, W, B, g):
         for i in range(d_in):
             acc = 0.0
             for o in range(d_out):
-                acc += dY[t][o] * W[o][i] * B[o][i // g]
+                acc += dY[t][o] * W[o][i] * B[o // g_out][i // g]
             dX[t][i] = acc
     return np.array(dX)
 
 
-def _brute_dgate(dY, X, W, g):
+def _brute_dgate(dY, X, W, g, g_out=1):
     T, d_out = dY.shape
     d_in = X.shape[1]
-    out = [[0.0] * (d_in // g) for _ in range(d_out)]
-    for o in range(d_out):
+    out = [[0.0] * (d_in // g) for _ in range(d_out // g_out)]
+    for u in range(d_out // g_out):
         for v in range(d_in // g):
             acc = 0.0
-            for i in range(v * g, (v + 1) * g):
-                for t in range(T):
-                    acc += dY[t][o] * X[t][i] * W[o][i]
-            out[o][v] = acc
+            for o in range(u * g_out, (u + 1) * g_out):
+                for i in range(v * g, (v + 1) * g):
+                    for t in range(T):
+                        acc += dY[t][o] * X[t][i] * W[o][i]
+            out[u][v] = acc
     return np.array(out)
 
 
-TINY = [(3, 5, 2, 4), (2, 4, 3, 2), (4, 3, 1, 8), (1, 6, 4, 1)]  # (T, d_out, G_in, g)
+# (T, d_out, G_in, g, g_out): 1 x g groups and 2-D g_out x g groups
+TINY = [(3, 5, 2, 4, 1), (2, 4, 3, 2, 1), (4, 3, 1, 8, 1), (1, 6, 4, 1, 1), (3, 6, 2, 4, 3), (2, 8, 3, 2, 2),
+        (2, 4, 2, 4, 4)]
 
 
-@pytest.mark.parametrize("T,d_out,G_in,g", TINY)
-def test_fwd_matches_brute_force(T, d_out, G_in, g):
+@pytest.mark.parametrize("T,d_out,G_in,g,g_out", TINY)
+def test_fwd_matches_brute_force(T, d_out, G_in, g, g_out):
     d_in = G_in * g
     X, W = _rand((T, d_in), (1, T)), _rand((d_out, d_in), (2, T))
-    B = _soft_mask((d_out, G_in), (3, T))
-    np.testing.assert_allclose(oracle.linear_fwd(X, W, B, g), _brute_fwd(X, W, B, g), rtol=1e-12, atol=1e-12)
+    B = _soft_mask((d_out // g_out, G_in), (3, T, g_out))
+    np.testing.assert_allclose(oracle.linear_fwd(X, W, B, g, g_out), _brute_fwd(X, W, B, g, g_out), rtol=1e-12,
+                               atol=1e-12)
 
 
-@pytest.mark.parametrize("T,d_out,G_in,g", TINY)
-def test_dx_matches_brute_force(T, d_out, G_in, g):
+@pytest.mark.parametrize("T,d_out,G_in,g,g_out", TINY)
+def test_dx_matches_brute_force(T, d_out, G_in, g, g_out):
     d_in = G_in * g
     dY, W = _rand((T, d_out), (4, T)), _rand((d_out, d_in), (5, T))
-    B = _soft_mask((d_out, G_in), (6, T))
-    np.testing.assert_allclose(oracle.linear_bwd_dx(dY, W, B, g), _brute_dx(dY, W, B, g), rtol=1e-12, atol=1e-12)
+    B = _soft_mask((d_out // g_out, G_in), (6, T, g_out))
+    np.testing.assert_allclose(oracle.linear_bwd_dx(dY, W, B, g, g_out), _brute_dx(dY, W, B, g, g_out), rtol=1e-12,
+                               atol=1e-12)
 
 
-@pytest.mark.parametrize("T,d_out,G_in,g", TINY)
-def test_dgate_matches_brute_force(T, d_out, G_in, g):
+@pytest.mark.parametrize("T,d_out,G_in,g,g_out", TINY)
+def test_dgate_matches_brute_force(T, d_out, G_in, g, g_out):
     d_in = G_in * g
     dY, X, W = _rand((T, d_out), (7, T)), _rand((T, d_in), (8, T)), _rand((d_out, d_in), (9, T))
-    np.testing.assert_allclose(oracle.linear_bwd_dgate(dY, X, W, g), _brute_dgate(dY, X, W, g), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(oracle.linear_bwd_dgate(dY, X, W, g, g_out), _brute_dgate(dY, X, W, g, g_out),
+                               rtol=1e-12, atol=1e-12)
+
+
+def test_square_group_gradient_sums_the_row_gradients_of_its_block():
+    # A g_out x g group is the union of g_out row groups 1 x g sharing one
+    # selector: its gradient is the sum of theirs (Y is linear in each selector).
+    T, d_out, d_in, g, g_out = 5, 12, 16, 4, 3
+    dY, X, W = _rand((T, d_out), (40,)), _rand((T, d_in), (41,)), _rand((d_out, d_in), (42,))
+    rows = oracle.linear_bwd_dgate(dY, X, W, g)
+    np.testing.assert_allclose(oracle.linear_bwd_dgate(dY, X, W, g, g_out),
+                               rows.reshape(d_out // g_out, g_out, d_in // g).sum(axis=1), rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("h", [0.5, 3.0])
+def test_square_group_dgate_matches_central_finite_differences(h):
+    T, d_out, d_in, g, g_out = 4, 8, 12, 4, 2
+    dY, X, W = _rand((T, d_out), (43,)), _rand((T, d_in), (44,)), _rand((d_out, d_in), (45,))
+    B = _soft_mask((d_out // g_out, d_in // g), (46,))
+    dg = oracle.linear_bwd_dgate(dY, X, W, g, g_out)
+    for u, v in itertools.product(range(d_out // g_out), range(d_in // g)):
+        Bp, Bm = B.copy(), B.copy()
+        Bp[u, v] += h
+        Bm[u, v] -= h
+        fd = (np.sum(dY * oracle.linear_fwd(X, W, Bp, g, g_out)) - np.sum(dY * oracle.linear_fwd(X, W, Bm, g, g_out))) / (2 * h)
+        assert abs(fd - dg[u, v]) <= 1e-10 * (1 + abs(dg[u, v]))
+
+
+def test_single_square_group_scales_the_dense_layer():
+    T, d_out, d_in = 3, 6, 8
+    X, W = _rand((T, d_in), (47,)), _rand((d_out, d_in), (48,))
+    for b in (0.0, 0.3, 1.0):
+        np.testing.assert_allclose(oracle.linear_fwd(X, W, np.array([[b]]), d_in, d_out), b * np.matmul(X, W.T),
+                                   rtol=1e-13, atol=1e-13)
 
 
 # ----------------------------------------------------------- special cases (Eq. 1)
@@ -405,26 +443,44 @@ def test_budget_uniform_variant_is_the_sum_of_single_layer_losses():
 
 # ------------------------------------------------------- the pins catch mistakes
 
-def _mutant_fwd_strided_groups(X, W, B, g):
+def _mutant_fwd_strided_groups(X, W, B, g, g_out=1):
     # selector v applied to columns v, v + G_in, v + 2 G_in, ... instead of a contiguous block
-    M = np.tile(np.asarray(B, dtype=float), (1, g))
+    M = np.tile(np.repeat(np.asarray(B, dtype=float), g_out, axis=0), (1, g))
     return np.asarray(X, float) @ (np.asarray(W, float) * M).T
 
 
-def _mutant_dgate_no_weight(dY, X, W, g):
+def _mutant_fwd_strided_rows(X, W, B, g, g_out=1):
+    # row block u applied to rows u, u + G_out, ... instead of g_out consecutive rows
+    M = np.tile(np.repeat(np.asarray(B, dtype=float), g, axis=1), (g_out, 1))
+    return np.asarray(X, float) @ (np.asarray(W, float) * M).T
+
+
+def _mutant_dgate_no_weight(dY, X, W, g, g_out=1):
     d_out, d_in = np.asarray(W).shape
     G = np.asarray(dY, float).T @ np.asarray(X, float)
-    return G.reshape(d_out, d_in // g, g).sum(axis=2)
+    return G.reshape(d_out // g_out, g_out, d_in // g, g).sum(axis=(1, 3))
 
 
-def _mutant_dgate_strided_groups(dY, X, W, g):
+def _mutant_dgate_strided_groups(dY, X, W, g, g_out=1):
     d_out, d_in = np.asarray(W).shape
     G = np.asarray(dY, float).T @ np.asarray(X, float)
-    return (np.asarray(W, float) * G).reshape(d_out, g, d_in // g).sum(axis=1)
+    return (np.asarray(W, float) * G).reshape(d_out // g_out, g_out, g, d_in // g).sum(axis=(1, 2))
 
 
-def _mutant_dx_unmasked(dY, W, B, g):
+def _mutant_dgate_first_row_only(dY, X, W, g, g_out=1):
+    # a 2-D group's gradient taken from the first of its rows alone
+    d_out, d_in = np.asarray(W).shape
+    G = np.asarray(dY, float).T @ np.asarray(X, float)
+    return (np.asarray(W, float) * G).reshape(d_out // g_out, g_out, d_in // g, g)[:, 0].sum(axis=2)
+
+
+def _mutant_dx_unmasked(dY, W, B, g, g_out=1):
     return np.asarray(dY, float) @ np.asarray(W, float)
+
+
+def _mutant_dx_strided_rows(dY, W, B, g, g_out=1):
+    M = np.tile(np.repeat(np.asarray(B, dtype=float), g, axis=1), (g_out, 1))
+    return np.asarray(dY, float) @ (np.asarray(W, float) * M)
 
 
 def _mutant_gate_sign(logits, noise, tau, hard):
@@ -475,6 +531,9 @@ def _mutant_budget_grad_no_inv_s(selectors, params, s_target, lam, uniform=False
 
 MUTANTS = [
     ("linear_fwd", _mutant_fwd_strided_groups),
+    ("linear_fwd", _mutant_fwd_strided_rows),
+    ("linear_bwd_dgate", _mutant_dgate_first_row_only),
+    ("linear_bwd_dx", _mutant_dx_strided_rows),
     ("linear_bwd_dgate", _mutant_dgate_no_weight),
     ("linear_bwd_dgate", _mutant_dgate_strided_groups),
     ("linear_bwd_dx", _mutant_dx_unmasked),
@@ -491,6 +550,9 @@ PIN_TESTS = [
     lambda: [test_fwd_matches_brute_force(*c) for c in TINY],
     lambda: [test_dx_matches_brute_force(*c) for c in TINY],
     lambda: [test_dgate_matches_brute_force(*c) for c in TINY],
+    test_square_group_gradient_sums_the_row_gradients_of_its_block,
+    lambda: test_square_group_dgate_matches_central_finite_differences(0.5),
+    test_single_square_group_scales_the_dense_layer,
     test_dx_is_the_adjoint_of_the_forward,
     lambda: test_dgate_matches_central_finite_differences(0.5),
     test_dgate_euler_and_row_sum_identities,
