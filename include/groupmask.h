@@ -2,18 +2,19 @@
  * groupmask.h -- C ABI of the group-masked linear layer of GroupMask
  * (layer-adaptive group-wise sparsity with frozen weights, Sec. 2).
  *
- * One target linear layer holds a frozen weight W [d_out, d_in].  Its input
- * dimension is cut into G_in = d_in / g groups of g consecutive columns, so
- * every output row o owns the groups (o, v), v = 0 .. G_in-1, each covering
- * W[o, v*g : (v+1)*g] (Sec. 2.1 with a 1 x g group shape; Eq. 1 expands the
- * selector matrix B [d_out, G_in] to the full-resolution mask by a Kronecker
- * product with a 1 x g block of ones).
+ * One target linear layer holds a frozen weight W [d_out, d_in], cut into
+ * g_out x g groups (Sec. 2.1): group (u, v) covers W[u*g_out : (u+1)*g_out,
+ * v*g : (v+1)*g], u < G_out = d_out / g_out, v < G_in = d_in / g.  Eq. 1
+ * expands the selector matrix B [G_out, G_in] to the full-resolution mask by a
+ * Kronecker product with a g_out x g block of ones.  Shapes built: row groups
+ * 1 x g with g in {64, 128, 256, 512} (g_out = 1) and square groups
+ * g x g with g in {16, 32, 64, 128} (g_out = g).
  *
  * Conventions shared by every call:
  *   - bf16 tensors are passed as uint16_t bit patterns; fp32 as float.
  *   - All tensors are dense, row-major, contiguous, in the nn.Linear
  *     convention: X [T, d_in], W [d_out, d_in], Y / dY [T, d_out],
- *     mask / dgate [d_out, G_in].
+ *     mask / dgate [G_out, G_in].
  *   - Every pointer argument is a DEVICE pointer unless stated otherwise, and
  *     must be 16-byte aligned unless stated otherwise (the per-layer arrays of
  *     the budget calls need only their element alignment).  The caller owns
@@ -39,7 +40,7 @@
 extern "C" {
 #endif
 
-#define GM_ABI_VERSION 1
+#define GM_ABI_VERSION 2
 
 /* Same object as a hipStream_t, declared here so that callers need no HIP headers. */
 typedef struct ihipStream_t* gm_stream_t;
@@ -149,33 +150,36 @@ gm_status gm_gate_bwd_budget(const float* dgate, const float* soft, int64_t n, f
  * (op = GM_OP_BWD) needs for the given shape.  No device work.
  *   bytes: HOST pointer, required.
  */
-gm_status gm_workspace_size(int op, int64_t T, int64_t d_in, int64_t d_out, int32_t g, size_t* bytes);
+gm_status gm_workspace_size(int op, int64_t T, int64_t d_in, int64_t d_out, int32_t g, int32_t g_out,
+                            size_t* bytes);
 
 /*
  * gm_masked_linear_fwd -- student forward of one target linear (Eq. 1):
- *   Y = X (W (.) (mask (x) 1_{1 x g}))^T,
- *   Y[t, o] = sum_v mask[o, v] * sum_{i in group v} X[t, i] W[o, i].
+ *   Y = X (W (.) (mask (x) 1_{g_out x g}))^T,
+ *   Y[t, o] = sum_v mask[o / g_out, v] * sum_{i in group v} X[t, i] W[o, i].
  * A group with mask == 0 is skipped (its weights are never read); any other
  * value scales the group (1.0 for a hard selector).  bf16 inputs, fp32
  * accumulation, Y rounded to bf16 (round to nearest even).
- *   X    [T, d_in]  bf16       W [d_out, d_in] bf16     mask [d_out, d_in/g] fp32
+ *   X    [T, d_in]  bf16       W [d_out, d_in] bf16
+ *   mask [d_out / g_out, d_in / g] fp32
  *   Y    [T, d_out] bf16, written in full
- *   T >= 1; d_in, d_out >= 1 and multiples of 8; g in {64, 128, 256, 512}
- *   dividing d_in, d_in / g <= 512; each of X, W, Y (T rounded up to a
- *   multiple of 8) below 2^30 - 2^22 elements.  Mask values must be finite
- *   and >= 0 (not checked).
+ *   T >= 1; d_in, d_out >= 1 and multiples of 8; (g_out, g) one of the
+ *   built shapes; d_in a multiple of max(g, 64) and at most 512 * max(g, 32);
+ *   d_out a multiple of g_out; each of X, W, Y (T rounded up to a multiple
+ *   of 8) below 2^30 - 2^22 elements.  Mask values must be finite and >= 0
+ *   (not checked).
  *   ws / ws_bytes: workspace of at least gm_workspace_size(GM_OP_FWD, ...)
  *   bytes (ws may be NULL when that size is 0).
  */
 gm_status gm_masked_linear_fwd(const uint16_t* X, const uint16_t* W, const float* mask, int64_t T,
-                               int64_t d_in, int64_t d_out, int32_t g, uint16_t* Y, void* ws,
-                               size_t ws_bytes, gm_stream_t stream);
+                               int64_t d_in, int64_t d_out, int32_t g, int32_t g_out, uint16_t* Y,
+                               void* ws, size_t ws_bytes, gm_stream_t stream);
 
 /*
  * gm_masked_linear_bwd -- backward of one target linear with frozen W
  * (Sec. 2.2 STE, Sec. 2.4 frozen weights):
  *   dX = dY (W (.) expand(mask))                       [T, d_in]   bf16
- *   dgate[o, v] = sum_{i in group v} W[o, i] (dY^T X)[o, i]   [d_out, G_in] fp32
+ *   dgate[u, v] = sum_{(o, i) in group (u, v)} W[o, i] (dY^T X)[o, i]   [G_out, G_in] fp32
  * dgate is produced for every group, kept or pruned, and does not depend on
  * the mask; the weight gradient is never formed.  Either output may be NULL to
  * skip it (both NULL is a no-op); mask may be NULL only when dX is NULL.
@@ -184,23 +188,25 @@ gm_status gm_masked_linear_fwd(const uint16_t* X, const uint16_t* W, const float
  */
 gm_status gm_masked_linear_bwd(const uint16_t* dY, const uint16_t* X, const uint16_t* W,
                                const float* mask, int64_t T, int64_t d_in, int64_t d_out, int32_t g,
-                               uint16_t* dX, float* dgate, void* ws, size_t ws_bytes,
+                               int32_t g_out, uint16_t* dX, float* dgate, void* ws, size_t ws_bytes,
                                gm_stream_t stream);
 
 /*
  * gm_pack_rows -- export of a learned mask (Appendix F): copies the retained
- * groups of W, row by row, into a packed buffer for the pruned model.
+ * groups of W, row by row, into a packed buffer for the pruned model.  A
+ * g_out x g group is stored as its g_out row pieces of g weights, so the
+ * export of every group shape is the same row-wise format.
  *   rowptr [d_out + 1] int32: rowptr[o] = number of kept groups in rows < o;
  *                             rowptr[d_out] = total kept groups k.
  *   Wp     [capacity, g] bf16: kept group number j of the matrix at Wp[j*g];
  *   chunk  [capacity] int32:  its group column v;
  *   scale  [capacity] fp32:   its mask value (1.0 for a hard selector).
- * Groups with mask == 0 are dropped.  Groups beyond `capacity` are not written:
- * the caller checks rowptr[d_out] <= capacity (capacity = d_out * d_in / g is
- * always enough).  Shape constraints as gm_masked_linear_fwd.
+ * Groups with mask == 0 are dropped.  Row pieces beyond `capacity` are not
+ * written: the caller checks rowptr[d_out] <= capacity (capacity = d_out *
+ * d_in / g is always enough).  Shape constraints as gm_masked_linear_fwd.
  */
 gm_status gm_pack_rows(const uint16_t* W, const float* mask, int64_t d_in, int64_t d_out, int32_t g,
-                       int64_t capacity, uint16_t* Wp, int32_t* chunk, float* scale,
+                       int32_t g_out, int64_t capacity, uint16_t* Wp, int32_t* chunk, float* scale,
                        int32_t* rowptr, gm_stream_t stream);
 
 /*
@@ -210,6 +216,8 @@ gm_status gm_pack_rows(const uint16_t* W, const float* mask, int64_t d_in, int64
  * every kept weight once per 16 tokens); any T >= 1 is accepted.
  *   X [T, d_in] bf16; Wp, chunk, scale, rowptr as written by gm_pack_rows,
  *   which must have held every kept group (rowptr[d_out] <= its capacity);
+ *   g is the width of the exported pieces (the group width; a square export
+ *   with g < 64 also needs d_out a multiple of g);
  *   Y [T, d_out] bf16, written in full.
  */
 gm_status gm_packed_linear_fwd(const uint16_t* X, const uint16_t* Wp, const int32_t* chunk,

@@ -46,10 +46,10 @@ def _load() -> ctypes.CDLL:
         "gm_gate_bwd": ([P, P, I64, F32, P, P], ctypes.c_int),
         "gm_budget_loss": ([P, I64, P, P, I32, F32, F32, ctypes.c_int, P, P, P, P], ctypes.c_int),
         "gm_gate_bwd_budget": ([P, P, I64, F32, P, I32, P, P, P], ctypes.c_int),
-        "gm_workspace_size": ([ctypes.c_int, I64, I64, I64, I32, ctypes.POINTER(SZ)], ctypes.c_int),
-        "gm_masked_linear_fwd": ([P, P, P, I64, I64, I64, I32, P, P, SZ, P], ctypes.c_int),
-        "gm_masked_linear_bwd": ([P, P, P, P, I64, I64, I64, I32, P, P, P, SZ, P], ctypes.c_int),
-        "gm_pack_rows": ([P, P, I64, I64, I32, I64, P, P, P, P, P], ctypes.c_int),
+        "gm_workspace_size": ([ctypes.c_int, I64, I64, I64, I32, I32, ctypes.POINTER(SZ)], ctypes.c_int),
+        "gm_masked_linear_fwd": ([P, P, P, I64, I64, I64, I32, I32, P, P, SZ, P], ctypes.c_int),
+        "gm_masked_linear_bwd": ([P, P, P, P, I64, I64, I64, I32, I32, P, P, P, SZ, P], ctypes.c_int),
+        "gm_pack_rows": ([P, P, I64, I64, I32, I32, I64, P, P, P, P, P], ctypes.c_int),
         "gm_packed_linear_fwd": ([P, P, P, P, P, I64, I64, I64, I32, P, P], ctypes.c_int),
     }
     for name, (args, res) in sigs.items():
@@ -114,33 +114,33 @@ def gm_gate_bwd_budget(dgate, soft, tau: float, offsets, coeff, dlogits, stream=
                                   _ptr(coeff), _ptr(dlogits), _stream(stream)), "gm_gate_bwd_budget")
 
 
-def gm_workspace_size(op: int, T: int, d_in: int, d_out: int, g: int) -> int:
+def gm_workspace_size(op: int, T: int, d_in: int, d_out: int, g: int, g_out: int = 1) -> int:
     out = ctypes.c_size_t(0)
-    _check(LIB.gm_workspace_size(int(op), int(T), int(d_in), int(d_out), int(g), ctypes.byref(out)),
+    _check(LIB.gm_workspace_size(int(op), int(T), int(d_in), int(d_out), int(g), int(g_out), ctypes.byref(out)),
            "gm_workspace_size")
     return out.value
 
 
-def gm_masked_linear_fwd(X, W, mask, g: int, Y, ws=None, stream=None) -> None:
+def gm_masked_linear_fwd(X, W, mask, g: int, Y, ws=None, stream=None, g_out: int = 1) -> None:
     T, d_in = X.shape
     d_out = W.shape[0]
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
-    _check(LIB.gm_masked_linear_fwd(_ptr(X), _ptr(W), _ptr(mask), T, d_in, d_out, int(g), _ptr(Y), _ptr(ws), nbytes,
-                                    _stream(stream)), "gm_masked_linear_fwd")
+    _check(LIB.gm_masked_linear_fwd(_ptr(X), _ptr(W), _ptr(mask), T, d_in, d_out, int(g), int(g_out), _ptr(Y),
+                                    _ptr(ws), nbytes, _stream(stream)), "gm_masked_linear_fwd")
 
 
-def gm_masked_linear_bwd(dY, X, W, mask, g: int, dX=None, dgate=None, ws=None, stream=None) -> None:
+def gm_masked_linear_bwd(dY, X, W, mask, g: int, dX=None, dgate=None, ws=None, stream=None, g_out: int = 1) -> None:
     T, d_in = X.shape
     d_out = W.shape[0]
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
-    _check(LIB.gm_masked_linear_bwd(_ptr(dY), _ptr(X), _ptr(W), _ptr(mask), T, d_in, d_out, int(g), _ptr(dX),
-                                    _ptr(dgate), _ptr(ws), nbytes, _stream(stream)), "gm_masked_linear_bwd")
+    _check(LIB.gm_masked_linear_bwd(_ptr(dY), _ptr(X), _ptr(W), _ptr(mask), T, d_in, d_out, int(g), int(g_out),
+                                    _ptr(dX), _ptr(dgate), _ptr(ws), nbytes, _stream(stream)), "gm_masked_linear_bwd")
 
 
-def gm_pack_rows(W, mask, g: int, capacity: int, Wp, chunk, scale, rowptr, stream=None) -> None:
+def gm_pack_rows(W, mask, g: int, capacity: int, Wp, chunk, scale, rowptr, stream=None, g_out: int = 1) -> None:
     d_out, d_in = W.shape
-    _check(LIB.gm_pack_rows(_ptr(W), _ptr(mask), d_in, d_out, int(g), int(capacity), _ptr(Wp), _ptr(chunk),
-                            _ptr(scale), _ptr(rowptr), _stream(stream)), "gm_pack_rows")
+    _check(LIB.gm_pack_rows(_ptr(W), _ptr(mask), d_in, d_out, int(g), int(g_out), int(capacity), _ptr(Wp),
+                            _ptr(chunk), _ptr(scale), _ptr(rowptr), _stream(stream)), "gm_pack_rows")
 
 
 def gm_packed_linear_fwd(X, Wp, chunk, scale, rowptr, d_out: int, g: int, Y, stream=None) -> None:

@@ -17,7 +17,7 @@
 namespace {
 
 constexpr int64_t kMaxDim = int64_t(1) << 30;  // kernels index rows and columns with 32-bit ints
-constexpr int kMaxGroupCols = 512;             // per-tile group-column list of the forward GEMM
+constexpr int kMaxUnits = 512;                 // forward GEMM: column units (max(g, 32) wide) per row
 constexpr int kDecodeTokens = 16;              // forward dispatch: T <= 16 takes the GEMV path
 constexpr int64_t kMaxElems = (int64_t(1) << 30) - (int64_t(1) << 22);  // bf16 elements per matrix (< 2 GiB)
 
@@ -55,43 +55,58 @@ gm_status from_hip(hipError_t e) { return e == hipSuccess ? GM_OK : device_error
 
 gm_status check_tau(float tau) { return (std::isfinite(tau) && tau > 0.0f) ? GM_OK : GM_ERR_VALUE; }
 
-gm_status check_linear_shape(int64_t T, int64_t d_in, int64_t d_out, int32_t g) {
+// Group shapes built: 1 x {64, 128, 256, 512} and square {16, 32, 64, 128}.
+bool group_shape_ok(int32_t g, int32_t g_out) {
+  if (g_out == 1) return g == 64 || g == 128 || g == 256 || g == 512;
+  return g_out == g && (g == 16 || g == 32 || g == 64 || g == 128);
+}
+
+// Width of a column unit of the forward GEMM and of a list column of dX.
+int64_t unit_width(int32_t g) { return g < 32 ? 32 : g; }
+int64_t list_width(int32_t g) { return g < 64 ? 64 : g; }
+
+gm_status check_linear_shape(int64_t T, int64_t d_in, int64_t d_out, int32_t g, int32_t g_out) {
   if (T < 1 || d_in < 1 || d_out < 1) return GM_ERR_SHAPE;
   if (T > kMaxDim || d_in > kMaxDim || d_out > kMaxDim) return GM_ERR_SHAPE;
   if (d_in % 8 || d_out % 8) return GM_ERR_SHAPE;
-  if (g != 64 && g != 128 && g != 256 && g != 512) return GM_ERR_SHAPE;
-  if (d_in % g) return GM_ERR_SHAPE;
-  if (d_in / g > kMaxGroupCols) return GM_ERR_SHAPE;
+  if (!group_shape_ok(g, g_out)) return GM_ERR_SHAPE;
+  if (d_in % list_width(g) || d_out % g_out) return GM_ERR_SHAPE;
+  if (d_in / unit_width(g) > kMaxUnits) return GM_ERR_SHAPE;
   // The GEMMs address every matrix with 32-bit byte offsets below 2 GiB.
   const int64_t t8 = (T + 7) / 8 * 8;
   if (t8 * d_in > kMaxElems || t8 * d_out > kMaxElems || d_out * d_in > kMaxElems) return GM_ERR_SHAPE;
   return GM_OK;
 }
 
-// Workspace of the backward, each part 256-byte aligned:
-//   colcount [G_in] int32 | colsoft [G_in] int32 | rows [G_in * d_out + 128] int32 |
-//   scales [G_in * d_out + 128] fp32 | dYt [d_out * ldt] bf16
+// Workspace of the backward, each part 256-byte aligned, over NL = d_in / lc
+// list columns of lc = max(g, 64) input columns (nsub = lc / g groups each):
+//   colcount [NL] int32 | colsoft [NL] int32 | rows [NL * d_out + 128] int32 |
+//   scales [(NL * d_out + 128) * nsub] fp32 | subbits [NL * d_out + 128] int32 (nsub > 1) |
+//   dYt [d_out * ldt] bf16
 // The 128 spare entries after the column lists keep the dX kernel's look-ahead
 // reads of the list (up to 63 entries past a column's end) inside the buffer.
 struct BwdLayout {
-  size_t colcount, colsoft, rows, scales, dyt, total;
-  int ldt;
+  size_t colcount, colsoft, rows, scales, subbits, dyt, total;
+  int ldt, nsub;
 };
 
 BwdLayout bwd_layout(int64_t T, int64_t d_in, int64_t d_out, int32_t g) {
   BwdLayout L;
-  const size_t G_in = size_t(d_in / g);
-  const size_t list = G_in * size_t(d_out) + 128;
+  L.nsub = int(list_width(g) / g);
+  const size_t NL = size_t(d_in / list_width(g));
+  const size_t list = NL * size_t(d_out) + 128;
   L.ldt = int(round_up(size_t(T), 8));
   size_t off = 0;
   L.colcount = off;
-  off = round_up(off + G_in * sizeof(int32_t), 256);
+  off = round_up(off + NL * sizeof(int32_t), 256);
   L.colsoft = off;
-  off = round_up(off + G_in * sizeof(int32_t), 256);
+  off = round_up(off + NL * sizeof(int32_t), 256);
   L.rows = off;
   off = round_up(off + list * sizeof(int32_t), 256);
   L.scales = off;
-  off = round_up(off + list * sizeof(float), 256);
+  off = round_up(off + list * size_t(L.nsub) * sizeof(float), 256);
+  L.subbits = off;
+  if (L.nsub > 1) off = round_up(off + list * sizeof(int32_t), 256);
   L.dyt = off;
   off = round_up(off + size_t(d_out) * size_t(L.ldt) * sizeof(uint16_t), 256);
   L.total = off;
@@ -168,36 +183,37 @@ GM_EXPORT gm_status gm_gate_bwd_budget(const float* dgate, const float* soft, in
   return from_hip(gm::launch_gate_bwd_budget(dgate, soft, n, tau, offsets, L, coeff, dlogits, stream));
 }
 
-GM_EXPORT gm_status gm_workspace_size(int op, int64_t T, int64_t d_in, int64_t d_out, int32_t g, size_t* bytes) {
+GM_EXPORT gm_status gm_workspace_size(int op, int64_t T, int64_t d_in, int64_t d_out, int32_t g, int32_t g_out,
+                                      size_t* bytes) {
   if (!bytes) return GM_ERR_NULL;
   if (op != GM_OP_FWD && op != GM_OP_BWD) return GM_ERR_VALUE;
-  if (gm_status st = check_linear_shape(T, d_in, d_out, g)) return st;
+  if (gm_status st = check_linear_shape(T, d_in, d_out, g, g_out)) return st;
   *bytes = op == GM_OP_FWD ? 0 : bwd_layout(T, d_in, d_out, g).total;
   return GM_OK;
 }
 
 GM_EXPORT gm_status gm_masked_linear_fwd(const uint16_t* X, const uint16_t* W, const float* mask, int64_t T,
-                                         int64_t d_in, int64_t d_out, int32_t g, uint16_t* Y, void* ws,
-                                         size_t ws_bytes, gm_stream_t stream) {
+                                         int64_t d_in, int64_t d_out, int32_t g, int32_t g_out, uint16_t* Y,
+                                         void* ws, size_t ws_bytes, gm_stream_t stream) {
   (void)ws;
   (void)ws_bytes;
   if (!X || !W || !mask || !Y) return GM_ERR_NULL;
-  if (gm_status st = check_linear_shape(T, d_in, d_out, g)) return st;
+  if (gm_status st = check_linear_shape(T, d_in, d_out, g, g_out)) return st;
   if (!aligned16(X) || !aligned16(W) || !aligned16(mask) || !aligned16(Y)) return GM_ERR_ALIGN;
   if (gm_status st = check_device()) return st;
   const int t = int(T), di = int(d_in), dout = int(d_out);
   if (T <= kDecodeTokens && d_in / g <= gm::gemv_max_groups_per_row())
-    return from_hip(gm::launch_gemv_inplace(X, W, mask, t, di, dout, g, Y, stream));
-  return from_hip(gm::launch_fwd(X, W, mask, t, di, dout, g, Y, stream));
+    return from_hip(gm::launch_gemv_inplace(X, W, mask, t, di, dout, g, g_out, Y, stream));
+  return from_hip(gm::launch_fwd(X, W, mask, t, di, dout, g, g_out, Y, stream));
 }
 
 GM_EXPORT gm_status gm_masked_linear_bwd(const uint16_t* dY, const uint16_t* X, const uint16_t* W,
                                          const float* mask, int64_t T, int64_t d_in, int64_t d_out, int32_t g,
-                                         uint16_t* dX, float* dgate, void* ws, size_t ws_bytes,
+                                         int32_t g_out, uint16_t* dX, float* dgate, void* ws, size_t ws_bytes,
                                          gm_stream_t stream) {
   if (!dY || !X || !W) return GM_ERR_NULL;
   if (dX && !mask) return GM_ERR_NULL;
-  if (gm_status st = check_linear_shape(T, d_in, d_out, g)) return st;
+  if (gm_status st = check_linear_shape(T, d_in, d_out, g, g_out)) return st;
   if (!aligned16(dY) || !aligned16(X) || !aligned16(W) || (mask && !aligned16(mask)) || (dX && !aligned16(dX)) ||
       (dgate && !aligned16(dgate)))
     return GM_ERR_ALIGN;
@@ -218,42 +234,47 @@ GM_EXPORT gm_status gm_masked_linear_bwd(const uint16_t* dY, const uint16_t* X, 
     int* colsoft = reinterpret_cast<int*>(base + L.colsoft);
     int* rows = reinterpret_cast<int*>(base + L.rows);
     float* scales = reinterpret_cast<float*>(base + L.scales);
-    if (gm_status st = from_hip(gm::launch_col_lists(mask, dout, G_in, colcount, colsoft, rows, scales, stream)))
+    int* subbits = L.nsub > 1 ? reinterpret_cast<int*>(base + L.subbits) : nullptr;
+    if (gm_status st = from_hip(gm::launch_col_lists(mask, dout, G_in, g_out, L.nsub, colcount, colsoft, rows, scales,
+                                                     subbits, stream)))
       return st;
     // dY^T: a side output of the dgate GEMM, or a transpose pass without it.
     if (dgate) {
-      if (gm_status st = from_hip(gm::launch_dgate(dY, X, W, t, di, dout, g, dgate, dyt, L.ldt, stream))) return st;
+      if (gm_status st = from_hip(gm::launch_dgate(dY, X, W, t, di, dout, g, g_out, dgate, dyt, L.ldt, stream)))
+        return st;
     } else {
       if (gm_status st = from_hip(gm::launch_transpose(dY, t, dout, dyt, L.ldt, stream))) return st;
     }
-    if (gm_status st = from_hip(gm::launch_dx(dyt, L.ldt, W, colcount, rows, scales, colsoft, t, di, dout, g, dX,
-                                              stream)))
+    if (gm_status st = from_hip(gm::launch_dx(dyt, L.ldt, W, colcount, rows, scales, subbits, colsoft, t, di, dout,
+                                              g, dX, stream)))
       return st;
   } else {
-    if (gm_status st = from_hip(gm::launch_dgate(dY, X, W, t, di, dout, g, dgate, nullptr, 0, stream))) return st;
+    if (gm_status st = from_hip(gm::launch_dgate(dY, X, W, t, di, dout, g, g_out, dgate, nullptr, 0, stream)))
+      return st;
   }
   return GM_OK;
 }
 
 GM_EXPORT gm_status gm_pack_rows(const uint16_t* W, const float* mask, int64_t d_in, int64_t d_out, int32_t g,
-                                 int64_t capacity, uint16_t* Wp, int32_t* chunk, float* scale, int32_t* rowptr,
-                                 gm_stream_t stream) {
+                                 int32_t g_out, int64_t capacity, uint16_t* Wp, int32_t* chunk, float* scale,
+                                 int32_t* rowptr, gm_stream_t stream) {
   if (!W || !mask || !Wp || !chunk || !scale || !rowptr) return GM_ERR_NULL;
-  if (gm_status st = check_linear_shape(1, d_in, d_out, g)) return st;
+  if (gm_status st = check_linear_shape(1, d_in, d_out, g, g_out)) return st;
   if (capacity < 0 || capacity > d_out * (d_in / g)) return GM_ERR_SHAPE;
   if (!aligned16(W) || !aligned16(mask) || !aligned16(Wp) || !aligned16(chunk) || !aligned16(scale) ||
       !aligned16(rowptr))
     return GM_ERR_ALIGN;
   if (gm_status st = check_device()) return st;
-  return from_hip(gm::launch_pack_rows(W, mask, int(d_in), int(d_out), g, capacity, Wp, chunk, scale, rowptr,
-                                       stream));
+  return from_hip(gm::launch_pack_rows(W, mask, int(d_in), int(d_out), g, g_out, capacity, Wp, chunk, scale,
+                                       rowptr, stream));
 }
 
 GM_EXPORT gm_status gm_packed_linear_fwd(const uint16_t* X, const uint16_t* Wp, const int32_t* chunk,
                                          const float* scale, const int32_t* rowptr, int64_t T, int64_t d_in,
                                          int64_t d_out, int32_t g, uint16_t* Y, gm_stream_t stream) {
   if (!X || !Wp || !chunk || !scale || !rowptr || !Y) return GM_ERR_NULL;
-  if (gm_status st = check_linear_shape(T, d_in, d_out, g)) return st;
+  // the export holds row pieces of g weights whatever the group's height
+  if (gm_status st = check_linear_shape(T, d_in, d_out, g, g < 64 ? g : 1)) return st;
   if (!aligned16(X) || !aligned16(Wp) || !aligned16(chunk) || !aligned16(scale) || !aligned16(rowptr) ||
       !aligned16(Y))
     return GM_ERR_ALIGN;

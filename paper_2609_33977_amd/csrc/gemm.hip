@@ -1,8 +1,11 @@
 // bf16 MFMA GEMMs of the group-masked linear layer on gfx950.
 //
-//   fwd   Y[t, o]     = sum_v mask[o, v] sum_{i in v} X[t, i] W[o, i]          (Eq. 1)
-//   dX    dX[t, i]    = sum_{o kept in column v(i)} mask[o, v] dY[t, o] W[o, i]
-//   dgate dgate[o, v] = sum_{i in v} W[o, i] sum_t dY[t, o] X[t, i]
+//   fwd   Y[t, o]     = sum_v mask[u(o), v] sum_{i in v} X[t, i] W[o, i]        (Eq. 1)
+//   dX    dX[t, i]    = sum_{o kept in column v(i)} mask[u(o), v] dY[t, o] W[o, i]
+//   dgate dgate[u, v] = sum_{o in u, i in v} W[o, i] sum_t dY[t, o] X[t, i]
+//
+// Groups are g_out x g blocks (Sec. 2.1): u(o) = o / g_out is the mask row of
+// output row o, v(i) = i / g its mask column; 1 x g groups have g_out = 1.
 //
 // Shared machinery (gm_pipe.h): 256 x 256 output tiles (dX: min(g, 256) x 256),
 // four waves of 128 x 128 (dX: g/2 x 128) accumulated in AGPRs with
@@ -218,65 +221,95 @@ __device__ __forceinline__ void store4_bf16(uint16_t* p, const f32x4& v) {
 // ============================================================================ fwd
 
 // C[o, t] over K = d_in, tile 256 (o) x 256 (t); waves 2 (o) x 2 (t).
-template <int G>
+//
+// The K-loop walks column units of U = max(g, 32) input columns (a 16-wide
+// group shares its 32-deep slice with its neighbour) and visits only the
+// units that some row of the tile keeps; inside a visited unit each 16-byte
+// chunk of W whose group is pruned for its row is zero-filled instead of read.
+template <int G, int GO>
 __global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
                                                   const float* __restrict__ mask, int T, int d_in, int d_out,
                                                   uint16_t* __restrict__ Y) {
   constexpr int NW = kFwdWaves, WN = NW / 2;  // waves per block; wave grid 2 (M) x WN (N)
   constexpr int BM = 256, BN = 256, MB = 8, NB = BN / WN / 16;
-  constexpr int SUB = G / kBK;                // K slices per group column
-  constexpr int MAXG = 512;                   // group-column limit (checked by the host)
+  constexpr int U = G < kBK ? kBK : G;        // input columns of one unit
+  constexpr int UG = U / G;                   // groups per unit (2 for g = 16)
+  constexpr int SUB = U / kBK;                // K slices per unit
+  constexpr int RB = BM / GO;                 // mask rows met by one tile
+  constexpr int MAXG = GO == 1 ? 512 : 1024;  // selectors per mask row (checked by the host)
+  constexpr int MAXU = 512;                   // units per row (checked by the host)
   constexpr int PER_STAGE = 32 / NW;          // DMA instructions per wave per slice
   constexpr int CA = PER_STAGE / 2;           // of which copies of the W tile (the rest: X tile)
   constexpr int STAGES = 4;
+  static_assert(GO == 1 || GO == G, "groups are 1 x g or square");
   __shared__ u32x4 As[STAGES][BM * 4];
   __shared__ u32x4 Bs[STAGES][BN * 4];
-  __shared__ uint32_t s_bits[BM][MAXG / 32];  // kept bits of the tile's rows
-  __shared__ uint32_t s_any[MAXG / 32];       // column kept by some row of the tile
-  __shared__ int s_cols[MAXG];
+  __shared__ uint32_t s_bits[RB][MAXG / 32];  // kept bits of the tile's mask rows
+  __shared__ uint32_t s_any[MAXU / 32];       // unit kept by some row of the tile
+  __shared__ int s_cols[MAXU];
   __shared__ int s_ncols, s_soft;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
-  const int G_in = d_in / G;
-  const int words = (G_in + 31) / 32;
+  const int G_in = d_in / G, NU = d_in / U;
   const int tiles_m = (d_out + BM - 1) / BM, tiles_n = (T + BN - 1) / BN;
   int tm, tn;
   tile_coords(gridDim.x, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
 
-  // Prologue: kept bits of every row of the tile, the columns some row keeps, soft values.
-  if (tid < MAXG / 32) s_any[tid] = 0;
+  // Prologue: kept bits of every mask row of the tile, the units some row keeps, soft values.
+  if (tid < MAXU / 32) s_any[tid] = 0;
+  if constexpr (GO > 1)
+    for (int w = tid; w < RB * (MAXG / 32); w += 64 * NW) (&s_bits[0][0])[w] = 0u;
   if (tid == 0) {
     s_soft = 0;
-    s_cols[0] = 0;  // read (unused) by the zero-fill copies when no column is kept
+    s_cols[0] = 0;  // read (unused) by the zero-fill copies when no unit is kept
   }
   __syncthreads();
-  if (tid < BM) {
-    const int o = m0 + tid;
+  if constexpr (GO == 1) {
+    // one thread per row; a unit is one group
+    if (tid < BM) {
+      const int o = m0 + tid;
+      const int words = (G_in + 31) / 32;
+      bool soft = false;
+      for (int w = 0; w < words; ++w) {
+        uint32_t b = 0;
+        if (o < d_out)
+          for (int q = 0; q < 32 && w * 32 + q < G_in; ++q) {
+            const float m = mask[int64_t(o) * G_in + w * 32 + q];
+            b |= uint32_t(m != 0.0f) << q;
+            soft |= (m != 0.0f) && (m != 1.0f);
+          }
+        s_bits[tid][w] = b;
+        if (b) atomicOr(&s_any[w], b);
+      }
+      if (soft) s_soft = 1;
+    }
+  } else {
+    // the tile's RB mask rows are contiguous in the mask: read them coalesced
+    const int u0 = m0 / GO, G_out = d_out / GO;
     bool soft = false;
-    for (int w = 0; w < words; ++w) {
-      uint32_t b = 0;
-      if (o < d_out)
-        for (int q = 0; q < 32 && w * 32 + q < G_in; ++q) {
-          const float m = mask[int64_t(o) * G_in + w * 32 + q];
-          b |= uint32_t(m != 0.0f) << q;
-          soft |= (m != 0.0f) && (m != 1.0f);
-        }
-      s_bits[tid][w] = b;
-      if (b) atomicOr(&s_any[w], b);
+    for (int e = tid; e < RB * G_in; e += 64 * NW) {
+      const int rb = e / G_in, v = e - rb * G_in;
+      const float m = u0 + rb < G_out ? mask[int64_t(u0) * G_in + e] : 0.0f;
+      if (m != 0.0f) {
+        atomicOr(&s_bits[rb][v >> 5], 1u << (v & 31));
+        const int un = v / UG;
+        atomicOr(&s_any[un >> 5], 1u << (un & 31));
+        soft |= m != 1.0f;
+      }
     }
     if (soft) s_soft = 1;
   }
   __syncthreads();
   if (wave == 0) {
     int cnt = 0;
-    for (int vb = 0; vb < G_in; vb += 64) {
-      const int v = vb + lane;
-      const bool f = v < G_in && ((s_any[v >> 5] >> (v & 31)) & 1);
+    for (int ub = 0; ub < NU; ub += 64) {
+      const int un = ub + lane;
+      const bool f = un < NU && ((s_any[un >> 5] >> (un & 31)) & 1);
       const uint64_t bal = __ballot(f);
-      if (f) s_cols[cnt + __popcll(bal & ((uint64_t(1) << lane) - 1))] = v;
+      if (f) s_cols[cnt + __popcll(bal & ((uint64_t(1) << lane) - 1))] = un;
       cnt += __popcll(bal);
     }
     if (lane == 0) s_ncols = cnt;
@@ -285,13 +318,16 @@ __global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __r
   const int nst = s_ncols * SUB;
 
   // This lane's CA DMA rows (the same in both tiles): row = 16 (CA wave + j) + lane / 4,
+  // their mask rows within the tile, the group of their chunk within a unit,
   // and their byte offsets within a K slice (out-of-range rows read zeros).
-  int rowj[CA];
+  int rowj[CA], brow[CA], gsub[CA];
   uint32_t offA[CA], offB[CA];
 #pragma unroll
   for (int j = 0; j < CA; ++j) {
     int c;
     km_dma_target((wave * CA + j) * 64 + lane, rowj[j], c);
+    brow[j] = rowj[j] / GO;
+    gsub[j] = UG == 2 ? c >> 1 : 0;
     offA[j] = group_voffset(uint32_t((m0 + rowj[j]) * d_in + 8 * c) * 2u, j);
     offB[j] = group_voffset(uint32_t((n0 + rowj[j]) * d_in + 8 * c) * 2u, j);
   }
@@ -299,28 +335,29 @@ __global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __r
   const uint32_t bytesX = uint32_t(T) * uint32_t(d_in) * 2u;
 
   // Per-slice copy state, set by prepare(): the buffer resources of the
-  // slice's K range and the W offsets for its group column (pruned rows get
-  // an out-of-range offset).  prepare() has no branches: the column of the
-  // next slice and the kept bits of this lane's rows for it are read from LDS
-  // one slice ahead, so their latency is hidden.
+  // slice's K range and the W offsets for its unit (chunks of pruned groups
+  // get an out-of-range offset).  prepare() has no branches: the unit of the
+  // next slice and the kept bits of this lane's chunks for it are read from
+  // LDS one slice ahead, so their latency is hidden.
   const uint32_t ldsA = lds_addr(As), ldsB = lds_addr(Bs);
-  auto col_of = [&](int st) { return st < nst ? st / SUB : 0; };  // slices past the end reuse column 0
+  auto col_of = [&](int st) { return st < nst ? st / SUB : 0; };  // slices past the end reuse unit 0
+  auto group_of = [&](int un, int j) { return un * UG + gsub[j]; };
   int v_cur = __builtin_amdgcn_readfirstlane(s_cols[0]);
   int v_nxt = __builtin_amdgcn_readfirstlane(s_cols[col_of(1)]);
   uint32_t bits_cur[CA];
 #pragma unroll
-  for (int j = 0; j < CA; ++j) bits_cur[j] = s_bits[rowj[j]][v_cur >> 5];
+  for (int j = 0; j < CA; ++j) bits_cur[j] = s_bits[brow[j]][group_of(v_cur, j) >> 5];
   uint32_t curA[CA];
   i32x4_t rA, rB;
   auto prepare = [&](int st) {
     const bool live = st < nst;
 #pragma unroll
-    for (int j = 0; j < CA; ++j) curA[j] = offA[j] | (((~bits_cur[j] >> (v_cur & 31)) & 1u) << 31);
-    const int k0 = live ? v_cur * G + (st % SUB) * kBK : 0;
+    for (int j = 0; j < CA; ++j) curA[j] = offA[j] | (((~bits_cur[j] >> (group_of(v_cur, j) & 31)) & 1u) << 31);
+    const int k0 = live ? v_cur * U + (st % SUB) * kBK : 0;
     rA = make_rsrc_grouped(W + k0, live ? bytesW - 2u * uint32_t(k0) : 0u);
     rB = make_rsrc_grouped(X + k0, live ? bytesX - 2u * uint32_t(k0) : 0u);
 #pragma unroll
-    for (int j = 0; j < CA; ++j) bits_cur[j] = s_bits[rowj[j]][v_nxt >> 5];
+    for (int j = 0; j < CA; ++j) bits_cur[j] = s_bits[brow[j]][group_of(v_nxt, j) >> 5];
     v_cur = v_nxt;
     v_nxt = __builtin_amdgcn_readfirstlane(s_cols[col_of(st + 2)]);
   };
@@ -335,11 +372,12 @@ __global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __r
   };
   // Soft selectors: scale this lane's freshly landed W chunks by their mask value.
   auto rescale = [&](int st) {
-    const int v = s_cols[st / SUB];
+    const int un = s_cols[st / SUB];
     u32x4* A = As[st % STAGES];
     float m[CA];
 #pragma unroll
-    for (int j = 0; j < CA; ++j) m[j] = m0 + rowj[j] < d_out ? mask[int64_t(m0 + rowj[j]) * G_in + v] : 0.0f;
+    for (int j = 0; j < CA; ++j)
+      m[j] = m0 + rowj[j] < d_out ? mask[int64_t((m0 + rowj[j]) / GO) * G_in + group_of(un, j)] : 0.0f;
     wait_vmcnt<0>();
 #pragma unroll
     for (int j = 0; j < CA; ++j) {
@@ -374,7 +412,7 @@ __global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __r
 // The epilogue forms dgate[o, v] = sum_{i in v} W[o, i] C[i, o].  For g = 512 a
 // group spans two tiles, each adding its half onto a zeroed dgate (two
 // addends onto zero: the same sum whichever lands first).
-template <int G>
+template <int G, int GO>
 __global__ __launch_bounds__(64 * kDgateWaves) void dgate_kernel(const uint16_t* __restrict__ dY, const uint16_t* __restrict__ X,
                                                     const uint16_t* __restrict__ W, int T, int d_in, int d_out,
                                                     float* __restrict__ dgate, uint16_t* __restrict__ dYt, int ldt) {
@@ -448,65 +486,126 @@ __global__ __launch_bounds__(64 * kDgateWaves) void dgate_kernel(const uint16_t*
   // Epilogue.  Lane (l >> 4, l & 15) holds, for every (mb, nb), rows
   // i = i0 .. i0 + 3 of column o: W[o, i0 .. i0 + 3] is one 8-byte load.
   const int ibase = m0 + wm * 128 + 4 * (lane >> 4);
-  float part[NB][2];  // per o column: group sums over this wave's first / second 64 rows of i
+  if constexpr (GO > 1) {
+    // Square groups (GO = G = 16 .. 128): a 16 x 16 fragment lies inside one
+    // group, so each lane sums its products per group of the wave's 128 (i) x
+    // 64 (o) sub-tile, and one reduction over the 64 lanes finishes the wave's
+    // share of each group.  Groups of 128 rows span two waves (wn pairs),
+    // which add their halves in a fixed order through LDS.
+    constexpr int IB = 128 / G;                  // groups along i in a wave
+    constexpr int OS = GO < 64 ? 64 / GO : 1;    // groups (or group halves) along o in a wave
+    float part[IB][OS];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const int o = n0 + wn * NB * 16 + nb * 16 + (lane & 15);
-    float s0 = 0.0f, s1 = 0.0f;
+    for (int a = 0; a < IB; ++a)
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      const int i0 = ibase + mb * 16;
-      if (o < d_out && i0 < d_in) {
-        const uint2 w = *reinterpret_cast<const uint2*>(W + int64_t(o) * d_in + i0);
-        const float s = acc[mb][nb][0] * bf16_lo(w.x) + acc[mb][nb][1] * bf16_hi(w.x) +
-                        acc[mb][nb][2] * bf16_lo(w.y) + acc[mb][nb][3] * bf16_hi(w.y);
-        if (mb < MB / 2) s0 += s; else s1 += s;
+      for (int b = 0; b < OS; ++b) part[a][b] = 0.0f;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int o = n0 + wn * NB * 16 + nb * 16 + (lane & 15);
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const int i0 = ibase + mb * 16;
+        if (o < d_out && i0 < d_in) {
+          const uint2 w = *reinterpret_cast<const uint2*>(W + int64_t(o) * d_in + i0);
+          part[mb * 16 / G][nb * 16 / (GO < 64 ? GO : 64)] +=
+              acc[mb][nb][0] * bf16_lo(w.x) + acc[mb][nb][1] * bf16_hi(w.x) + acc[mb][nb][2] * bf16_lo(w.y) +
+              acc[mb][nb][3] * bf16_hi(w.y);
+        }
       }
     }
-    // sum over the four lane groups (they hold the other i of the same o)
-    s0 += __shfl_xor(s0, 16);
-    s0 += __shfl_xor(s0, 32);
-    s1 += __shfl_xor(s1, 16);
-    s1 += __shfl_xor(s1, 32);
-    part[nb][0] = s0;
-    part[nb][1] = s1;
-  }
-  if constexpr (G == 64) {
-    if (lane < 16) {
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const int o = n0 + wn * NB * 16 + nb * 16 + lane;
-        const int v = (m0 + wm * 128) / 64;
-        if (o < d_out && v < G_in) dgate[int64_t(o) * G_in + v] = part[nb][0];
-        if (o < d_out && v + 1 < G_in) dgate[int64_t(o) * G_in + v + 1] = part[nb][1];
+    for (int a = 0; a < IB; ++a)
+#pragma unroll
+      for (int b = 0; b < OS; ++b) {
+        float x = part[a][b];
+#pragma unroll
+        for (int d = 32; d >= 1; d >>= 1) x += __shfl_xor(x, d);
+        part[a][b] = x;
       }
-    }
-  } else if constexpr (G == 128) {
-    if (lane < 16) {
+    const int G_out = d_out / GO;
+    if constexpr (GO < 128) {
+      if (lane == 0) {
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const int o = n0 + wn * NB * 16 + nb * 16 + lane;
-        const int v = (m0 + wm * 128) / 128;
-        if (o < d_out && v < G_in) dgate[int64_t(o) * G_in + v] = part[nb][0] + part[nb][1];
+        for (int a = 0; a < IB; ++a)
+#pragma unroll
+          for (int b = 0; b < OS; ++b) {
+            const int v = (m0 + wm * 128) / G + a;
+            const int u = (n0 + wn * 64) / GO + b;
+            if (u < G_out && v < G_in) dgate[int64_t(u) * G_in + v] = part[a][b];
+          }
+      }
+    } else {
+      float* s_half = reinterpret_cast<float*>(&As[0][0]);
+      __syncthreads();  // every wave has left its K-loop (copies drained)
+      if (lane == 0) s_half[wave] = part[0][0];
+      __syncthreads();
+      if (tid < 4) {  // group (a, b) of the tile: waves (a, 2b) and (a, 2b + 1)
+        const int a = tid >> 1, b = tid & 1;
+        const int u = n0 / GO + b, v = m0 / G + a;
+        if (u < G_out && v < G_in) dgate[int64_t(u) * G_in + v] = s_half[a * WN + 2 * b] + s_half[a * WN + 2 * b + 1];
       }
     }
   } else {
-    // The two wave rows combine through LDS, reusing the first stage buffer
-    // once every wave has finished its K-loop (their copies have drained).
-    float(*s_part)[BN] = reinterpret_cast<float(*)[BN]>(&As[0][0]);
-    __syncthreads();
-    if (lane < 16) {
+    float part[NB][2];  // per o column: group sums over this wave's first / second 64 rows of i
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) s_part[wm][wn * NB * 16 + nb * 16 + lane] = part[nb][0] + part[nb][1];
+    for (int nb = 0; nb < NB; ++nb) {
+      const int o = n0 + wn * NB * 16 + nb * 16 + (lane & 15);
+      float s0 = 0.0f, s1 = 0.0f;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const int i0 = ibase + mb * 16;
+        if (o < d_out && i0 < d_in) {
+          const uint2 w = *reinterpret_cast<const uint2*>(W + int64_t(o) * d_in + i0);
+          const float s = acc[mb][nb][0] * bf16_lo(w.x) + acc[mb][nb][1] * bf16_hi(w.x) +
+                          acc[mb][nb][2] * bf16_lo(w.y) + acc[mb][nb][3] * bf16_hi(w.y);
+          if (mb < MB / 2) s0 += s; else s1 += s;
+        }
+      }
+      // sum over the four lane groups (they hold the other i of the same o)
+      s0 += __shfl_xor(s0, 16);
+      s0 += __shfl_xor(s0, 32);
+      s1 += __shfl_xor(s1, 16);
+      s1 += __shfl_xor(s1, 32);
+      part[nb][0] = s0;
+      part[nb][1] = s1;
     }
-    __syncthreads();
-    const int o = n0 + tid;
-    if (tid < BN && o < d_out) {
-      const float h = s_part[0][tid] + s_part[1][tid];
-      if constexpr (G == 256)
-        dgate[int64_t(o) * G_in + m0 / 256] = h;
-      else
-        atomicAdd(dgate + int64_t(o) * G_in + m0 / 512, h);
+    if constexpr (G == 64) {
+      if (lane < 16) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          const int o = n0 + wn * NB * 16 + nb * 16 + lane;
+          const int v = (m0 + wm * 128) / 64;
+          if (o < d_out && v < G_in) dgate[int64_t(o) * G_in + v] = part[nb][0];
+          if (o < d_out && v + 1 < G_in) dgate[int64_t(o) * G_in + v + 1] = part[nb][1];
+        }
+      }
+    } else if constexpr (G == 128) {
+      if (lane < 16) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          const int o = n0 + wn * NB * 16 + nb * 16 + lane;
+          const int v = (m0 + wm * 128) / 128;
+          if (o < d_out && v < G_in) dgate[int64_t(o) * G_in + v] = part[nb][0] + part[nb][1];
+        }
+      }
+    } else {
+      // The two wave rows combine through LDS, reusing the first stage buffer
+      // once every wave has finished its K-loop (their copies have drained).
+      float(*s_part)[BN] = reinterpret_cast<float(*)[BN]>(&As[0][0]);
+      __syncthreads();
+      if (lane < 16) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) s_part[wm][wn * NB * 16 + nb * 16 + lane] = part[nb][0] + part[nb][1];
+      }
+      __syncthreads();
+      const int o = n0 + tid;
+      if (tid < BN && o < d_out) {
+        const float h = s_part[0][tid] + s_part[1][tid];
+        if constexpr (G == 256)
+          dgate[int64_t(o) * G_in + m0 / 256] = h;
+        else
+          atomicAdd(dgate + int64_t(o) * G_in + m0 / 512, h);
+      }
     }
   }
 }
@@ -519,16 +618,19 @@ __global__ __launch_bounds__(256) void zero_f32_kernel(float* __restrict__ p, in
 
 // ============================================================================ dX
 
-// C[i, t] = sum_k W[o_k, i] dYt[o_k, t] over the kept rows o_k of group column
-// v, tile BM (i, BM = min(g, 256)) x 256 (t); waves 2 (i) x 2 (t).  The column
-// list is read with scalar loads (eight entries per wave per slice), one slice
-// ahead of its DMA.
-template <int BM>
+// C[i, t] = sum_k W[o_k, i] dYt[o_k, t] over the listed rows o_k of list
+// column v (lc = max(g, 64) input columns), tile BM (i, BM = min(lc, 256)) x
+// 256 (t); waves 2 (i) x WN (t).  The column list is read with scalar loads
+// (KR entries per wave per slice), one slice ahead of its DMA.  With NSUB > 1
+// (groups of 16 or 32 columns) a list column holds NSUB groups and lists
+// every row that keeps one of them; each entry carries its kept bits, and the
+// 16-byte chunks of W in a pruned group are zero-filled instead of read.
+template <int BM, int NSUB>
 __global__ __launch_bounds__(64 * dx_waves(BM)) void dx_kernel(const uint16_t* __restrict__ dYt, int ldt,
                                                  const uint16_t* __restrict__ W, const int* __restrict__ colcount,
                                                  const int* __restrict__ rows, const float* __restrict__ scales,
-                                                 const int* __restrict__ colsoft, int T, int d_in, int d_out, int g,
-                                                 uint16_t* __restrict__ dX) {
+                                                 const int* __restrict__ subbits, const int* __restrict__ colsoft,
+                                                 int T, int d_in, int d_out, int lc, uint16_t* __restrict__ dX) {
   constexpr int NW = dx_waves(BM), WN = NW / 2;  // waves per block; wave grid 2 (i) x WN (t)
   constexpr int BN = 256, MB = BM / 32, NB = BN / WN / 16;
   constexpr int KR = kBK / NW;               // k-rows of a slice gathered by one wave
@@ -546,30 +648,42 @@ __global__ __launch_bounds__(64 * dx_waves(BM)) void dx_kernel(const uint16_t* _
   int tm, tn;
   tile_coords(gridDim.x, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
-  const int v = m0 / g;
+  const int v = m0 / lc;
   const int kv = colcount[v];
   const bool soft = colsoft[v] != 0;
   const int* __restrict__ rl = rows + int64_t(v) * d_out;
-  const float* __restrict__ sl = scales + int64_t(v) * d_out;
+  const int* __restrict__ bl = subbits + int64_t(v) * d_out;
+  const float* __restrict__ sl = scales + int64_t(v) * d_out * NSUB;
   const int nst = (kv + kBK - 1) / kBK;
+  constexpr int CPS = BM / 8 / NSUB;  // 16-byte chunks per group along i (NSUB > 1)
 
   // Slice st uses k-rows st*32 + r; this wave gathers rows r = KR wave .. KR wave + KR - 1,
   // whose list entries are read with scalar loads one slice ahead.
-  int idx[KR];
+  int idx[KR], kbits[NSUB > 1 ? KR : 1];
   auto load_idx = [&](int st) {  // st <= nst: at most 31 + 32 entries past the column's end
     const int base = st * kBK + wave * KR;
 #pragma unroll
-    for (int q = 0; q < KR; ++q) idx[q] = rl[base + q];  // uniform: scalar loads
+    for (int q = 0; q < KR; ++q) {
+      idx[q] = rl[base + q];  // uniform: scalar loads
+      if constexpr (NSUB > 1) kbits[q] = bl[base + q];
+    }
   };
   // Copy j of a wave in a tile with C columns (CPR = C / 8 chunks per k-row)
   // covers k-rows KR wave + j * RPI + lane / CPR, RPI = 64 / CPR: the lane's
   // row is one of RPI consecutive list entries of the wave.
-  auto pick = [&](int j, int rpi, int u) {
-    int o = idx[j * rpi];
-    for (int q = 1; q < rpi; ++q) o = u == q ? idx[j * rpi + q] : o;
+  // The entries are wave-uniform; passing them through readfirstlane keeps the
+  // compiler from turning the select chain into a per-lane indexed load from a
+  // stack copy of the array.
+  auto pick_in = [&](const int* a, int j, auto rpi_c, int u) {
+    constexpr int rpi = decltype(rpi_c)::value;
+    int o = __builtin_amdgcn_readfirstlane(a[j * rpi]);
+#pragma unroll
+    for (int q = 1; q < rpi; ++q) o = u == q ? __builtin_amdgcn_readfirstlane(a[j * rpi + q]) : o;
     return o;
   };
-  constexpr int RPI_A = 512 / BM, RPI_B = 512 / BN;
+  auto pick = [&](int j, auto rpi_c, int u) { return pick_in(idx, j, rpi_c, u); };
+  constexpr std::integral_constant<int, 512 / BM> RPI_A{};
+  constexpr std::integral_constant<int, 512 / BN> RPI_B{};
   const i32x4_t rA = make_rsrc_grouped(W + m0, (uint32_t(d_out) * uint32_t(d_in) - uint32_t(m0)) * 2u);
   const i32x4_t rB = make_rsrc_grouped(dYt + n0, (uint32_t(d_out) * uint32_t(ldt) - uint32_t(n0)) * 2u);
   uint32_t offA[NA], offB[NBC];  // this slice's per-lane offsets (rows past the list read zeros)
@@ -580,7 +694,9 @@ __global__ __launch_bounds__(64 * dx_waves(BM)) void dx_kernel(const uint16_t* _
       int row, c;
       mn_dma_target<BM>((wave * NA + j) * 64 + lane, row, c);
       const int o = pick(j, RPI_A, lane / (BM / 8));
-      offA[j] = group_voffset(uint32_t(o * d_in + 8 * c) * 2u | uint32_t(k0 + row >= kv) << 31, j);
+      bool dead = k0 + row >= kv;
+      if constexpr (NSUB > 1) dead |= ((pick_in(kbits, j, RPI_A, lane / (BM / 8)) >> (c / CPS)) & 1) == 0;
+      offA[j] = group_voffset(uint32_t(o * d_in + 8 * c) * 2u | uint32_t(dead) << 31, j);
     }
 #pragma unroll
     for (int j = 0; j < NBC; ++j) {
@@ -608,7 +724,7 @@ __global__ __launch_bounds__(64 * dx_waves(BM)) void dx_kernel(const uint16_t* _
       int row, c;
       mn_dma_target<BM>(b * 64 + lane, row, c);
       if (k0 + row < kv) {
-        const float s = sl[k0 + row];
+        const float s = NSUB > 1 ? sl[(k0 + row) * NSUB + c / CPS] : sl[k0 + row];
         u32x4* p = A + b * 64 + lane;
         if (s != 1.0f) *p = scale_bf16x8(*p, s);
       }
@@ -661,24 +777,31 @@ __global__ __launch_bounds__(256) void transpose_kernel(const uint16_t* __restri
 
 // ============================================================================ launchers
 
-#define GM_LAUNCH_G(KERNEL, GRID, THREADS, ...)                                                       \
-  switch (g) {                                                                                        \
-    case 64: hipLaunchKernelGGL(KERNEL<64>, dim3(GRID), dim3(THREADS), 0, s, __VA_ARGS__); break;   \
-    case 128: hipLaunchKernelGGL(KERNEL<128>, dim3(GRID), dim3(THREADS), 0, s, __VA_ARGS__); break; \
-    case 256: hipLaunchKernelGGL(KERNEL<256>, dim3(GRID), dim3(THREADS), 0, s, __VA_ARGS__); break; \
-    case 512: hipLaunchKernelGGL(KERNEL<512>, dim3(GRID), dim3(THREADS), 0, s, __VA_ARGS__); break; \
-    default: return hipErrorInvalidValue;                                                             \
+// The group shapes built: 1 x {64, 128, 256, 512} and square {16, 32, 64, 128}.
+#define GM_CASE_G(KERNEL, G, GO, GRID, THREADS, ...) \
+  case (G << 8) | GO: hipLaunchKernelGGL((KERNEL<G, GO>), dim3(GRID), dim3(THREADS), 0, s, __VA_ARGS__); break;
+#define GM_LAUNCH_G(KERNEL, GRID, THREADS, ...)                  \
+  switch ((g << 8) | go) {                                       \
+    GM_CASE_G(KERNEL, 64, 1, GRID, THREADS, __VA_ARGS__)         \
+    GM_CASE_G(KERNEL, 128, 1, GRID, THREADS, __VA_ARGS__)        \
+    GM_CASE_G(KERNEL, 256, 1, GRID, THREADS, __VA_ARGS__)        \
+    GM_CASE_G(KERNEL, 512, 1, GRID, THREADS, __VA_ARGS__)        \
+    GM_CASE_G(KERNEL, 16, 16, GRID, THREADS, __VA_ARGS__)        \
+    GM_CASE_G(KERNEL, 32, 32, GRID, THREADS, __VA_ARGS__)        \
+    GM_CASE_G(KERNEL, 64, 64, GRID, THREADS, __VA_ARGS__)        \
+    GM_CASE_G(KERNEL, 128, 128, GRID, THREADS, __VA_ARGS__)      \
+    default: return hipErrorInvalidValue;                        \
   }
 
 hipError_t launch_fwd(const uint16_t* X, const uint16_t* W, const float* mask, int T, int d_in, int d_out, int g,
-                      uint16_t* Y, hipStream_t s) {
+                      int go, uint16_t* Y, hipStream_t s) {
   const int tiles = ((T + 255) / 256) * ((d_out + 255) / 256);
   GM_LAUNCH_G(fwd_kernel, tiles, 64 * kFwdWaves, X, W, mask, T, d_in, d_out, Y)
   return hipGetLastError();
 }
 
 hipError_t launch_dgate(const uint16_t* dY, const uint16_t* X, const uint16_t* W, int T, int d_in, int d_out, int g,
-                        float* dgate, uint16_t* dYt, int ldt, hipStream_t s) {
+                        int go, float* dgate, uint16_t* dYt, int ldt, hipStream_t s) {
   const int tiles = ((d_out + 255) / 256) * ((d_in + 255) / 256);
   if (g == 512) {
     const int64_t n = int64_t(d_out) * (d_in / g);
@@ -698,16 +821,24 @@ hipError_t launch_transpose(const uint16_t* dY, int T, int d_out, uint16_t* dYt,
 }
 
 hipError_t launch_dx(const uint16_t* dYt, int ldt, const uint16_t* W, const int* colcount, const int* rows,
-                     const float* scales, const int* colsoft, int T, int d_in, int d_out, int g, uint16_t* dX,
-                     hipStream_t s) {
-  const int bm = g < 256 ? g : 256;
+                     const float* scales, const int* subbits, const int* colsoft, int T, int d_in, int d_out, int g,
+                     uint16_t* dX, hipStream_t s) {
+  const int lc = g < 64 ? 64 : g;  // list-column width
+  const int bm = lc < 256 ? lc : 256;
   const int tiles = (d_in / bm) * ((T + 255) / 256);
-  switch (bm) {
-    case 64: hipLaunchKernelGGL(dx_kernel<64>, dim3(tiles), dim3(64 * dx_waves(64)), 0, s, dYt, ldt, W, colcount, rows, scales, colsoft, T, d_in, d_out, g, dX); break;
-    case 128: hipLaunchKernelGGL(dx_kernel<128>, dim3(tiles), dim3(64 * dx_waves(128)), 0, s, dYt, ldt, W, colcount, rows, scales, colsoft, T, d_in, d_out, g, dX); break;
-    case 256: hipLaunchKernelGGL(dx_kernel<256>, dim3(tiles), dim3(64 * dx_waves(256)), 0, s, dYt, ldt, W, colcount, rows, scales, colsoft, T, d_in, d_out, g, dX); break;
+#define GM_DX(BM, NSUB)                                                                                        \
+  hipLaunchKernelGGL((dx_kernel<BM, NSUB>), dim3(tiles), dim3(64 * dx_waves(BM)), 0, s, dYt, ldt, W, colcount, \
+                     rows, scales, subbits, colsoft, T, d_in, d_out, lc, dX)
+  switch (g) {
+    case 16: GM_DX(64, 4); break;
+    case 32: GM_DX(64, 2); break;
+    case 64: GM_DX(64, 1); break;
+    case 128: GM_DX(128, 1); break;
+    case 256:
+    case 512: GM_DX(256, 1); break;
     default: return hipErrorInvalidValue;
   }
+#undef GM_DX
   return hipGetLastError();
 }
 

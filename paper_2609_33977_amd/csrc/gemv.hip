@@ -1,8 +1,8 @@
 // Decode-sized forward of a group-masked linear: Y[t, o] = sum over the kept
-// groups (o, v) of mask[o, v] * sum_{i in v} X[t, i] W[o, i], for up to 16
-// tokens per pass (Eq. 1 applied to the pruned model's linear).
+// groups (o / g_out, v) of mask[o / g_out, v] * sum_{i in v} X[t, i] W[o, i],
+// for up to 16 tokens per pass (Eq. 1 applied to the pruned model's linear).
 //
-// One wave per output row.  A group of g bf16 weights is g*2 contiguous bytes;
+// One wave per output row.  The row's part of a group, g bf16 weights, is g*2 contiguous bytes;
 // the wave covers 512 consecutive weights per step (512/g groups side by side,
 // 16 bytes per lane), so every kept weight is read from HBM exactly once per
 // pass and pruned groups are never touched.  Bytes per pass: 2 * nnz (kept
@@ -37,17 +37,19 @@ __device__ __forceinline__ float dot8_bf16(u32x4 w, u32x4 x) {
   return acc;
 }
 
-constexpr int kMaxGroupsPerRow = 512;  // G_in limit of the in-place variant's per-wave list
+constexpr int kMaxGroupsPerRow = 1024;  // G_in limit of the in-place variant's per-wave list
 
-template <int TB, bool PACKED>
+// MAXG: capacity of the in-place variant's per-wave list (512 or 1024; the
+// smaller list leaves more LDS for other blocks).  A row reads mask row o / go.
+template <int TB, bool PACKED, int MAXG>
 __global__ __launch_bounds__(256) void gemv_kernel(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
                                                    const float* __restrict__ mask,
                                                    const uint16_t* __restrict__ Wp, const int* __restrict__ chunk,
                                                    const float* __restrict__ scale,
                                                    const int* __restrict__ rowptr, int T, int t0, int d_in,
-                                                   int d_out, int g, uint16_t* __restrict__ Y) {
-  __shared__ int s_v[4][PACKED ? 1 : kMaxGroupsPerRow];
-  __shared__ float s_m[4][PACKED ? 1 : kMaxGroupsPerRow];
+                                                   int d_out, int g, int go, uint16_t* __restrict__ Y) {
+  __shared__ int s_v[4][PACKED ? 1 : MAXG];
+  __shared__ float s_m[4][PACKED ? 1 : MAXG];
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
   const int o = blockIdx.x * 4 + wv;
@@ -69,7 +71,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(const uint16_t* __restrict__ 
     nk = 0;
     for (int vb = 0; vb < G_in; vb += 64) {
       const int v = vb + lane;
-      const float m = v < G_in ? mask[int64_t(o) * G_in + v] : 0.0f;
+      const float m = v < G_in ? mask[int64_t(o / go) * G_in + v] : 0.0f;
       const uint64_t bal = __ballot(m != 0.0f);
       if (m != 0.0f) {
         const int r = nk + __popcll(bal & ((uint64_t(1) << lane) - 1));
@@ -142,25 +144,25 @@ __global__ __launch_bounds__(256) void gemv_kernel(const uint16_t* __restrict__ 
   }
 }
 
-template <bool PACKED>
+template <bool PACKED, int MAXG>
 static hipError_t gemv_passes(const uint16_t* X, const uint16_t* W, const float* mask, const uint16_t* Wp,
                               const int* chunk, const float* scale, const int* rowptr, int T, int d_in, int d_out,
-                              int g, uint16_t* Y, hipStream_t s) {
+                              int g, int go, uint16_t* Y, hipStream_t s) {
   const dim3 grid((d_out + 3) / 4), block(256);
   for (int t0 = 0; t0 < T; t0 += 16) {
     const int nt = T - t0;
     if (nt == 1)
-      hipLaunchKernelGGL((gemv_kernel<1, PACKED>), grid, block, 0, s, X, W, mask, Wp, chunk, scale, rowptr, T, t0,
-                         d_in, d_out, g, Y);
+      hipLaunchKernelGGL((gemv_kernel<1, PACKED, MAXG>), grid, block, 0, s, X, W, mask, Wp, chunk, scale, rowptr, T,
+                         t0, d_in, d_out, g, go, Y);
     else if (nt <= 4)
-      hipLaunchKernelGGL((gemv_kernel<4, PACKED>), grid, block, 0, s, X, W, mask, Wp, chunk, scale, rowptr, T, t0,
-                         d_in, d_out, g, Y);
+      hipLaunchKernelGGL((gemv_kernel<4, PACKED, MAXG>), grid, block, 0, s, X, W, mask, Wp, chunk, scale, rowptr, T,
+                         t0, d_in, d_out, g, go, Y);
     else if (nt <= 8)
-      hipLaunchKernelGGL((gemv_kernel<8, PACKED>), grid, block, 0, s, X, W, mask, Wp, chunk, scale, rowptr, T, t0,
-                         d_in, d_out, g, Y);
+      hipLaunchKernelGGL((gemv_kernel<8, PACKED, MAXG>), grid, block, 0, s, X, W, mask, Wp, chunk, scale, rowptr, T,
+                         t0, d_in, d_out, g, go, Y);
     else
-      hipLaunchKernelGGL((gemv_kernel<16, PACKED>), grid, block, 0, s, X, W, mask, Wp, chunk, scale, rowptr, T, t0,
-                         d_in, d_out, g, Y);
+      hipLaunchKernelGGL((gemv_kernel<16, PACKED, MAXG>), grid, block, 0, s, X, W, mask, Wp, chunk, scale, rowptr, T,
+                         t0, d_in, d_out, g, go, Y);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -168,13 +170,16 @@ static hipError_t gemv_passes(const uint16_t* X, const uint16_t* W, const float*
 }
 
 hipError_t launch_gemv_inplace(const uint16_t* X, const uint16_t* W, const float* mask, int T, int d_in, int d_out,
-                               int g, uint16_t* Y, hipStream_t s) {
-  return gemv_passes<false>(X, W, mask, nullptr, nullptr, nullptr, nullptr, T, d_in, d_out, g, Y, s);
+                               int g, int go, uint16_t* Y, hipStream_t s) {
+  if (d_in / g <= 512)
+    return gemv_passes<false, 512>(X, W, mask, nullptr, nullptr, nullptr, nullptr, T, d_in, d_out, g, go, Y, s);
+  return gemv_passes<false, kMaxGroupsPerRow>(X, W, mask, nullptr, nullptr, nullptr, nullptr, T, d_in, d_out, g, go,
+                                              Y, s);
 }
 
 hipError_t launch_gemv_packed(const uint16_t* X, const uint16_t* Wp, const int* chunk, const float* scale,
                               const int* rowptr, int T, int d_in, int d_out, int g, uint16_t* Y, hipStream_t s) {
-  return gemv_passes<true>(X, nullptr, nullptr, Wp, chunk, scale, rowptr, T, d_in, d_out, g, Y, s);
+  return gemv_passes<true, 1>(X, nullptr, nullptr, Wp, chunk, scale, rowptr, T, d_in, d_out, g, 1, Y, s);
 }
 
 int gemv_max_groups_per_row() { return kMaxGroupsPerRow; }

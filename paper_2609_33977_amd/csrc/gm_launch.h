@@ -19,24 +19,25 @@ hipError_t launch_budget_loss(const float* mask, int64_t n, const int64_t* offse
 hipError_t launch_gate_bwd_budget(const float* dgate, const float* soft, int64_t n, float tau,
                                   const int64_t* offsets, int L, const float* coeff, float* dlogits, hipStream_t s);
 
-hipError_t launch_col_lists(const float* mask, int d_out, int G_in, int* colcount, int* colsoft, int* rows,
-                            float* scales, hipStream_t s);
-hipError_t launch_pack_rows(const uint16_t* W, const float* mask, int d_in, int d_out, int g, int64_t capacity,
-                            uint16_t* Wp, int* chunk, float* scale, int* rowptr, hipStream_t s);
+// Group shapes: g_out x g (go = g_out; 1 for row groups).
+hipError_t launch_col_lists(const float* mask, int d_out, int G_in, int go, int nsub, int* colcount, int* colsoft,
+                            int* rows, float* scales, int* subbits, hipStream_t s);
+hipError_t launch_pack_rows(const uint16_t* W, const float* mask, int d_in, int d_out, int g, int go,
+                            int64_t capacity, uint16_t* Wp, int* chunk, float* scale, int* rowptr, hipStream_t s);
 
 hipError_t launch_gemv_inplace(const uint16_t* X, const uint16_t* W, const float* mask, int T, int d_in, int d_out,
-                               int g, uint16_t* Y, hipStream_t s);
+                               int g, int go, uint16_t* Y, hipStream_t s);
 hipError_t launch_gemv_packed(const uint16_t* X, const uint16_t* Wp, const int* chunk, const float* scale,
                               const int* rowptr, int T, int d_in, int d_out, int g, uint16_t* Y, hipStream_t s);
 int gemv_max_groups_per_row();
 
 hipError_t launch_fwd(const uint16_t* X, const uint16_t* W, const float* mask, int T, int d_in, int d_out, int g,
-                      uint16_t* Y, hipStream_t s);
+                      int go, uint16_t* Y, hipStream_t s);
 hipError_t launch_dgate(const uint16_t* dY, const uint16_t* X, const uint16_t* W, int T, int d_in, int d_out, int g,
-                        float* dgate, uint16_t* dYt, int ldt, hipStream_t s);
+                        int go, float* dgate, uint16_t* dYt, int ldt, hipStream_t s);
 hipError_t launch_transpose(const uint16_t* dY, int T, int d_out, uint16_t* dYt, int ldt, hipStream_t s);
 hipError_t launch_dx(const uint16_t* dYt, int ldt, const uint16_t* W, const int* colcount, const int* rows,
-                     const float* scales, const int* colsoft, int T, int d_in, int d_out, int g, uint16_t* dX,
-                     hipStream_t s);
+                     const float* scales, const int* subbits, const int* colsoft, int T, int d_in, int d_out, int g,
+                     uint16_t* dX, hipStream_t s);
 
 }  // namespace gm

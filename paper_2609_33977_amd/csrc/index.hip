@@ -1,10 +1,15 @@
-// Group index structures built from a selector matrix mask [d_out, G_in].
+// Group index structures built from a selector matrix mask [d_out / g_out, G_in]
+// (g_out x g groups; output row o belongs to mask row o / g_out).
 //
-// Column lists (consumed by the dX GEMM): for every group column v the kept
-// output rows in increasing order, rows[v * d_out + j], with their mask values
-// scales[v * d_out + j], the count colcount[v] and colsoft[v] = 1 when some
-// kept value of the column differs from 1.  This is the group-compacted
-// view of W that lets the dX K-loop visit only kept groups.
+// Column lists (consumed by the dX GEMM): list column c covers nsub
+// consecutive group columns (nsub = 1 unless groups are narrower than 64
+// columns).  For every c: the output rows that keep one of its groups, in
+// increasing order, rows[c * d_out + j], with their mask values
+// scales[(c * d_out + j) * nsub + s] for group column c * nsub + s, their kept
+// bits subbits[c * d_out + j] (bit s; written only when nsub > 1), the count
+// colcount[c] and colsoft[c] = 1 when some kept value differs from 1.  This
+// is the group-compacted view of W that lets the dX K-loop visit only kept
+// groups.
 //
 // Row-packed export (Appendix F): rowptr / packed values / group column ids,
 // written by three passes (count per row, scan, copy).
@@ -13,12 +18,13 @@
 
 namespace gm {
 
-// One 1024-thread block per group column v; scans the rows in blocks of 1024
+// One 1024-thread block per list column c; scans the rows in blocks of 1024
 // and compacts the kept ones with a wave ballot plus a 16-entry LDS prefix.
 __global__ __launch_bounds__(1024) void col_lists_kernel(const float* __restrict__ mask, int d_out, int G_in,
-                                                        int* __restrict__ colcount, int* __restrict__ colsoft,
-                                                        int* __restrict__ rows, float* __restrict__ scales) {
-  const int v = blockIdx.x;
+                                                        int go, int nsub, int* __restrict__ colcount,
+                                                        int* __restrict__ colsoft, int* __restrict__ rows,
+                                                        float* __restrict__ scales, int* __restrict__ subbits) {
+  const int c = blockIdx.x;
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   __shared__ int wave_cnt[16];
@@ -28,8 +34,17 @@ __global__ __launch_bounds__(1024) void col_lists_kernel(const float* __restrict
   int base = 0;
   for (int o0 = 0; o0 < d_out; o0 += 1024) {
     const int o = o0 + threadIdx.x;
-    const float m = o < d_out ? mask[int64_t(o) * G_in + v] : 0.0f;
-    const bool keep = m != 0.0f;
+    float m[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    int bits = 0;
+    bool soft = false;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (q < nsub && o < d_out) {
+        m[q] = mask[int64_t(o / go) * G_in + c * nsub + q];
+        bits |= int(m[q] != 0.0f) << q;
+        soft |= m[q] != 0.0f && m[q] != 1.0f;
+      }
+    const bool keep = bits != 0;
     const uint64_t bal = __ballot(keep);
     const int rank = __popcll(bal & ((uint64_t(1) << lane) - 1));
     if (lane == 0) wave_cnt[w] = __popcll(bal);
@@ -37,23 +52,27 @@ __global__ __launch_bounds__(1024) void col_lists_kernel(const float* __restrict
     int off = base;
     for (int q = 0; q < w; ++q) off += wave_cnt[q];
     if (keep) {
-      rows[int64_t(v) * d_out + off + rank] = o;
-      scales[int64_t(v) * d_out + off + rank] = m;
-      if (m != 1.0f) s_soft = 1;
+      const int64_t e = int64_t(c) * d_out + off + rank;
+      rows[e] = o;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (q < nsub) scales[e * nsub + q] = m[q];
+      if (nsub > 1) subbits[e] = bits;
+      if (soft) s_soft = 1;
     }
     for (int q = 0; q < 16; ++q) base += wave_cnt[q];
     __syncthreads();
   }
   if (threadIdx.x == 0) {
-    colcount[v] = base;
-    colsoft[v] = s_soft;
+    colcount[c] = base;
+    colsoft[c] = s_soft;
   }
 }
 
-hipError_t launch_col_lists(const float* mask, int d_out, int G_in, int* colcount, int* colsoft, int* rows,
-                            float* scales, hipStream_t s) {
-  hipLaunchKernelGGL(col_lists_kernel, dim3(G_in), dim3(1024), 0, s, mask, d_out, G_in, colcount, colsoft, rows,
-                     scales);
+hipError_t launch_col_lists(const float* mask, int d_out, int G_in, int go, int nsub, int* colcount, int* colsoft,
+                            int* rows, float* scales, int* subbits, hipStream_t s) {
+  hipLaunchKernelGGL(col_lists_kernel, dim3(G_in / nsub), dim3(1024), 0, s, mask, d_out, G_in, go, nsub, colcount,
+                     colsoft, rows, scales, subbits);
   return hipGetLastError();
 }
 
@@ -61,12 +80,12 @@ hipError_t launch_col_lists(const float* mask, int d_out, int G_in, int* colcoun
 
 // rowptr[o + 1] = number of kept groups of row o; rowptr[0] = 0.
 __global__ __launch_bounds__(256) void row_counts_kernel(const float* __restrict__ mask, int d_out, int G_in,
-                                                         int* __restrict__ rowptr) {
+                                                         int go, int* __restrict__ rowptr) {
   const int o = blockIdx.x * blockDim.x + threadIdx.x;
   if (o == 0) rowptr[0] = 0;
   if (o >= d_out) return;
   int c = 0;
-  for (int v = 0; v < G_in; ++v) c += mask[int64_t(o) * G_in + v] != 0.0f;
+  for (int v = 0; v < G_in; ++v) c += mask[int64_t(o / go) * G_in + v] != 0.0f;
   rowptr[o + 1] = c;
 }
 
@@ -94,10 +113,11 @@ __global__ __launch_bounds__(1024) void scan_rowptr_kernel(int* __restrict__ row
   }
 }
 
-// One wave per row: copies each kept group (g bf16 values) to its packed slot.
+// One wave per row: copies each kept group (g bf16 values of the row) to its
+// packed slot; a g_out x g group becomes g_out row pieces.
 __global__ __launch_bounds__(256) void pack_copy_kernel(const uint16_t* __restrict__ W,
                                                         const float* __restrict__ mask, int d_in, int d_out,
-                                                        int g, int64_t capacity, const int* __restrict__ rowptr,
+                                                        int g, int go, int64_t capacity, const int* __restrict__ rowptr,
                                                         uint16_t* __restrict__ Wp, int* __restrict__ chunk,
                                                         float* __restrict__ scale) {
   const int lane = threadIdx.x & 63;
@@ -107,7 +127,7 @@ __global__ __launch_bounds__(256) void pack_copy_kernel(const uint16_t* __restri
   int64_t j = rowptr[o];
   const int vec_per_group = g / 8;  // 16-byte vectors per group
   for (int v = 0; v < G_in; ++v) {
-    const float m = mask[int64_t(o) * G_in + v];
+    const float m = mask[int64_t(o / go) * G_in + v];
     if (m == 0.0f) continue;  // uniform across the wave
     if (j < capacity) {
       const uint16_t* src = W + int64_t(o) * d_in + int64_t(v) * g;
@@ -122,17 +142,17 @@ __global__ __launch_bounds__(256) void pack_copy_kernel(const uint16_t* __restri
   }
 }
 
-hipError_t launch_pack_rows(const uint16_t* W, const float* mask, int d_in, int d_out, int g, int64_t capacity,
-                            uint16_t* Wp, int* chunk, float* scale, int* rowptr, hipStream_t s) {
+hipError_t launch_pack_rows(const uint16_t* W, const float* mask, int d_in, int d_out, int g, int go,
+                            int64_t capacity, uint16_t* Wp, int* chunk, float* scale, int* rowptr, hipStream_t s) {
   const int G_in = d_in / g;
-  hipLaunchKernelGGL(row_counts_kernel, dim3((d_out + 255) / 256), dim3(256), 0, s, mask, d_out, G_in, rowptr);
+  hipLaunchKernelGGL(row_counts_kernel, dim3((d_out + 255) / 256), dim3(256), 0, s, mask, d_out, G_in, go, rowptr);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(scan_rowptr_kernel, dim3(1), dim3(1024), 0, s, rowptr, d_out);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(pack_copy_kernel, dim3((d_out + 3) / 4), dim3(256), 0, s, W, mask, d_in, d_out, g, capacity,
-                     rowptr, Wp, chunk, scale);
+  hipLaunchKernelGGL(pack_copy_kernel, dim3((d_out + 3) / 4), dim3(256), 0, s, W, mask, d_in, d_out, g, go,
+                     capacity, rowptr, Wp, chunk, scale);
   return hipGetLastError();
 }
 

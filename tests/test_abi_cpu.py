@@ -30,7 +30,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version_and_status_strings():
-    assert gm.gm_abi_version() == 1
+    assert gm.gm_abi_version() == 2
     for s in range(7):
         assert gm.status_string(s)
     assert gm.status_string(99) == "unknown status"
@@ -50,22 +50,50 @@ def test_workspace_size_host_only():
     assert gm.gm_workspace_size(gm.GM_OP_BWD, 77, 320, 200, 64) > 200 * 80 * 2
 
 
+@pytest.mark.parametrize("g,nsub", [(16, 4), (32, 2), (64, 1), (128, 1)])
+def test_workspace_size_square_groups(g, nsub):
+    # list columns of max(g, 64) input columns with nsub groups each: one
+    # scale per group and entry, and kept bits per entry when nsub > 1
+    T, d_in, d_out = 1000, 4096, 2048
+    NL = d_in // max(g, 64)
+    r256 = lambda x: (x + 255) // 256 * 256
+    lst = NL * d_out + 128
+    expect = (2 * r256(NL * 4) + r256(lst * 4) + r256(lst * nsub * 4) + (r256(lst * 4) if nsub > 1 else 0)
+              + r256(d_out * 1000 * 2))
+    assert gm.gm_workspace_size(gm.GM_OP_BWD, T, d_in, d_out, g, g) == expect
+    assert gm.gm_workspace_size(gm.GM_OP_FWD, T, d_in, d_out, g, g) == 0
+
+
 @pytest.mark.parametrize("args,code", [
-    ((4096, 4096, 4096, 100), gm.GM_ERR_SHAPE),      # group size not supported
-    ((4096, 4000, 4096, 256), gm.GM_ERR_SHAPE),      # d_in not a multiple of g
-    ((0, 4096, 4096, 256), gm.GM_ERR_SHAPE),         # empty T
-    ((16, 4096, 4092, 256), gm.GM_ERR_SHAPE),        # d_out not a multiple of 8
-    ((16, 64 * 1024, 64, 64), gm.GM_ERR_SHAPE),      # more than 512 group columns
+    ((4096, 4096, 4096, 100, 1), gm.GM_ERR_SHAPE),     # group size not supported
+    ((4096, 4000, 4096, 256, 1), gm.GM_ERR_SHAPE),     # d_in not a multiple of g
+    ((0, 4096, 4096, 256, 1), gm.GM_ERR_SHAPE),        # empty T
+    ((16, 4096, 4092, 256, 1), gm.GM_ERR_SHAPE),       # d_out not a multiple of 8
+    ((16, 64 * 1024, 64, 64, 1), gm.GM_ERR_SHAPE),     # more than 512 group columns
+    ((16, 4096, 4096, 16, 1), gm.GM_ERR_SHAPE),        # 1 x 16 is not a built shape
+    ((16, 4096, 4096, 32, 16), gm.GM_ERR_SHAPE),       # not square
+    ((16, 4096, 4096, 256, 256), gm.GM_ERR_SHAPE),     # square groups stop at 128
+    ((16, 4096 + 32, 4096, 16, 16), gm.GM_ERR_SHAPE),  # 16 x 16 needs d_in a multiple of 64
+    ((16, 4096, 4096 + 8, 16, 16), gm.GM_ERR_SHAPE),   # d_out not a multiple of g_out
+    ((16, 16384 + 64, 64, 16, 16), gm.GM_ERR_SHAPE),   # more than 512 units of 32 columns
+    ((16, 4096, 4096, 64, 0), gm.GM_ERR_SHAPE),
 ])
 def test_workspace_size_rejects_bad_shapes(args, code):
     out = ctypes.c_size_t(0)
     assert gm.LIB.gm_workspace_size(gm.GM_OP_BWD, *args, ctypes.byref(out)) == code
 
 
+@pytest.mark.parametrize("args", [(16, 16384, 64, 16, 16), (16, 11008, 4096, 16, 16), (16, 11008, 4096, 32, 32),
+                                  (16, 4096, 4096, 128, 128), (1, 64, 128, 64, 64)])
+def test_workspace_size_accepts_square_groups(args):
+    out = ctypes.c_size_t(0)
+    assert gm.LIB.gm_workspace_size(gm.GM_OP_BWD, *args, ctypes.byref(out)) == gm.GM_OK
+
+
 def test_workspace_size_rejects_bad_op_and_null():
     out = ctypes.c_size_t(0)
-    assert gm.LIB.gm_workspace_size(7, 16, 256, 256, 256, ctypes.byref(out)) == gm.GM_ERR_VALUE
-    assert gm.LIB.gm_workspace_size(gm.GM_OP_FWD, 16, 256, 256, 256, None) == gm.GM_ERR_NULL
+    assert gm.LIB.gm_workspace_size(7, 16, 256, 256, 256, 1, ctypes.byref(out)) == gm.GM_ERR_VALUE
+    assert gm.LIB.gm_workspace_size(gm.GM_OP_FWD, 16, 256, 256, 256, 1, None) == gm.GM_ERR_NULL
 
 
 def test_gate_argument_errors():
@@ -134,31 +162,40 @@ def test_budget_argument_errors():
 def test_linear_argument_errors():
     L = gm.LIB
     fwd = L.gm_masked_linear_fwd
-    assert fwd(None, FAKE, FAKE, 16, 256, 256, 256, FAKE, None, 0, None) == gm.GM_ERR_NULL
-    assert fwd(FAKE, FAKE, None, 16, 256, 256, 256, FAKE, None, 0, None) == gm.GM_ERR_NULL
-    assert fwd(FAKE, FAKE, FAKE, 16, 256, 256, 96, FAKE, None, 0, None) == gm.GM_ERR_SHAPE
-    assert fwd(FAKE, FAKE, FAKE, 0, 256, 256, 256, FAKE, None, 0, None) == gm.GM_ERR_SHAPE
-    assert fwd(FAKE, FAKE, FAKE, 16, 256, 250, 256, FAKE, None, 0, None) == gm.GM_ERR_SHAPE
-    assert fwd(FAKE, MISALIGNED, FAKE, 16, 256, 256, 256, FAKE, None, 0, None) == gm.GM_ERR_ALIGN
+    assert fwd(None, FAKE, FAKE, 16, 256, 256, 256, 1, FAKE, None, 0, None) == gm.GM_ERR_NULL
+    assert fwd(FAKE, FAKE, None, 16, 256, 256, 256, 1, FAKE, None, 0, None) == gm.GM_ERR_NULL
+    assert fwd(FAKE, FAKE, FAKE, 16, 256, 256, 96, 1, FAKE, None, 0, None) == gm.GM_ERR_SHAPE
+    assert fwd(FAKE, FAKE, FAKE, 0, 256, 256, 256, 1, FAKE, None, 0, None) == gm.GM_ERR_SHAPE
+    assert fwd(FAKE, FAKE, FAKE, 16, 256, 250, 256, 1, FAKE, None, 0, None) == gm.GM_ERR_SHAPE
+    assert fwd(FAKE, FAKE, FAKE, 16, 256, 256, 256, 2, FAKE, None, 0, None) == gm.GM_ERR_SHAPE
+    assert fwd(FAKE, FAKE, FAKE, 16, 256, 264, 16, 16, FAKE, None, 0, None) == gm.GM_ERR_SHAPE
+    assert fwd(FAKE, MISALIGNED, FAKE, 16, 256, 256, 256, 1, FAKE, None, 0, None) == gm.GM_ERR_ALIGN
+    assert fwd(FAKE, FAKE, MISALIGNED, 16, 256, 256, 32, 32, FAKE, None, 0, None) == gm.GM_ERR_ALIGN
 
     bwd = L.gm_masked_linear_bwd
     # dX requested without a mask
-    assert bwd(FAKE, FAKE, FAKE, None, 16, 256, 256, 256, FAKE, None, FAKE, 1 << 30, None) == gm.GM_ERR_NULL
-    assert bwd(None, FAKE, FAKE, FAKE, 16, 256, 256, 256, FAKE, FAKE, FAKE, 1 << 30, None) == gm.GM_ERR_NULL
+    assert bwd(FAKE, FAKE, FAKE, None, 16, 256, 256, 256, 1, FAKE, None, FAKE, 1 << 30, None) == gm.GM_ERR_NULL
+    assert bwd(None, FAKE, FAKE, FAKE, 16, 256, 256, 256, 1, FAKE, FAKE, FAKE, 1 << 30, None) == gm.GM_ERR_NULL
     # both outputs NULL: nothing to do
-    assert bwd(FAKE, FAKE, FAKE, FAKE, 16, 256, 256, 256, None, None, None, 0, None) == gm.GM_OK
+    assert bwd(FAKE, FAKE, FAKE, FAKE, 16, 256, 256, 256, 1, None, None, None, 0, None) == gm.GM_OK
+    assert bwd(FAKE, FAKE, FAKE, FAKE, 16, 256, 256, 16, 32, None, None, None, 0, None) == gm.GM_ERR_SHAPE
     # dX needs the workspace
     need = gm.gm_workspace_size(gm.GM_OP_BWD, 16, 256, 256, 256)
-    assert bwd(FAKE, FAKE, FAKE, FAKE, 16, 256, 256, 256, FAKE, None, None, 0, None) == gm.GM_ERR_WORKSPACE
-    assert bwd(FAKE, FAKE, FAKE, FAKE, 16, 256, 256, 256, FAKE, None, FAKE, need - 1, None) == gm.GM_ERR_WORKSPACE
-    assert bwd(FAKE, FAKE, FAKE, FAKE, 16, 256, 256, 256, FAKE, None, MISALIGNED, need, None) == gm.GM_ERR_ALIGN
-    assert bwd(FAKE, FAKE, FAKE, FAKE, 16, 256, 512, 256, FAKE, MISALIGNED, FAKE, need, None) == gm.GM_ERR_ALIGN
+    assert bwd(FAKE, FAKE, FAKE, FAKE, 16, 256, 256, 256, 1, FAKE, None, None, 0, None) == gm.GM_ERR_WORKSPACE
+    assert bwd(FAKE, FAKE, FAKE, FAKE, 16, 256, 256, 256, 1, FAKE, None, FAKE, need - 1, None) == gm.GM_ERR_WORKSPACE
+    assert bwd(FAKE, FAKE, FAKE, FAKE, 16, 256, 256, 256, 1, FAKE, None, MISALIGNED, need, None) == gm.GM_ERR_ALIGN
+    assert bwd(FAKE, FAKE, FAKE, FAKE, 16, 256, 512, 256, 1, FAKE, MISALIGNED, FAKE, need, None) == gm.GM_ERR_ALIGN
+    need16 = gm.gm_workspace_size(gm.GM_OP_BWD, 16, 256, 256, 16, 16)
+    assert need16 > need
+    assert bwd(FAKE, FAKE, FAKE, FAKE, 16, 256, 256, 16, 16, FAKE, None, FAKE, need16 - 1, None) == gm.GM_ERR_WORKSPACE
 
 
 def test_pack_argument_errors():
     L = gm.LIB
-    assert L.gm_pack_rows(FAKE, FAKE, 256, 16, 256, 16, FAKE, FAKE, None, FAKE, None) == gm.GM_ERR_NULL
-    assert L.gm_pack_rows(FAKE, FAKE, 256, 16, 256, 17, FAKE, FAKE, FAKE, FAKE, None) == gm.GM_ERR_SHAPE
-    assert L.gm_pack_rows(FAKE, FAKE, 256, 16, 256, -1, FAKE, FAKE, FAKE, FAKE, None) == gm.GM_ERR_SHAPE
+    assert L.gm_pack_rows(FAKE, FAKE, 256, 16, 256, 1, 16, FAKE, FAKE, None, FAKE, None) == gm.GM_ERR_NULL
+    assert L.gm_pack_rows(FAKE, FAKE, 256, 16, 256, 1, 17, FAKE, FAKE, FAKE, FAKE, None) == gm.GM_ERR_SHAPE
+    assert L.gm_pack_rows(FAKE, FAKE, 256, 16, 256, 1, -1, FAKE, FAKE, FAKE, FAKE, None) == gm.GM_ERR_SHAPE
+    assert L.gm_pack_rows(FAKE, FAKE, 256, 16, 32, 32, 1, FAKE, FAKE, FAKE, FAKE, None) == gm.GM_ERR_SHAPE
+    assert L.gm_pack_rows(FAKE, FAKE, 256, 16, 32, 16, 1, FAKE, FAKE, FAKE, FAKE, None) == gm.GM_ERR_SHAPE
     assert L.gm_packed_linear_fwd(FAKE, FAKE, FAKE, FAKE, None, 1, 256, 16, 256, FAKE, None) == gm.GM_ERR_NULL
     assert L.gm_packed_linear_fwd(FAKE, FAKE, FAKE, FAKE, FAKE, 1, 200, 16, 256, FAKE, None) == gm.GM_ERR_SHAPE

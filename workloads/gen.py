@@ -127,20 +127,22 @@ class LinearCase:
     X: np.ndarray       # uint16 [T, d_in]
     W: np.ndarray       # uint16 [d_out, d_in]
     dY: np.ndarray      # uint16 [T, d_out]
-    logits: np.ndarray  # f32 [d_out, d_in/g]
-    noise: np.ndarray   # f32 [d_out, d_in/g]
-    mask: np.ndarray    # f32 [d_out, d_in/g], the hard decision the gate inputs encode
+    logits: np.ndarray  # f32 [d_out/g_out, d_in/g]
+    noise: np.ndarray   # f32 [d_out/g_out, d_in/g]
+    mask: np.ndarray    # f32 [d_out/g_out, d_in/g], the hard decision the gate inputs encode
     kept: int
+    g_out: int = 1
 
 
 def make_linear_case(key: Sequence[int], T: int, d_in: int, d_out: int, g: int, kept: Optional[int],
-                     tau: float = 0.5, w_std: float = 0.02, x_std: float = 1.0, dy_std: float = 1.0) -> LinearCase:
+                     tau: float = 0.5, w_std: float = 0.02, x_std: float = 1.0, dy_std: float = 1.0,
+                     g_out: int = 1) -> LinearCase:
     """One masked linear: X ~ N(0, x_std), W ~ N(0, w_std), dY ~ N(0, dy_std), all rounded to bf16;
-    a uniformly random kept set of ``kept`` groups (half when None) and gate inputs encoding it."""
-    if d_in % g:
-        raise ValueError("d_in must be a multiple of g")
-    G_in = d_in // g
-    n = d_out * G_in
+    a uniformly random kept set of ``kept`` groups of g_out x g (half when None) and gate inputs encoding it."""
+    if d_in % g or d_out % g_out:
+        raise ValueError("d_in must be a multiple of g and d_out of g_out")
+    G_in, G_out = d_in // g, d_out // g_out
+    n = G_out * G_in
     if kept is None:
         kept = n // 2
     rng = _rng(*key)
@@ -150,8 +152,8 @@ def make_linear_case(key: Sequence[int], T: int, d_in: int, d_out: int, g: int, 
     mask = random_kept_mask(rng, n, kept)
     logits, noise = budgeted_gate_inputs(rng, mask)
     return LinearCase(T, d_in, d_out, g, tau, X, W, dY,
-                      logits.reshape(d_out, G_in), noise.reshape(d_out, G_in),
-                      mask.reshape(d_out, G_in), kept)
+                      logits.reshape(G_out, G_in), noise.reshape(G_out, G_in),
+                      mask.reshape(G_out, G_in), kept, g_out)
 
 
 def rng_for(*key: int) -> np.random.Generator:
