@@ -11,8 +11,9 @@ FLOPs 2*T*d_out*d_in for dgate (every selector receives a gradient).  Inputs
 are seeded synthetic tensors resident in HBM before timing starts.
 
 The JSON line also carries the roofline of the dominant kernel (dgate), the
-fp64 oracle timed on the host cores as a reported baseline, and the decode
-GEMV bandwidth on LLaMA-2-13B shapes.
+fp64 oracle timed on the host cores as a reported baseline, the decode GEMV
+bandwidth on LLaMA-2-13B shapes, the sparsity-budget regulariser over the
+LLaMA-2-7B selectors, and the same step with square g x g groups.
 """
 from __future__ import annotations
 
@@ -66,6 +67,7 @@ def _parse():
                     help="approximate host time spent timing the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gemv", action="store_true")
+    ap.add_argument("--no-square", action="store_true")
     ap.add_argument("--gemv-layers", type=int, default=40)
     ap.add_argument("--profile-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this size (counter calibration runs)")
@@ -99,41 +101,41 @@ def _to_device(case):
 class Step:
     """Buffers and the sequence of library calls of one mask-learning step."""
 
-    def __init__(self, d, g, tau):
+    def __init__(self, d, g, tau, g_out=1):
         import torch
         import paper_2609_33977_amd as gm
-        self.gm, self.d, self.g, self.tau = gm, d, g, tau
+        self.gm, self.d, self.g, self.g_out, self.tau = gm, d, g, g_out, tau
         T, d_in = d["X"].shape
         d_out = d["W"].shape[0]
-        G_in = d_in // g
+        G_in, G_out = d_in // g, d_out // g_out
         dev = "cuda"
-        self.mask = torch.empty(d_out, G_in, dtype=torch.float32, device=dev)
-        self.soft = torch.empty(d_out, G_in, dtype=torch.float32, device=dev)
+        self.mask = torch.empty(G_out, G_in, dtype=torch.float32, device=dev)
+        self.soft = torch.empty(G_out, G_in, dtype=torch.float32, device=dev)
         self.Y = torch.empty(T, d_out, dtype=torch.bfloat16, device=dev)
         self.dX = torch.empty(T, d_in, dtype=torch.bfloat16, device=dev)
-        self.dgate = torch.empty(d_out, G_in, dtype=torch.float32, device=dev)
-        self.dlogits = torch.empty(d_out, G_in, dtype=torch.float32, device=dev)
-        self.ws = torch.empty(max(gm.gm_workspace_size(gm.GM_OP_BWD, T, d_in, d_out, g), 16), dtype=torch.uint8,
-                              device=dev)
-        self.fws = torch.empty(max(gm.gm_workspace_size(gm.GM_OP_FWD, T, d_in, d_out, g), 16), dtype=torch.uint8,
-                               device=dev)
+        self.dgate = torch.empty(G_out, G_in, dtype=torch.float32, device=dev)
+        self.dlogits = torch.empty(G_out, G_in, dtype=torch.float32, device=dev)
+        self.ws = torch.empty(max(gm.gm_workspace_size(gm.GM_OP_BWD, T, d_in, d_out, g, g_out), 16),
+                              dtype=torch.uint8, device=dev)
+        self.fws = torch.empty(max(gm.gm_workspace_size(gm.GM_OP_FWD, T, d_in, d_out, g, g_out), 16),
+                               dtype=torch.uint8, device=dev)
 
     def gate(self):
         self.gm.gm_gate(self.d["logits"], self.d["noise"], self.tau, True, self.mask, self.soft)
 
     def fwd(self):
-        self.gm.gm_masked_linear_fwd(self.d["X"], self.d["W"], self.mask, self.g, self.Y, self.fws)
+        self.gm.gm_masked_linear_fwd(self.d["X"], self.d["W"], self.mask, self.g, self.Y, self.fws, g_out=self.g_out)
 
     def bwd(self):
         self.gm.gm_masked_linear_bwd(self.d["dY"], self.d["X"], self.d["W"], self.mask, self.g, self.dX, self.dgate,
-                                     self.ws)
+                                     self.ws, g_out=self.g_out)
 
     def gate_bwd(self):
         self.gm.gm_gate_bwd(self.dgate, self.soft, self.tau, self.dlogits)
 
     def dgate_only(self):
         self.gm.gm_masked_linear_bwd(self.d["dY"], self.d["X"], self.d["W"], self.mask, self.g, None, self.dgate,
-                                     self.ws)
+                                     self.ws, g_out=self.g_out)
 
     def __call__(self):
         self.gate()
@@ -180,6 +182,41 @@ def _cpu_baseline(case, flops_per_step, budget_s):
     return {"value": flops_per_step / sec / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
             "sample": f"{reps} whole step(s) of the headline workload (gate, fwd, dX, dgate, STE) in fp64 NumPy, "
                       f"{sec:.2f} s per step"}
+
+
+# ------------------------------------------------------------------ square groups
+
+def _square_groups(d, case, reps):
+    """The same step on the headline tensors with g x g groups (g = 16 .. 128), half of the groups kept."""
+    import torch
+    import workloads
+    T, d_in, d_out = case.T, case.d_in, case.d_out
+    out = {"workload": f"headline tensors (T {T}, W {d_out}x{d_in}) with square g x g groups, 50% kept at random"}
+    for g in (16, 32, 64, 128):
+        G = (d_out // g) * (d_in // g)
+        r = workloads.gen.rng_for(2, 1, g)
+        keep = workloads.random_kept_mask(r, G, G // 2)
+        logits, noise = workloads.budgeted_gate_inputs(r, keep)
+        shape = (d_out // g, d_in // g)
+        dd = dict(d, logits=torch.from_numpy(np.ascontiguousarray(logits.reshape(shape), dtype=np.float32)).cuda(),
+                  noise=torch.from_numpy(np.ascontiguousarray(noise.reshape(shape), dtype=np.float32)).cuda())
+        step = Step(dd, g, case.tau, g_out=g)
+        for _ in range(3):
+            step()
+        torch.cuda.synchronize()
+        if int(step.mask.sum().item()) != G // 2:
+            raise RuntimeError(f"gate kept count differs from the budget ({g}x{g})")
+        nnz = (G // 2) * g * g
+        fl = {"fwd": 2.0 * T * nnz, "dx": 2.0 * T * nnz, "dgate": 2.0 * T * d_out * d_in}
+        ms = _events_ms(step, reps)
+        br = {name: _events_ms(getattr(step, name), reps) for name in ("fwd", "bwd")}
+        dg = _events_ms(step.dgate_only, reps)
+        out[f"{g}x{g}"] = {"ms_per_step": ms, "TFLOP/s": sum(fl.values()) / (ms / 1e3) / 1e12,
+                           "fwd_ms": br["fwd"], "fwd_kept_TFLOP/s": fl["fwd"] / (br["fwd"] / 1e3) / 1e12,
+                           "bwd_ms": br["bwd"], "dgate_ms": dg,
+                           "dgate_TFLOP/s": fl["dgate"] / (dg / 1e3) / 1e12}
+        del step, dd
+    return out
 
 
 # ------------------------------------------------------------------ decode GEMV
@@ -317,6 +354,10 @@ def main():
 
     budget = _budget_bandwidth(max(5, args.steps))
 
+    square = None
+    if not args.no_square:
+        square = _square_groups(d, case, max(5, args.steps // 2))
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = _cpu_baseline(case, flops_step, args.cpu_seconds)
@@ -348,6 +389,7 @@ def main():
         "cpu_baseline": cpu,
         "gemv": gemv,
         "budget": budget,
+        "square_groups": square,
     }
     print(json.dumps(out), flush=True)
 

@@ -104,6 +104,11 @@ __device__ __forceinline__ void mfma_row(int mb, const u32x4& af, const u32x4 (&
   for (int nb = 0; nb < NB; ++nb) mfma_at<FIRST>(mb, nb, af, bf[nb], acc);
 }
 
+// Every fragment row of the wave computes every slice.
+struct AllRows {
+  __device__ uint32_t operator()(int) const { return ~0u; }
+};
+
 // The K-loop shared by the three GEMMs.  `prepare(st)` computes whatever the
 // copies of K slice st need (buffer resources, per-lane offsets); it is called
 // once per slice, in increasing st, at a point where this wave has no LDS read
@@ -114,7 +119,10 @@ __device__ __forceinline__ void mfma_row(int mb, const u32x4& af, const u32x4 (&
 // this wave's copies of slice st completed and before the barrier that
 // publishes them (soft-selector rescaling).  `bhook(kt, bf)` sees the B
 // fragments of slice kt once they are in registers.  The accumulators are
-// written by the first slice's MFMAs (zero when nst is 0).
+// written by the first slice's MFMAs (zero when nst is 0).  `live(kt)`
+// (wave-uniform) has bit mb set when fragment row mb needs the MFMAs of slice
+// kt; rows whose A operand is all zeros for the slice skip them.  The first
+// slice runs every row, since its MFMAs also initialise the accumulators.
 //
 // Software pipeline: rows 0 .. MB-2 of slice kt run first (A fragments
 // streamed one row ahead); then the wave waits for slice kt+1, meets the
@@ -127,10 +135,10 @@ __device__ __forceinline__ void mfma_row(int mb, const u32x4& af, const u32x4 (&
 // and the loop body has no branches around the accumulators; the first and
 // the last slice are peeled off.
 template <int MB, int NB, bool A_KM, bool B_KM, int CA, int CB, int PER_STAGE, int STAGES, int ABUF, int BBUF,
-          class Prepare, class Issue, class Landed, class BHook>
+          class Prepare, class Issue, class Landed, class BHook, class Live = AllRows>
 __device__ __forceinline__ void gemm_mainloop(u32x4 (*As)[ABUF], u32x4 (*Bs)[BBUF], int nst, int a0, int b0, int lane,
                                               f32x4 (&acc)[MB][NB], Prepare&& prepare, Issue&& issue,
-                                              Landed&& landed, BHook&& bhook) {
+                                              Landed&& landed, BHook&& bhook, Live live = Live{}) {
   static_assert(PER_STAGE <= NB, "copies are interleaved with the NB MFMAs of one row");
   constexpr int AHEAD = PER_STAGE * (STAGES - 2);  // copies issued after the slice being waited for
   if (nst <= 0) {
@@ -161,12 +169,13 @@ __device__ __forceinline__ void gemm_mainloop(u32x4 (*As)[ABUF], u32x4 (*Bs)[BBU
   // the last row interleaved with the next slice's copies and fragment reads.
   auto slice = [&](int kt, auto first) {
     constexpr bool FIRST = decltype(first)::value;
+    const uint32_t lv = FIRST ? ~0u : live(kt);
     bhook(kt, bf);
     const u32x4* A = As[kt % STAGES];
 #pragma unroll
     for (int mb = 0; mb < MB - 1; ++mb) {
       const u32x4 an = load_afrag<A_KM, CA>(A, a0 + (mb + 1) * 16, lane);
-      mfma_row<FIRST, MB, NB>(mb, af, bf, acc);
+      if ((lv >> mb) & 1u) mfma_row<FIRST, MB, NB>(mb, af, bf, acc);
       af = an;
     }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's reads of slice kt are done
@@ -177,7 +186,7 @@ __device__ __forceinline__ void gemm_mainloop(u32x4 (*As)[ABUF], u32x4 (*Bs)[BBU
     const u32x4* Bn = Bs[(kt + 1) % STAGES];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      mfma_at<FIRST, MB, NB>(MB - 1, nb, af, bf[nb], acc);
+      if ((lv >> (MB - 1)) & 1u) mfma_at<FIRST, MB, NB>(MB - 1, nb, af, bf[nb], acc);
       __builtin_amdgcn_sched_barrier(0);
       if (nb < PER_STAGE) issue(kt + STAGES, nb);
       bf[nb] = B_KM ? km_frag(Bn, b0 + nb * 16, lane) : mn_frag<CB>(Bn, b0 + nb * 16, lane);
@@ -188,15 +197,16 @@ __device__ __forceinline__ void gemm_mainloop(u32x4 (*As)[ABUF], u32x4 (*Bs)[BBU
   // The last slice: all rows, no further copies.
   auto last = [&](auto first) {
     constexpr bool FIRST = decltype(first)::value;
+    const uint32_t lv = FIRST ? ~0u : live(nst - 1);
     bhook(nst - 1, bf);
     const u32x4* A = As[(nst - 1) % STAGES];
 #pragma unroll
     for (int mb = 0; mb < MB - 1; ++mb) {
       const u32x4 an = load_afrag<A_KM, CA>(A, a0 + (mb + 1) * 16, lane);
-      mfma_row<FIRST, MB, NB>(mb, af, bf, acc);
+      if ((lv >> mb) & 1u) mfma_row<FIRST, MB, NB>(mb, af, bf, acc);
       af = an;
     }
-    mfma_row<FIRST, MB, NB>(MB - 1, af, bf, acc);
+    if ((lv >> (MB - 1)) & 1u) mfma_row<FIRST, MB, NB>(MB - 1, af, bf, acc);
   };
 
   if (nst == 1) {
@@ -247,6 +257,7 @@ __global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __r
   __shared__ uint32_t s_bits[RB][MAXG / 32];  // kept bits of the tile's mask rows
   __shared__ uint32_t s_any[MAXU / 32];       // unit kept by some row of the tile
   __shared__ int s_cols[MAXU];
+  __shared__ uint32_t s_live[GO >= 32 ? MAXU : 1];  // per listed unit: bit f = 16-row fragment f of the tile keeps it
   __shared__ int s_ncols, s_soft;
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -309,7 +320,22 @@ __global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __r
       const int un = ub + lane;
       const bool f = un < NU && ((s_any[un >> 5] >> (un & 31)) & 1);
       const uint64_t bal = __ballot(f);
-      if (f) s_cols[cnt + __popcll(bal & ((uint64_t(1) << lane) - 1))] = un;
+      if (f) {
+        const int pos = cnt + __popcll(bal & ((uint64_t(1) << lane) - 1));
+        s_cols[pos] = un;
+        if constexpr (GO >= 32) {
+          // square groups: all rows of a mask row share the unit's kept bits
+          uint32_t live = 0;
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) {
+            uint32_t k = 0;
+#pragma unroll
+            for (int q = 0; q < UG; ++q) k |= s_bits[rb][(un * UG + q) >> 5] >> ((un * UG + q) & 31);
+            if (k & 1u) live |= ((1u << (GO / 16)) - 1u) << (rb * (GO / 16));
+          }
+          s_live[pos] = live;
+        }
+      }
       cnt += __popcll(bal);
     }
     if (lane == 0) s_ncols = cnt;
@@ -344,6 +370,13 @@ __global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __r
   auto group_of = [&](int un, int j) { return un * UG + gsub[j]; };
   int v_cur = __builtin_amdgcn_readfirstlane(s_cols[0]);
   int v_nxt = __builtin_amdgcn_readfirstlane(s_cols[col_of(1)]);
+  // Square groups of 32 rows and more: fragment rows of this wave that keep
+  // the unit of the slice consumed next (slice st - STAGES + 1 when
+  // prepare(st) runs).  With 16 x 16 groups a fragment row skips a 32-deep
+  // slice only when both of its groups are pruned, and the branches cost more
+  // than the skipped MFMAs save, so every row runs.
+  constexpr bool SKIP = GO >= 32;
+  uint32_t live_nxt = ~0u;
   uint32_t bits_cur[CA];
 #pragma unroll
   for (int j = 0; j < CA; ++j) bits_cur[j] = s_bits[brow[j]][group_of(v_cur, j) >> 5];
@@ -360,7 +393,10 @@ __global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __r
     for (int j = 0; j < CA; ++j) bits_cur[j] = s_bits[brow[j]][group_of(v_nxt, j) >> 5];
     v_cur = v_nxt;
     v_nxt = __builtin_amdgcn_readfirstlane(s_cols[col_of(st + 2)]);
+    if constexpr (SKIP)
+      live_nxt = (__builtin_amdgcn_readfirstlane(s_live[col_of(max(st - STAGES + 1, 0))]) >> (wm * 8)) & 0xffu;
   };
+  auto live = [&](int) { return live_nxt; };
   // copies 0..CA-1 fill this wave's row blocks of the W tile, CA..2CA-1 of the X tile
   auto issue = [&](int st, int p) {
     const int j = p % CA;
@@ -391,10 +427,10 @@ __global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __r
   f32x4 acc[MB][NB];
   if (s_soft)
     gemm_mainloop<MB, NB, true, true, 0, 0, PER_STAGE, STAGES>(As, Bs, nst, wm * 128, wn * NB * 16, lane, acc, prepare,
-                                                              issue, rescale, [](int, const u32x4(&)[NB]) {});
+                                                              issue, rescale, [](int, const u32x4(&)[NB]) {}, live);
   else
     gemm_mainloop<MB, NB, true, true, 0, 0, PER_STAGE, STAGES>(As, Bs, nst, wm * 128, wn * NB * 16, lane, acc, prepare,
-                                                              issue, [](int) {}, [](int, const u32x4(&)[NB]) {});
+                                                              issue, [](int) {}, [](int, const u32x4(&)[NB]) {}, live);
 
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
