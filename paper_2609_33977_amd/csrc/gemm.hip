@@ -707,14 +707,16 @@ __global__ __launch_bounds__(64 * dx_waves(BM)) void dx_kernel(const uint16_t* _
   // Copy j of a wave in a tile with C columns (CPR = C / 8 chunks per k-row)
   // covers k-rows KR wave + j * RPI + lane / CPR, RPI = 64 / CPR: the lane's
   // row is one of RPI consecutive list entries of the wave.
-  // The entries are wave-uniform; passing them through readfirstlane keeps the
-  // compiler from turning the select chain into a per-lane indexed load from a
-  // stack copy of the array.
+  // The entries are wave-uniform.  For chains of more than two, passing them
+  // through readfirstlane keeps the compiler from turning the selects into a
+  // per-lane indexed load from a stack copy of the array (for two it emits
+  // one select, and the extra moves would only cost VALU issue slots).
   auto pick_in = [&](const int* a, int j, auto rpi_c, int u) {
     constexpr int rpi = decltype(rpi_c)::value;
-    int o = __builtin_amdgcn_readfirstlane(a[j * rpi]);
+    auto entry = [&](int q) { return rpi > 2 ? __builtin_amdgcn_readfirstlane(a[j * rpi + q]) : a[j * rpi + q]; };
+    int o = entry(0);
 #pragma unroll
-    for (int q = 1; q < rpi; ++q) o = u == q ? __builtin_amdgcn_readfirstlane(a[j * rpi + q]) : o;
+    for (int q = 1; q < rpi; ++q) o = u == q ? entry(q) : o;
     return o;
   };
   auto pick = [&](int j, auto rpi_c, int u) { return pick_in(idx, j, rpi_c, u); };
