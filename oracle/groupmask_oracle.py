@@ -31,6 +31,12 @@ design notes of the repository):
   is nonzero (the discrete B).  Its gradient is the derivative of the loss
   with B taken as continuous (what the STE hands to the relaxation), with
   sign(0) = 0 at s = s_t; the uniform variant sums the per-layer terms.
+* Distillation loss (Sec. 2.4, Eq. 4): teacher and student logits come from
+  one frozen LM head applied to the final hidden states of the dense (teacher)
+  and the masked (student) pass; N counts the valid tokens (a per-token flag);
+  with no valid token the loss and its gradient are zero.  The gradient goes
+  to the student's hidden states only (the teacher is detached, the LM head
+  is frozen).
 """
 from __future__ import annotations
 
@@ -40,6 +46,7 @@ __all__ = [
     "from_bf16", "logistic_noise", "gate", "gate_bwd", "expand_mask", "masked_weight",
     "linear_fwd", "linear_bwd_dx", "linear_bwd_dgate", "linear_bwd", "sparsity",
     "preserved_rate", "near_threshold", "kept_count", "budget_loss",
+    "softmax_rows", "distill_loss", "distill_loss_bwd",
 ]
 
 
@@ -208,3 +215,57 @@ def budget_loss(selectors, params, s_target: float, lam: float, uniform: bool = 
             L = float(lam * abs(logr))
             coeff = lam * np.sign(logr) / s * (-(P / G) / np.sum(P))
     return L, coeff, kept
+
+
+# ------------------------------------------------ distillation loss (Sec. 2.4, Eq. 4)
+
+def softmax_rows(z) -> np.ndarray:
+    """Softmax over the last axis: exp(z - max) / sum(exp(z - max))."""
+    z = np.asarray(z, dtype=np.float64)
+    e = np.exp(z - z.max(axis=-1, keepdims=True))
+    return e / e.sum(axis=-1, keepdims=True)
+
+
+def _lm_logits(H, W) -> np.ndarray:
+    """Logits of the LM head: z[t, v] = sum_j H[t, j] W[v, j]."""
+    return np.asarray(H, dtype=np.float64) @ np.asarray(W, dtype=np.float64).T
+
+
+def distill_loss(H_t, H_s, W, valid=None):
+    """Self-distillation loss of Eq. 4 over N valid tokens.
+
+    L = -(1/N) sum_{valid t} sum_v p_T(t, v) log p_S(t, v), with p_T, p_S the
+    softmax over the vocabulary of the teacher and student logits H W^T.
+    Returns (L, ce, lse_t, lse_s): ce[t] = -sum_v p_T log p_S per token (for
+    every token, valid or not) and the log-sum-exp of each token's teacher and
+    student logits.
+    """
+    z_t, z_s = _lm_logits(H_t, W), _lm_logits(H_s, W)
+    m_s = z_s.max(axis=1, keepdims=True)
+    lse_s = (m_s + np.log(np.exp(z_s - m_s).sum(axis=1, keepdims=True)))[:, 0]
+    m_t = z_t.max(axis=1, keepdims=True)
+    lse_t = (m_t + np.log(np.exp(z_t - m_t).sum(axis=1, keepdims=True)))[:, 0]
+    p_t = softmax_rows(z_t)
+    log_p_s = z_s - lse_s[:, None]
+    ce = -(p_t * log_p_s).sum(axis=1)
+    v = np.ones(ce.shape[0], dtype=bool) if valid is None else np.asarray(valid) != 0
+    n = int(v.sum())
+    L = float(ce[v].sum() / n) if n else 0.0
+    return L, ce, lse_t, lse_s
+
+
+def distill_loss_bwd(H_t, H_s, W, valid=None) -> np.ndarray:
+    """Gradient of Eq. 4 with respect to the student's hidden states.
+
+    dL/dz_S[t, v] = (p_S(t, v) - p_T(t, v)) / N for a valid token (the teacher
+    probabilities sum to one), zero otherwise; dH_S = dz_S W.
+    """
+    W = np.asarray(W, dtype=np.float64)
+    p_t = softmax_rows(_lm_logits(H_t, W))
+    p_s = softmax_rows(_lm_logits(H_s, W))
+    v = np.ones(p_t.shape[0], dtype=bool) if valid is None else np.asarray(valid) != 0
+    n = int(v.sum())
+    dz = np.zeros_like(p_s)
+    if n:
+        dz[v] = (p_s[v] - p_t[v]) / n
+    return dz @ W

@@ -441,6 +441,100 @@ def test_budget_uniform_variant_is_the_sum_of_single_layer_losses():
     assert np.allclose(cu, [x[1][0] for x in singles], rtol=1e-12, atol=0)
 
 
+# ------------------------------------------- distillation loss (Sec. 2.4, Eq. 4)
+
+def _distill_case(N, V, d, key, noise=0.5, w_scale=1.0):
+    H_t = _rand((N, d), (60,) + key)
+    H_s = H_t + noise * _rand((N, d), (61,) + key)
+    W = _rand((V, d), (62,) + key, w_scale)
+    return H_t, H_s, W
+
+
+def test_distill_matches_brute_force_loops():
+    H_t, H_s, W = _distill_case(3, 5, 4, (0,))
+    total = 0.0
+    for t in range(3):
+        zt = [sum(H_t[t][j] * W[v][j] for j in range(4)) for v in range(5)]
+        zs = [sum(H_s[t][j] * W[v][j] for j in range(4)) for v in range(5)]
+        et, es = [math.exp(x) for x in zt], [math.exp(x) for x in zs]
+        total -= sum(et[v] / sum(et) * math.log(es[v] / sum(es)) for v in range(5))
+    L, ce, _, _ = oracle.distill_loss(H_t, H_s, W)
+    assert abs(L - total / 3) <= 1e-12 * abs(total)
+    assert abs(ce.mean() - total / 3) <= 1e-12 * abs(total)
+
+
+def test_distill_is_kl_plus_teacher_entropy():
+    # the identity stated after Eq. 4: cross-entropy = KL(p_T || p_S) + H(p_T)
+    from scipy.special import entr, rel_entr, softmax
+    H_t, H_s, W = _distill_case(6, 40, 16, (1,), w_scale=0.7)
+    p_t, p_s = softmax(H_t @ W.T, axis=1), softmax(H_s @ W.T, axis=1)
+    ref = (rel_entr(p_t, p_s).sum(axis=1) + entr(p_t).sum(axis=1)).mean()
+    L, _, _, _ = oracle.distill_loss(H_t, H_s, W)
+    assert abs(L - ref) <= 1e-12 * abs(ref)
+
+
+def test_distill_of_identical_passes_is_teacher_entropy_with_zero_gradient():
+    from scipy.special import softmax
+    from scipy.stats import entropy
+    H_t, H_s, W = _distill_case(5, 30, 12, (2,))
+    L0, _, _, _ = oracle.distill_loss(H_t, H_t, W)
+    assert abs(L0 - entropy(softmax(H_t @ W.T, axis=1), axis=1).mean()) <= 1e-12 * L0
+    assert not np.any(oracle.distill_loss_bwd(H_t, H_t, W))
+    L1, ce1, _, _ = oracle.distill_loss(H_t, H_s, W)
+    _, ce0, _, _ = oracle.distill_loss(H_t, H_t, W)
+    assert L1 > L0 and np.all(ce1 >= ce0)  # Gibbs: cross-entropy >= entropy
+
+
+def test_distill_one_hot_teacher_is_cross_entropy():
+    from scipy.special import log_softmax
+    N, V, d = 4, 9, 64
+    _, H_s, W = _distill_case(N, V, d, (3,))
+    k = np.array([2, 7, 0, 7])
+    H_t = 200.0 * W[k] / np.linalg.norm(W[k], axis=1, keepdims=True)  # the target row dominates by > 700 nats
+    L, _, _, _ = oracle.distill_loss(H_t, H_s, W)
+    ref = -log_softmax(H_s @ W.T, axis=1)[np.arange(N), k].mean()
+    assert abs(L - ref) <= 1e-12 * abs(ref)
+
+
+def test_distill_uniform_teacher():
+    from scipy.special import logsumexp
+    _, H_s, W = _distill_case(5, 17, 8, (4,))
+    L, _, lse_t, lse_s = oracle.distill_loss(np.zeros_like(H_s), H_s, W)
+    z = H_s @ W.T
+    ref = (logsumexp(z, axis=1) - z.mean(axis=1)).mean()
+    assert abs(L - ref) <= 1e-12 * abs(ref)
+    assert np.allclose(lse_t, np.log(17.0), rtol=1e-15, atol=0)
+    assert np.allclose(lse_s, logsumexp(z, axis=1), rtol=1e-13, atol=0)
+
+
+def test_distill_gradient_matches_finite_differences():
+    H_t, H_s, W = _distill_case(4, 11, 6, (5,))
+    dH = oracle.distill_loss_bwd(H_t, H_s, W)
+    h = 1e-5
+    for t, j in itertools.product(range(4), range(6)):
+        Hp, Hm = H_s.copy(), H_s.copy()
+        Hp[t, j] += h
+        Hm[t, j] -= h
+        fd = (oracle.distill_loss(H_t, Hp, W)[0] - oracle.distill_loss(H_t, Hm, W)[0]) / (2 * h)
+        assert abs(fd - dH[t, j]) <= 1e-8 * (1 + abs(dH[t, j]))
+
+
+def test_distill_counts_only_valid_tokens():
+    H_t, H_s, W = _distill_case(7, 13, 5, (6,))
+    valid = np.array([1, 0, 1, 1, 0, 0, 1], dtype=np.uint8)
+    sub = valid != 0
+    L, ce, _, _ = oracle.distill_loss(H_t, H_s, W, valid)
+    L_sub, ce_sub, _, _ = oracle.distill_loss(H_t[sub], H_s[sub], W)
+    assert abs(L - L_sub) <= 1e-14 * abs(L_sub)
+    assert np.array_equal(ce[sub], ce_sub)
+    dH = oracle.distill_loss_bwd(H_t, H_s, W, valid)
+    assert not np.any(dH[~sub])
+    np.testing.assert_allclose(dH[sub], oracle.distill_loss_bwd(H_t[sub], H_s[sub], W), rtol=1e-14, atol=0)
+    none = np.zeros(7, dtype=np.uint8)
+    assert oracle.distill_loss(H_t, H_s, W, none)[0] == 0.0
+    assert not np.any(oracle.distill_loss_bwd(H_t, H_s, W, none))
+
+
 # ------------------------------------------------------- the pins catch mistakes
 
 def _mutant_fwd_strided_groups(X, W, B, g, g_out=1):
@@ -529,6 +623,39 @@ def _mutant_budget_grad_no_inv_s(selectors, params, s_target, lam, uniform=False
     return L, c * (s_l if uniform else s), k
 
 
+_ORIG_DISTILL = oracle.distill_loss
+_ORIG_DISTILL_BWD = oracle.distill_loss_bwd
+
+
+def _mutant_distill_sum(H_t, H_s, W, valid=None):
+    L, ce, lt, ls = _ORIG_DISTILL(H_t, H_s, W, valid)
+    n = len(ce) if valid is None else int(np.count_nonzero(valid))
+    return L * n, ce, lt, ls
+
+
+def _mutant_distill_reversed(H_t, H_s, W, valid=None):
+    return _ORIG_DISTILL(H_s, H_t, W, valid)
+
+
+def _mutant_distill_over_tokens(H_t, H_s, W, valid=None):
+    # softmax over the token axis instead of the vocabulary
+    z_t, z_s = np.asarray(H_t, float) @ np.asarray(W, float).T, np.asarray(H_s, float) @ np.asarray(W, float).T
+    p_t = oracle.softmax_rows(z_t.T).T
+    ls = z_s - np.log(np.exp(z_s).sum(axis=0, keepdims=True))
+    ce = -(p_t * ls).sum(axis=1)
+    _, _, lse_t, lse_s = _ORIG_DISTILL(H_t, H_s, W, valid)
+    return float(ce.mean()), ce, lse_t, lse_s
+
+
+def _mutant_distill_bwd_sign(H_t, H_s, W, valid=None):
+    return -_ORIG_DISTILL_BWD(H_t, H_s, W, valid)
+
+
+def _mutant_distill_bwd_no_teacher(H_t, H_s, W, valid=None):
+    p_s = oracle.softmax_rows(np.asarray(H_s, float) @ np.asarray(W, float).T)
+    return p_s / p_s.shape[0] @ np.asarray(W, float)
+
+
 MUTANTS = [
     ("linear_fwd", _mutant_fwd_strided_groups),
     ("linear_fwd", _mutant_fwd_strided_rows),
@@ -544,6 +671,11 @@ MUTANTS = [
     ("budget_loss", _mutant_budget_unweighted),
     ("budget_loss", _mutant_budget_grad_sign),
     ("budget_loss", _mutant_budget_grad_no_inv_s),
+    ("distill_loss", _mutant_distill_sum),
+    ("distill_loss", _mutant_distill_reversed),
+    ("distill_loss", _mutant_distill_over_tokens),
+    ("distill_loss_bwd", _mutant_distill_bwd_sign),
+    ("distill_loss_bwd", _mutant_distill_bwd_no_teacher),
 ]
 
 PIN_TESTS = [
@@ -565,6 +697,13 @@ PIN_TESTS = [
     test_budget_global_sparsity_is_the_fraction_of_pruned_weights,
     lambda: test_budget_gradient_matches_selector_flips(False),
     lambda: test_budget_gradient_matches_selector_flips(True),
+    test_distill_matches_brute_force_loops,
+    test_distill_is_kl_plus_teacher_entropy,
+    test_distill_of_identical_passes_is_teacher_entropy_with_zero_gradient,
+    test_distill_one_hot_teacher_is_cross_entropy,
+    test_distill_uniform_teacher,
+    test_distill_gradient_matches_finite_differences,
+    test_distill_counts_only_valid_tokens,
 ]
 
 
