@@ -29,7 +29,7 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-GEMM_SOURCES = ["paper_2609_33977_amd/csrc/gemm.hip", "paper_2609_33977_amd/csrc/gm_pipe.h",
+GEMM_SOURCES = ["paper_2609_33977_amd/csrc/gemm.hip", "paper_2609_33977_amd/csrc/gm_gemm.h", "paper_2609_33977_amd/csrc/gm_pipe.h",
                 "paper_2609_33977_amd/csrc/gm_device.h"]
 
 # HBM traffic of one dgate_kernel<256> launch on the headline workload, from

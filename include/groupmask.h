@@ -224,6 +224,53 @@ gm_status gm_packed_linear_fwd(const uint16_t* X, const uint16_t* Wp, const int3
                                const float* scale, const int32_t* rowptr, int64_t T, int64_t d_in,
                                int64_t d_out, int32_t g, uint16_t* Y, gm_stream_t stream);
 
+/*
+ * Self-distillation loss through the frozen LM head (Sec. 2.4, Eq. 4).
+ * The teacher pass (all selectors 1) and the student pass (the learned
+ * selectors) end in final hidden states H_T, H_S [N, d] (bf16), and share
+ * the LM head W [V, d] (bf16, row v = vocabulary entry v).  With
+ * z = H W^T, p = softmax over the vocabulary, and N_valid the number of
+ * tokens whose `valid` flag is nonzero (all N when valid is NULL):
+ *   L = -(1/N_valid) sum_{valid t} sum_v p_T(t, v) log p_S(t, v)
+ * (the forward KL from teacher to student plus the teacher entropy, which
+ * does not depend on the student).  Gradients go to H_S only (the teacher is
+ * detached, the LM head frozen):
+ *   dH_S = dz_S W,  dz_S(t, v) = (p_S(t, v) - p_T(t, v)) / N_valid for valid t, 0 otherwise.
+ * With no valid token, L = 0 and dH_S = 0.
+ * Shapes: N >= 1; d a multiple of 32 in [32, 65536]; V a multiple of 8 in
+ * [8, 2^20]; V d, N d and N ceil32(V) each below 2^30 - 2^22 elements.
+ * Logits are accumulated in fp32 from the bf16 inputs; softmax statistics
+ * and the token sums in fp32/fp64; dz_S is rounded to bf16 before the
+ * product with W.
+ *
+ * gm_distill_workspace_size -- host-only query of the workspace both calls
+ * below need (bytes; about 8 N V + 2 N V bytes: the fp32 logits of both passes
+ * and the bf16 dz_S).  bytes: HOST pointer, required.
+ */
+gm_status gm_distill_workspace_size(int64_t N, int64_t d, int64_t V, size_t* bytes);
+
+/*
+ * gm_distill_fwd -- the loss.
+ *   Ht, Hs [N, d] bf16; W [V, d] bf16; valid [N] uint8 or NULL;
+ *   loss: one fp32 (device), written; ce [N] fp32 or NULL: each token's
+ *   cross-entropy -sum_v p_T log p_S (for every token, valid or not).
+ *   ws / ws_bytes: caller-owned workspace of gm_distill_workspace_size bytes;
+ *   it receives both passes' logits and per-token statistics, which
+ *   gm_distill_bwd reads.  loss and ce need 4-byte alignment.
+ */
+gm_status gm_distill_fwd(const uint16_t* Ht, const uint16_t* Hs, const uint16_t* W, const uint8_t* valid,
+                         int64_t N, int64_t d, int64_t V, float* loss, float* ce, void* ws, size_t ws_bytes,
+                         gm_stream_t stream);
+
+/*
+ * gm_distill_bwd -- dH_S [N, d] bf16 (written in full) from the workspace
+ * that the last gm_distill_fwd on the same stream filled for the same W, N,
+ * d and V (the workspace must not change in between; the valid flags of that
+ * call apply).
+ */
+gm_status gm_distill_bwd(const uint16_t* W, int64_t N, int64_t d, int64_t V, uint16_t* dHs, void* ws,
+                         size_t ws_bytes, gm_stream_t stream);
+
 #ifdef __cplusplus
 } /* extern "C" */
 #endif

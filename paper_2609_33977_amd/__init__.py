@@ -8,4 +8,5 @@ from ._lib import (  # noqa: F401
     gm_abi_version, gm_gate, gm_gate_bwd, gm_budget_loss, gm_gate_bwd_budget, gm_workspace_size,
     gm_masked_linear_fwd, gm_masked_linear_bwd,
     gm_pack_rows, gm_packed_linear_fwd,
+    gm_distill_workspace_size, gm_distill_fwd, gm_distill_bwd,
 )

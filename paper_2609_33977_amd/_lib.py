@@ -20,6 +20,7 @@ EXPORTS = (
     "gm_abi_version", "gm_status_string", "gm_gate", "gm_gate_bwd", "gm_budget_loss", "gm_gate_bwd_budget",
     "gm_workspace_size",
     "gm_masked_linear_fwd", "gm_masked_linear_bwd", "gm_pack_rows", "gm_packed_linear_fwd",
+    "gm_distill_workspace_size", "gm_distill_fwd", "gm_distill_bwd",
 )
 
 
@@ -51,6 +52,9 @@ def _load() -> ctypes.CDLL:
         "gm_masked_linear_bwd": ([P, P, P, P, I64, I64, I64, I32, I32, P, P, P, SZ, P], ctypes.c_int),
         "gm_pack_rows": ([P, P, I64, I64, I32, I32, I64, P, P, P, P, P], ctypes.c_int),
         "gm_packed_linear_fwd": ([P, P, P, P, P, I64, I64, I64, I32, P, P], ctypes.c_int),
+        "gm_distill_workspace_size": ([I64, I64, I64, ctypes.POINTER(SZ)], ctypes.c_int),
+        "gm_distill_fwd": ([P, P, P, P, I64, I64, I64, P, P, P, SZ, P], ctypes.c_int),
+        "gm_distill_bwd": ([P, I64, I64, I64, P, P, SZ, P], ctypes.c_int),
     }
     for name, (args, res) in sigs.items():
         fn = getattr(lib, name)
@@ -147,3 +151,25 @@ def gm_packed_linear_fwd(X, Wp, chunk, scale, rowptr, d_out: int, g: int, Y, str
     T, d_in = X.shape
     _check(LIB.gm_packed_linear_fwd(_ptr(X), _ptr(Wp), _ptr(chunk), _ptr(scale), _ptr(rowptr), T, d_in, int(d_out),
                                     int(g), _ptr(Y), _stream(stream)), "gm_packed_linear_fwd")
+
+
+def gm_distill_workspace_size(N: int, d: int, V: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(LIB.gm_distill_workspace_size(int(N), int(d), int(V), ctypes.byref(out)), "gm_distill_workspace_size")
+    return out.value
+
+
+def gm_distill_fwd(Ht, Hs, W, valid, loss, ce, ws, stream=None) -> None:
+    """Distillation loss of Eq. 4 (see gm_distill_fwd in the header); valid and ce may be None."""
+    N, d = Ht.shape
+    V = W.shape[0]
+    _check(LIB.gm_distill_fwd(_ptr(Ht), _ptr(Hs), _ptr(W), _ptr(valid), N, d, V, _ptr(loss), _ptr(ce), _ptr(ws),
+                              ws.numel() * ws.element_size(), _stream(stream)), "gm_distill_fwd")
+
+
+def gm_distill_bwd(W, dHs, ws, stream=None) -> None:
+    """Gradient of the distillation loss to the student hidden states, from the forward's workspace."""
+    N, d = dHs.shape
+    V = W.shape[0]
+    _check(LIB.gm_distill_bwd(_ptr(W), N, d, V, _ptr(dHs), _ptr(ws), ws.numel() * ws.element_size(),
+                              _stream(stream)), "gm_distill_bwd")

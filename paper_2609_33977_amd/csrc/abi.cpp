@@ -113,6 +113,49 @@ BwdLayout bwd_layout(int64_t T, int64_t d_in, int64_t d_out, int32_t g) {
   return L;
 }
 
+// Distillation loss: limits keep every 32-bit byte offset of its GEMMs below 2^31.
+constexpr int64_t kMaxHidden = 65536;
+constexpr int64_t kMaxVocab = int64_t(1) << 20;
+
+gm_status check_distill_shape(int64_t N, int64_t d, int64_t V) {
+  if (N < 1 || d < 32 || V < 8) return GM_ERR_SHAPE;
+  if (N > kMaxDim || d > kMaxHidden || V > kMaxVocab) return GM_ERR_SHAPE;
+  if (d % 32 || V % 8) return GM_ERR_SHAPE;
+  const int64_t ldv = (V + 31) / 32 * 32;
+  if (V * d > kMaxElems || N * d > kMaxElems || N * ldv > kMaxElems) return GM_ERR_SHAPE;
+  return GM_OK;
+}
+
+// Workspace of the distillation loss, each part 256-byte aligned:
+//   z_T, z_S [N, V] fp32 | statistics [5, ceil(V/256), N] fp32 |
+//   lse_T, lse_S, cross-entropy, token weight [N] fp32 each | dz_S [N, ldv] bf16
+struct DistillLayout {
+  size_t zt, zs, part, lse_t, lse_s, ce, wtok, dz, total;
+  int ldv, tiles;
+};
+
+DistillLayout distill_layout(int64_t N, int64_t V) {
+  DistillLayout L;
+  L.ldv = int((V + 31) / 32 * 32);
+  L.tiles = gm::distill_vocab_tiles(int(V));
+  const size_t n = size_t(N);
+  size_t off = 0;
+  auto take = [&](size_t& at, size_t bytes) {
+    at = off;
+    off = round_up(off + bytes, 256);
+  };
+  take(L.zt, n * size_t(V) * 4);
+  take(L.zs, n * size_t(V) * 4);
+  take(L.part, 5 * size_t(L.tiles) * n * 4);
+  take(L.lse_t, n * 4);
+  take(L.lse_s, n * 4);
+  take(L.ce, n * 4);
+  take(L.wtok, n * 4);
+  take(L.dz, n * size_t(L.ldv) * 2);
+  L.total = off;
+  return L;
+}
+
 }  // namespace
 
 GM_EXPORT int gm_abi_version(void) { return GM_ABI_VERSION; }
@@ -281,4 +324,41 @@ GM_EXPORT gm_status gm_packed_linear_fwd(const uint16_t* X, const uint16_t* Wp, 
   if (gm_status st = check_device()) return st;
   return from_hip(
       gm::launch_gemv_packed(X, Wp, chunk, scale, rowptr, int(T), int(d_in), int(d_out), g, Y, stream));
+}
+
+GM_EXPORT gm_status gm_distill_workspace_size(int64_t N, int64_t d, int64_t V, size_t* bytes) {
+  if (!bytes) return GM_ERR_NULL;
+  if (gm_status st = check_distill_shape(N, d, V)) return st;
+  *bytes = distill_layout(N, V).total;
+  return GM_OK;
+}
+
+GM_EXPORT gm_status gm_distill_fwd(const uint16_t* Ht, const uint16_t* Hs, const uint16_t* W, const uint8_t* valid,
+                                   int64_t N, int64_t d, int64_t V, float* loss, float* ce, void* ws,
+                                   size_t ws_bytes, gm_stream_t stream) {
+  if (!Ht || !Hs || !W || !loss || !ws) return GM_ERR_NULL;
+  if (gm_status st = check_distill_shape(N, d, V)) return st;
+  if (!aligned16(Ht) || !aligned16(Hs) || !aligned16(W) || !aligned16(ws) || !aligned4(loss) || (ce && !aligned4(ce)))
+    return GM_ERR_ALIGN;
+  const DistillLayout L = distill_layout(N, V);
+  if (ws_bytes < L.total) return GM_ERR_WORKSPACE;
+  if (gm_status st = check_device()) return st;
+  char* b = static_cast<char*>(ws);
+  auto f = [&](size_t off) { return reinterpret_cast<float*>(b + off); };
+  return from_hip(gm::launch_distill_fwd(Ht, Hs, W, valid, int(N), int(d), int(V), f(L.zt), f(L.zs), f(L.part),
+                                         f(L.lse_t), f(L.lse_s), f(L.ce), f(L.wtok), loss, ce, stream));
+}
+
+GM_EXPORT gm_status gm_distill_bwd(const uint16_t* W, int64_t N, int64_t d, int64_t V, uint16_t* dHs, void* ws,
+                                   size_t ws_bytes, gm_stream_t stream) {
+  if (!W || !dHs || !ws) return GM_ERR_NULL;
+  if (gm_status st = check_distill_shape(N, d, V)) return st;
+  if (!aligned16(W) || !aligned16(dHs) || !aligned16(ws)) return GM_ERR_ALIGN;
+  const DistillLayout L = distill_layout(N, V);
+  if (ws_bytes < L.total) return GM_ERR_WORKSPACE;
+  if (gm_status st = check_device()) return st;
+  char* b = static_cast<char*>(ws);
+  auto f = [&](size_t off) { return reinterpret_cast<float*>(b + off); };
+  return from_hip(gm::launch_distill_bwd(W, int(N), int(d), int(V), f(L.zt), f(L.zs), f(L.lse_t), f(L.lse_s),
+                                         f(L.wtok), reinterpret_cast<uint16_t*>(b + L.dz), L.ldv, dHs, stream));
 }

@@ -40,4 +40,13 @@ hipError_t launch_dx(const uint16_t* dYt, int ldt, const uint16_t* W, const int*
                      const float* scales, const int* subbits, const int* colsoft, int T, int d_in, int d_out, int g,
                      uint16_t* dX, hipStream_t s);
 
+// Distillation loss (Sec. 2.4, Eq. 4) through the LM head.
+int distill_vocab_tiles(int V);
+hipError_t launch_distill_fwd(const uint16_t* Ht, const uint16_t* Hs, const uint16_t* W, const uint8_t* valid, int N,
+                              int d, int V, float* zt, float* zs, float* part, float* lse_t, float* lse_s, float* ce,
+                              float* wtok, float* loss, float* ce_out, hipStream_t s);
+hipError_t launch_distill_bwd(const uint16_t* W, int N, int d, int V, const float* zt, const float* zs,
+                              const float* lse_t, const float* lse_s, const float* wtok, uint16_t* dz, int ldv,
+                              uint16_t* dH, hipStream_t s);
+
 }  // namespace gm

@@ -199,3 +199,40 @@ def test_pack_argument_errors():
     assert L.gm_pack_rows(FAKE, FAKE, 256, 16, 32, 16, 1, FAKE, FAKE, FAKE, FAKE, None) == gm.GM_ERR_SHAPE
     assert L.gm_packed_linear_fwd(FAKE, FAKE, FAKE, FAKE, None, 1, 256, 16, 256, FAKE, None) == gm.GM_ERR_NULL
     assert L.gm_packed_linear_fwd(FAKE, FAKE, FAKE, FAKE, FAKE, 1, 200, 16, 256, FAKE, None) == gm.GM_ERR_SHAPE
+
+
+def test_distill_workspace_size():
+    N, d, V = 4096, 4096, 32000
+    r256 = lambda x: (x + 255) // 256 * 256
+    tiles = (V + 255) // 256
+    ldv = (V + 31) // 32 * 32
+    expect = 2 * r256(N * V * 4) + r256(5 * tiles * N * 4) + 4 * r256(N * 4) + r256(N * ldv * 2)
+    assert gm.gm_distill_workspace_size(N, d, V) == expect
+    assert gm.gm_distill_workspace_size(77, 96, 1000) > 77 * 1000 * 8
+
+
+@pytest.mark.parametrize("N,d,V", [(0, 256, 1000), (16, 48, 1000), (16, 16, 1000), (16, 256, 1004), (16, 256, 0),
+                                   (16, 65536 + 32, 64), (16, 64, (1 << 20) + 8), (1 << 20, 2048, 64)])
+def test_distill_rejects_bad_shapes(N, d, V):
+    out = ctypes.c_size_t(0)
+    assert gm.LIB.gm_distill_workspace_size(N, d, V, ctypes.byref(out)) == gm.GM_ERR_SHAPE
+
+
+def test_distill_argument_errors():
+    L = gm.LIB
+    need = gm.gm_distill_workspace_size(16, 256, 1000)
+    fwd = L.gm_distill_fwd
+    assert fwd(None, FAKE, FAKE, None, 16, 256, 1000, FAKE, None, FAKE, need, None) == gm.GM_ERR_NULL
+    assert fwd(FAKE, FAKE, FAKE, None, 16, 256, 1000, None, None, FAKE, need, None) == gm.GM_ERR_NULL
+    assert fwd(FAKE, FAKE, FAKE, None, 16, 256, 1000, FAKE, None, None, need, None) == gm.GM_ERR_NULL
+    assert fwd(FAKE, FAKE, FAKE, None, 16, 250, 1000, FAKE, None, FAKE, need, None) == gm.GM_ERR_SHAPE
+    assert fwd(FAKE, MISALIGNED, FAKE, None, 16, 256, 1000, FAKE, None, FAKE, need, None) == gm.GM_ERR_ALIGN
+    odd = ctypes.c_void_p(FAKE.value + 2)
+    assert fwd(FAKE, FAKE, FAKE, None, 16, 256, 1000, odd, None, FAKE, need, None) == gm.GM_ERR_ALIGN
+    assert fwd(FAKE, FAKE, FAKE, None, 16, 256, 1000, FAKE, None, FAKE, need - 1, None) == gm.GM_ERR_WORKSPACE
+    bwd = L.gm_distill_bwd
+    assert bwd(None, 16, 256, 1000, FAKE, FAKE, need, None) == gm.GM_ERR_NULL
+    assert bwd(FAKE, 16, 256, 1000, None, FAKE, need, None) == gm.GM_ERR_NULL
+    assert bwd(FAKE, 16, 256, 1001, FAKE, FAKE, need, None) == gm.GM_ERR_SHAPE
+    assert bwd(FAKE, 16, 256, 1000, MISALIGNED, FAKE, need, None) == gm.GM_ERR_ALIGN
+    assert bwd(FAKE, 16, 256, 1000, FAKE, FAKE, need - 256, None) == gm.GM_ERR_WORKSPACE

@@ -23,5 +23,7 @@ from .gen import (  # noqa: F401
     kept_counts_beta_law,
     LinearCase,
     make_linear_case,
+    DistillCase,
+    make_distill_case,
 )
 from .configs import CONFIGS, LLAMA2_7B_LINEARS, LLAMA2_13B_LINEARS, config  # noqa: F401

@@ -156,6 +156,31 @@ def make_linear_case(key: Sequence[int], T: int, d_in: int, d_out: int, g: int, 
                       mask.reshape(G_out, G_in), kept, g_out)
 
 
+@dataclasses.dataclass
+class DistillCase:
+    """Host copies of the LM-head inputs of the distillation loss (bf16 as uint16 bits)."""
+    N: int
+    d: int
+    V: int
+    Ht: np.ndarray      # uint16 [N, d]  teacher final hidden states
+    Hs: np.ndarray      # uint16 [N, d]  student final hidden states
+    W: np.ndarray       # uint16 [V, d]  LM head
+    valid: np.ndarray   # uint8 [N]
+
+
+def make_distill_case(key: Sequence[int], N: int, d: int, V: int, student_noise: float = 0.3,
+                      logit_std: float = 3.0, valid_frac: float = 1.0) -> DistillCase:
+    """H_T ~ N(0, 1); H_S = H_T + student_noise N(0, 1) (the pruned pass drifts from the dense one);
+    W ~ N(0, logit_std^2 / d), so logits have standard deviation about logit_std whatever d;
+    each token valid with probability valid_frac (all valid at 1)."""
+    rng = _rng(*key)
+    ht = rng.standard_normal((N, d), dtype=np.float32)
+    hs = ht + np.float32(student_noise) * rng.standard_normal((N, d), dtype=np.float32)
+    w = rng.standard_normal((V, d), dtype=np.float32) * np.float32(logit_std / np.sqrt(d))
+    valid = np.ones(N, dtype=np.uint8) if valid_frac >= 1.0 else (rng.uniform(size=N) < valid_frac).astype(np.uint8)
+    return DistillCase(N, d, V, bf16_bits_from_f32(ht), bf16_bits_from_f32(hs), bf16_bits_from_f32(w), valid)
+
+
 def rng_for(*key: int) -> np.random.Generator:
     """A generator for ad-hoc draws in tests, derived from the shared seed."""
     return _rng(*key)
