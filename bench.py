@@ -13,7 +13,8 @@ are seeded synthetic tensors resident in HBM before timing starts.
 The JSON line also carries the roofline of the dominant kernel (dgate), the
 fp64 oracle timed on the host cores as a reported baseline, the decode GEMV
 bandwidth on LLaMA-2-13B shapes, the sparsity-budget regulariser over the
-LLaMA-2-7B selectors, and the same step with square g x g groups.
+LLaMA-2-7B selectors, the same step with square g x g groups, and the
+distillation loss through the LLaMA-2-7B LM head.
 """
 from __future__ import annotations
 
@@ -68,6 +69,7 @@ def _parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gemv", action="store_true")
     ap.add_argument("--no-square", action="store_true")
+    ap.add_argument("--no-distill", action="store_true")
     ap.add_argument("--gemv-layers", type=int, default=40)
     ap.add_argument("--profile-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this size (counter calibration runs)")
@@ -219,6 +221,42 @@ def _square_groups(d, case, reps):
     return out
 
 
+# ------------------------------------------------------------------ distillation loss
+
+def _distill(reps):
+    """Distillation loss (Eq. 4) through the LLaMA-2-7B LM head over one batch: forward and backward."""
+    import torch
+    import paper_2609_33977_amd as gm
+    import workloads
+    N, d, V = workloads.config("llama2_7b_step")["T"], 4096, 32000
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(workloads.SEED)
+    Ht = torch.randn(N, d, device="cuda", generator=gen)
+    Hs = (Ht + 0.3 * torch.randn(N, d, device="cuda", generator=gen)).to(torch.bfloat16)
+    Ht = Ht.to(torch.bfloat16)
+    W = (torch.randn(V, d, device="cuda", generator=gen) * (3.0 / d ** 0.5)).to(torch.bfloat16)
+    ws = torch.empty(gm.gm_distill_workspace_size(N, d, V), dtype=torch.uint8, device="cuda")
+    loss = torch.empty(1, device="cuda")
+    dH = torch.empty(N, d, dtype=torch.bfloat16, device="cuda")
+
+    def fwd():
+        gm.gm_distill_fwd(Ht, Hs, W, None, loss, None, ws)
+
+    def bwd():
+        gm.gm_distill_bwd(W, dH, ws)
+
+    fwd(); bwd()
+    torch.cuda.synchronize()
+    t_f = _events_ms(fwd, reps)
+    t_b = _events_ms(bwd, reps)
+    fl_f, fl_b = 4.0 * N * V * d, 2.0 * N * V * d
+    return {"workload": f"LLaMA-2-7B LM head, V {V}, d {d}, {N} tokens of each pass (teacher, student)",
+            "fwd_ms": t_f, "fwd_TFLOP/s": fl_f / (t_f / 1e3) / 1e12,
+            "bwd_ms": t_b, "bwd_TFLOP/s": fl_b / (t_b / 1e3) / 1e12,
+            "TFLOP/s": (fl_f + fl_b) / ((t_f + t_b) / 1e3) / 1e12,
+            "logit_bytes_written": 8.0 * N * V, "loss": float(loss.item())}
+
+
 # ------------------------------------------------------------------ decode GEMV
 
 def _gemv_bandwidth(n_layers, reps):
@@ -358,6 +396,10 @@ def main():
     if not args.no_square:
         square = _square_groups(d, case, max(5, args.steps // 2))
 
+    distill = None
+    if not args.no_distill:
+        distill = _distill(max(3, args.steps // 4))
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = _cpu_baseline(case, flops_step, args.cpu_seconds)
@@ -390,6 +432,7 @@ def main():
         "gemv": gemv,
         "budget": budget,
         "square_groups": square,
+        "distill": distill,
     }
     print(json.dumps(out), flush=True)
 

@@ -127,7 +127,7 @@ gm_status check_distill_shape(int64_t N, int64_t d, int64_t V) {
 }
 
 // Workspace of the distillation loss, each part 256-byte aligned:
-//   z_T, z_S [N, V] fp32 | statistics [5, ceil(V/256), N] fp32 |
+//   z_T, z_S [N, V] fp32 | statistics [N, ceil(V/256), 5] fp32 |
 //   lse_T, lse_S, cross-entropy, token weight [N] fp32 each | dz_S [N, ldv] bf16
 struct DistillLayout {
   size_t zt, zs, part, lse_t, lse_s, ce, wtok, dz, total;

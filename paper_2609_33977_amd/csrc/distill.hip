@@ -53,7 +53,7 @@ __device__ __forceinline__ void lse_merge_c(float& m, float& s, float& c, float 
 // 0..127 are tokens t0..t0+127 of the teacher, 128..255 the same tokens of the
 // student.  Waves 2 (M) x 4 (N): waves with wn < 2 hold teacher logits, the
 // others the student logits of the same tokens and rows.  part holds the
-// statistics as [kLmStats][tiles of V][N].
+// statistics as [N][tiles of V][kLmStats].
 __global__ __launch_bounds__(64 * kLmWaves) void lmhead_fwd_kernel(const uint16_t* __restrict__ Ht,
                                                                   const uint16_t* __restrict__ Hs,
                                                                   const uint16_t* __restrict__ W, int N, int d,
@@ -191,44 +191,63 @@ __global__ __launch_bounds__(64 * kLmWaves) void lmhead_fwd_kernel(const uint16_
     float mt = a[0], st = a[1], ms = a[2], ss = a[3], c = a[4];
     lse_merge_c(mt, st, c, b[0], b[1], b[4]);
     lse_merge(ms, ss, b[2], b[3]);
-    const int64_t stride = int64_t(tiles_m) * N;
-    float* p = part + int64_t(tm) * N + t0 + tid;
+    float* p = part + (int64_t(t0 + tid) * tiles_m + tm) * kLmStats;
     p[0] = mt;
-    p[stride] = st;
-    p[2 * stride] = ms;
-    p[3 * stride] = ss;
-    p[4 * stride] = c;
+    p[1] = st;
+    p[2] = ms;
+    p[3] = ss;
+    p[4] = c;
   }
 }
 
 // ---------------------------------------------------------------- per token
 
-// One thread per token: merges the vocabulary tiles in increasing order.
+// One wave per token: lane l merges vocabulary tiles l, l + 64, ... in fp64,
+// then the lanes combine in a fixed butterfly order.
+__device__ __forceinline__ void merge_d(double& m, double& s, double m2, double s2) {
+  const double mx = fmax(m, m2);
+  if (mx == -INFINITY) return;
+  s = s * exp(m - mx) + s2 * exp(m2 - mx);
+  m = mx;
+}
+
+__device__ __forceinline__ void merge_dc(double& m, double& s, double& c, double m2, double s2, double c2) {
+  const double mx = fmax(m, m2);
+  if (mx == -INFINITY) return;
+  const double a = exp(m - mx), b = exp(m2 - mx);
+  s = s * a + s2 * b;
+  c = c * a + c2 * b;
+  m = mx;
+}
+
 __global__ __launch_bounds__(256) void distill_token_kernel(const float* __restrict__ part, int ntiles, int N,
                                                            float* __restrict__ lse_t, float* __restrict__ lse_s,
                                                            float* __restrict__ ce, float* __restrict__ ce_out) {
-  const int t = blockIdx.x * 256 + threadIdx.x;
-  if (t >= N) return;
-  const int64_t stride = int64_t(ntiles) * N;
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= N) return;  // whole wave
+  const float* p = part + int64_t(t) * ntiles * kLmStats;
   double mt = -INFINITY, st = 0.0, c = 0.0, ms = -INFINITY, ss = 0.0;
-  for (int i = 0; i < ntiles; ++i) {
-    const float* p = part + int64_t(i) * N + t;
-    const double m2 = p[0], s2 = p[stride], ms2 = p[2 * stride], ss2 = p[3 * stride], c2 = p[4 * stride];
-    const double mx = fmax(mt, m2);
-    const double a = exp(mt - mx), b = exp(m2 - mx);
-    st = st * a + s2 * b;
-    c = c * a + c2 * b;
-    mt = mx;
-    const double my = fmax(ms, ms2);
-    ss = ss * exp(ms - my) + ss2 * exp(ms2 - my);
-    ms = my;
+  for (int i = lane; i < ntiles; i += 64) {
+    const float* q = p + i * kLmStats;
+    merge_dc(mt, st, c, q[0], q[1], q[4]);
+    merge_d(ms, ss, q[2], q[3]);
   }
-  const double ls = ms + log(ss);
-  const double x = ls - c / st;
-  lse_t[t] = float(mt + log(st));
-  lse_s[t] = float(ls);
-  ce[t] = float(x);
-  if (ce_out) ce_out[t] = float(x);
+#pragma unroll
+  for (int x = 1; x < 64; x <<= 1) {
+    const double mt2 = __shfl_xor(mt, x), st2 = __shfl_xor(st, x), c2 = __shfl_xor(c, x);
+    const double ms2 = __shfl_xor(ms, x), ss2 = __shfl_xor(ss, x);
+    merge_dc(mt, st, c, mt2, st2, c2);
+    merge_d(ms, ss, ms2, ss2);
+  }
+  if (lane == 0) {
+    const double ls = ms + log(ss);
+    const double x = ls - c / st;
+    lse_t[t] = float(mt + log(st));
+    lse_s[t] = float(ls);
+    ce[t] = float(x);
+    if (ce_out) ce_out[t] = float(x);
+  }
 }
 
 // One block: the number of valid tokens, the mean cross-entropy over them
@@ -371,7 +390,7 @@ hipError_t launch_distill_fwd(const uint16_t* Ht, const uint16_t* Hs, const uint
                      V, zt, zs, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(distill_token_kernel, dim3(unsigned((N + 255) / 256)), dim3(256), 0, s, part, tiles_m, N, lse_t,
+  hipLaunchKernelGGL(distill_token_kernel, dim3(unsigned((N + 3) / 4)), dim3(256), 0, s, part, tiles_m, N, lse_t,
                      lse_s, ce, ce_out);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
