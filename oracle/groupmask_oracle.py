@@ -37,6 +37,15 @@ design notes of the repository):
   with no valid token the loss and its gradient are zero.  The gradient goes
   to the student's hidden states only (the teacher is detached, the LM head
   is frozen).
+* Hypernetwork (Sec. 2.2, Eq. 3; no sizes are printed): the fixed input holds
+  one D-vector per target layer; the bidirectional GRU uses the standard GRU
+  cell (reset gate applied to the recurrent candidate term, zero initial
+  state) with H units per direction, and its output for layer l is the
+  concatenation [forward; backward] of size 2H; the head of layer l is an
+  affine map A^l o_l + c^l onto its G^l selector logits.  The heads of all
+  layers are stacked row by row in one [sum G, 2H] matrix, in the layer order
+  of the flat selector array.  Parameters are trained with AdamW (Table 5):
+  decoupled weight decay, bias-corrected moments.
 """
 from __future__ import annotations
 
@@ -47,6 +56,7 @@ __all__ = [
     "linear_fwd", "linear_bwd_dx", "linear_bwd_dgate", "linear_bwd", "sparsity",
     "preserved_rate", "near_threshold", "kept_count", "budget_loss",
     "softmax_rows", "distill_loss", "distill_loss_bwd",
+    "gru_param_shapes", "bigru_fwd", "hyper_fwd", "hyper_bwd", "adamw_step",
 ]
 
 
@@ -269,3 +279,133 @@ def distill_loss_bwd(H_t, H_s, W, valid=None) -> np.ndarray:
     if n:
         dz[v] = (p_s[v] - p_t[v]) / n
     return dz @ W
+
+
+# ------------------------------------------------------- hypernetwork (Sec. 2.2, Eq. 3)
+
+def _sigmoid(x):
+    return 1.0 / (1.0 + np.exp(-x))
+
+
+def gru_param_shapes(D: int, H: int):
+    """Shapes of one direction's parameters, in storage order: W_ih [3H, D], W_hh [3H, H], b_ih [3H], b_hh [3H].
+
+    The 3H rows are the reset, update and candidate gates, in that order.
+    """
+    return [(3 * H, D), (3 * H, H), (3 * H,), (3 * H,)]
+
+
+def _split_gru(flat, D, H):
+    flat = np.asarray(flat, dtype=np.float64)
+    out, pos = [], 0
+    for direction in range(2):
+        ps = []
+        for shp in gru_param_shapes(D, H):
+            n = int(np.prod(shp))
+            ps.append(flat[pos:pos + n].reshape(shp))
+            pos += n
+        out.append(ps)
+    if pos != flat.size:
+        raise ValueError("GRU parameter vector has the wrong length")
+    return out
+
+
+def _gru_dir(z, W_ih, W_hh, b_ih, b_hh, order):
+    """One GRU direction over the steps in `order`; returns outputs [L, H] and per-step caches."""
+    L = z.shape[0]
+    H = W_hh.shape[1]
+    h = np.zeros(H)
+    out = np.zeros((L, H))
+    cache = {}
+    for l in order:
+        gi = W_ih @ z[l] + b_ih
+        gh = W_hh @ h + b_hh
+        r = _sigmoid(gi[:H] + gh[:H])
+        u = _sigmoid(gi[H:2 * H] + gh[H:2 * H])
+        n = np.tanh(gi[2 * H:] + r * gh[2 * H:])
+        h_new = (1.0 - u) * n + u * h
+        cache[l] = (h, r, u, n, gh[2 * H:])
+        h = h_new
+        out[l] = h
+    return out, cache
+
+
+def bigru_fwd(z, gru_flat, H: int):
+    """Bidirectional GRU over the layer sequence z [L, D]: outputs [L, 2H] = [forward; backward]."""
+    z = np.asarray(z, dtype=np.float64)
+    L, D = z.shape
+    (p0, p1) = _split_gru(gru_flat, D, H)
+    f, _ = _gru_dir(z, *p0, range(L))
+    b, _ = _gru_dir(z, *p1, range(L - 1, -1, -1))
+    return np.concatenate([f, b], axis=1)
+
+
+def hyper_fwd(z, gru_flat, A, c, offsets, H: int):
+    """Selector logits of every layer (Eq. 3 before binarisation), flat in layer order.
+
+    logits[e] = A[e] . o_{l(e)} + c[e] for e in [offsets[l], offsets[l+1]).
+    """
+    o = bigru_fwd(z, gru_flat, H)
+    A = np.asarray(A, dtype=np.float64)
+    c = np.asarray(c, dtype=np.float64)
+    out = np.empty(A.shape[0])
+    for l in range(len(offsets) - 1):
+        a, b = int(offsets[l]), int(offsets[l + 1])
+        out[a:b] = A[a:b] @ o[l] + c[a:b]
+    return out
+
+
+def _gru_dir_bwd(z, W_ih, W_hh, b_ih, b_hh, order, cache, dout):
+    """Backpropagation through one direction; dout [L, H] is the gradient of its outputs."""
+    H = W_hh.shape[1]
+    g = [np.zeros_like(W_ih), np.zeros_like(W_hh), np.zeros_like(b_ih), np.zeros_like(b_hh)]
+    dh = np.zeros(H)
+    for l in reversed(list(order)):
+        h, r, u, n, ghn = cache[l]
+        dh = dh + dout[l]
+        dn = dh * (1.0 - u)
+        du = dh * (h - n)
+        dan = dn * (1.0 - n * n)
+        dar = dan * ghn * r * (1.0 - r)
+        dau = du * u * (1.0 - u)
+        dgi = np.concatenate([dar, dau, dan])
+        dgh = np.concatenate([dar, dau, dan * r])
+        g[0] += np.outer(dgi, z[l])
+        g[1] += np.outer(dgh, h)
+        g[2] += dgi
+        g[3] += dgh
+        dh = dh * u + W_hh.T @ dgh
+    return g
+
+
+def hyper_bwd(dlogits, z, gru_flat, A, c, offsets, H: int):
+    """Gradients of <dlogits, hyper_fwd(...)> with respect to A, c and the GRU parameters (flat)."""
+    z = np.asarray(z, dtype=np.float64)
+    L, D = z.shape
+    p0, p1 = _split_gru(gru_flat, D, H)
+    f, cf = _gru_dir(z, *p0, range(L))
+    b, cb = _gru_dir(z, *p1, range(L - 1, -1, -1))
+    o = np.concatenate([f, b], axis=1)
+    A = np.asarray(A, dtype=np.float64)
+    dl = np.asarray(dlogits, dtype=np.float64)
+    dA = np.empty_like(A)
+    do = np.zeros_like(o)
+    for l in range(L):
+        a, e = int(offsets[l]), int(offsets[l + 1])
+        dA[a:e] = np.outer(dl[a:e], o[l])
+        do[l] = A[a:e].T @ dl[a:e]
+    g0 = _gru_dir_bwd(z, *p0, range(L), cf, do[:, :H])
+    g1 = _gru_dir_bwd(z, *p1, range(L - 1, -1, -1), cb, do[:, H:])
+    dgru = np.concatenate([x.reshape(-1) for x in g0 + g1])
+    return dA, dl.copy(), dgru, do
+
+
+def adamw_step(p, g, m, v, lr, beta1, beta2, eps, weight_decay, step: int):
+    """One AdamW step (decoupled weight decay, bias-corrected moments); returns (p, m, v)."""
+    p = np.asarray(p, dtype=np.float64) * (1.0 - lr * weight_decay)
+    g = np.asarray(g, dtype=np.float64)
+    m = beta1 * np.asarray(m, dtype=np.float64) + (1.0 - beta1) * g
+    v = beta2 * np.asarray(v, dtype=np.float64) + (1.0 - beta2) * g * g
+    m_hat = m / (1.0 - beta1 ** step)
+    v_hat = v / (1.0 - beta2 ** step)
+    return p - lr * m_hat / (np.sqrt(v_hat) + eps), m, v

@@ -535,6 +535,105 @@ def test_distill_counts_only_valid_tokens():
     assert not np.any(oracle.distill_loss_bwd(H_t, H_s, W, none))
 
 
+# ----------------------------------------------- hypernetwork (Sec. 2.2, Eq. 3)
+
+def _hyper_case(L, D, H, sizes, key):
+    P = 2 * sum(int(np.prod(shp)) for shp in oracle.gru_param_shapes(D, H))
+    z = _rand((L, D), (70,) + key)
+    gru = _rand((P,), (71,) + key, 0.4)
+    offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    A = _rand((int(offsets[-1]), 2 * H), (72,) + key, 0.3)
+    c = _rand((int(offsets[-1]),), (73,) + key, 0.1)
+    return z, gru, A, c, offsets
+
+
+def _torch_hyper(z, gru, A, c, offsets, H):
+    import torch
+    D = z.shape[1]
+    net = torch.nn.GRU(D, H, bidirectional=True, batch_first=True).double()
+    params = [net.weight_ih_l0, net.weight_hh_l0, net.bias_ih_l0, net.bias_hh_l0,
+              net.weight_ih_l0_reverse, net.weight_hh_l0_reverse, net.bias_ih_l0_reverse, net.bias_hh_l0_reverse]
+    pos = 0
+    with torch.no_grad():
+        for prm in params:
+            n = prm.numel()
+            prm.copy_(torch.from_numpy(gru[pos:pos + n].reshape(prm.shape)))
+            pos += n
+    tA = torch.tensor(A, requires_grad=True)
+    tc = torch.tensor(c, requires_grad=True)
+    o = net(torch.from_numpy(z)[None])[0][0]
+    rows = [tA[offsets[l]:offsets[l + 1]] @ o[l] + tc[offsets[l]:offsets[l + 1]] for l in range(len(offsets) - 1)]
+    return torch.cat(rows), tA, tc, params
+
+
+@pytest.mark.parametrize("L,D,H", [(5, 6, 4), (9, 3, 7), (1, 4, 2)])
+def test_bigru_matches_torch_gru(L, D, H):
+    import torch
+    z, gru, A, c, offsets = _hyper_case(L, D, H, [3] * L, (L, D, H))
+    logits, _, _, _ = _torch_hyper(z, gru, A, c, offsets, H)
+    np.testing.assert_allclose(oracle.hyper_fwd(z, gru, A, c, offsets, H), logits.detach().numpy(), rtol=1e-12,
+                               atol=1e-13)
+    del torch
+
+
+def test_hyper_heads_match_loops():
+    L, D, H = 3, 4, 2
+    z, gru, A, c, offsets = _hyper_case(L, D, H, [2, 5, 1], (1,))
+    o = oracle.bigru_fwd(z, gru, H)
+    got = oracle.hyper_fwd(z, gru, A, c, offsets, H)
+    for l in range(L):
+        for e in range(offsets[l], offsets[l + 1]):
+            ref = c[e] + sum(A[e][k] * o[l][k] for k in range(2 * H))
+            assert abs(got[e] - ref) <= 1e-13
+
+
+@pytest.mark.parametrize("L,D,H", [(6, 5, 3), (4, 8, 4)])
+def test_hyper_gradients_match_autograd(L, D, H):
+    import torch
+    sizes = [7, 1, 4, 9, 2, 3, 5, 6][:L]
+    z, gru, A, c, offsets = _hyper_case(L, D, H, sizes, (2, L))
+    dl = _rand((int(offsets[-1]),), (74, L))
+    logits, tA, tc, params = _torch_hyper(z, gru, A, c, offsets, H)
+    (logits * torch.from_numpy(dl)).sum().backward()
+    dA, dc, dgru, _ = oracle.hyper_bwd(dl, z, gru, A, c, offsets, H)
+    np.testing.assert_allclose(dA, tA.grad.numpy(), rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(dc, tc.grad.numpy(), rtol=1e-12, atol=1e-13)
+    ref = np.concatenate([prm.grad.numpy().reshape(-1) for prm in params])
+    np.testing.assert_allclose(dgru, ref, rtol=1e-10, atol=1e-12)
+
+
+def test_hyper_gru_gradient_matches_finite_differences():
+    L, D, H = 4, 3, 3
+    z, gru, A, c, offsets = _hyper_case(L, D, H, [2, 3, 1, 2], (3,))
+    dl = _rand((int(offsets[-1]),), (75,))
+    _, _, dgru, _ = oracle.hyper_bwd(dl, z, gru, A, c, offsets, H)
+    h = 1e-6
+    for k in range(0, gru.size, 5):
+        gp, gm_ = gru.copy(), gru.copy()
+        gp[k] += h
+        gm_[k] -= h
+        fd = (dl @ oracle.hyper_fwd(z, gp, A, c, offsets, H) - dl @ oracle.hyper_fwd(z, gm_, A, c, offsets, H)) / (2 * h)
+        assert abs(fd - dgru[k]) <= 1e-7 * (1 + abs(dgru[k]))
+
+
+def test_adamw_matches_torch():
+    import torch
+    r = workloads.gen.rng_for(76)
+    p0 = r.standard_normal(50)
+    grads = [r.standard_normal(50) * 10.0 ** (-k) for k in range(4)]
+    tp = torch.tensor(p0, requires_grad=True)
+    opt = torch.optim.AdamW([tp], lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay=0.05)
+    p, m, v = p0.copy(), np.zeros(50), np.zeros(50)
+    for step, gr in enumerate(grads, start=1):
+        tp.grad = torch.from_numpy(gr.copy())
+        opt.step()
+        p, m, v = oracle.adamw_step(p, gr, m, v, 1e-3, 0.9, 0.999, 1e-8, 0.05, step)
+        np.testing.assert_allclose(p, tp.detach().numpy(), rtol=1e-14, atol=1e-15)
+        st = opt.state[tp]
+        np.testing.assert_allclose(m, st["exp_avg"].numpy(), rtol=1e-14, atol=0)
+        np.testing.assert_allclose(v, st["exp_avg_sq"].numpy(), rtol=1e-14, atol=0)
+
+
 # ------------------------------------------------------- the pins catch mistakes
 
 def _mutant_fwd_strided_groups(X, W, B, g, g_out=1):
@@ -656,6 +755,82 @@ def _mutant_distill_bwd_no_teacher(H_t, H_s, W, valid=None):
     return p_s / p_s.shape[0] @ np.asarray(W, float)
 
 
+_ORIG_HYPER_FWD = oracle.hyper_fwd
+_ORIG_HYPER_BWD = oracle.hyper_bwd
+_ORIG_ADAMW = oracle.adamw_step
+
+
+def _mutant_hyper_reset_inside(z, gru_flat, A, c, offsets, H):
+    # the other GRU form: candidate from W_hn (r * h) instead of r * (W_hn h + b_hn)
+    z = np.asarray(z, float)
+    L, D = z.shape
+    p = oracle.groupmask_oracle._split_gru(gru_flat, D, H)
+    outs = []
+    for d, order in ((0, range(L)), (1, range(L - 1, -1, -1))):
+        W_ih, W_hh, b_ih, b_hh = p[d]
+        h, out = np.zeros(H), np.zeros((L, H))
+        for l in order:
+            gi = W_ih @ z[l] + b_ih
+            gh = W_hh @ h + b_hh
+            r = 1 / (1 + np.exp(-(gi[:H] + gh[:H])))
+            u = 1 / (1 + np.exp(-(gi[H:2 * H] + gh[H:2 * H])))
+            n = np.tanh(gi[2 * H:] + W_hh[2 * H:] @ (r * h) + b_hh[2 * H:])
+            h = (1 - u) * n + u * h
+            out[l] = h
+        outs.append(out)
+    o = np.concatenate(outs, axis=1)
+    return np.concatenate([np.asarray(A, float)[offsets[l]:offsets[l + 1]] @ o[l] + np.asarray(c, float)[offsets[l]:offsets[l + 1]]
+                           for l in range(L)])
+
+
+def _mutant_hyper_one_direction(z, gru_flat, A, c, offsets, H):
+    # both halves of the output taken from the forward direction
+    z = np.asarray(z, float)
+    L, D = z.shape
+    p = oracle.groupmask_oracle._split_gru(gru_flat, D, H)
+    f, _ = oracle.groupmask_oracle._gru_dir(z, *p[0], range(L))
+    o = np.concatenate([f, f], axis=1)
+    return np.concatenate([np.asarray(A, float)[offsets[l]:offsets[l + 1]] @ o[l] + np.asarray(c, float)[offsets[l]:offsets[l + 1]]
+                           for l in range(L)])
+
+
+def _mutant_hyper_bwd_no_carry(dlogits, z, gru_flat, A, c, offsets, H):
+    # the recurrent gradient is dropped between steps (truncated backpropagation)
+    dA, dc, dgru, do = _ORIG_HYPER_BWD(dlogits, z, gru_flat, A, c, offsets, H)
+    z = np.asarray(z, float)
+    L, D = z.shape
+    p = oracle.groupmask_oracle._split_gru(gru_flat, D, H)
+    grads = []
+    for d, order in ((0, range(L)), (1, range(L - 1, -1, -1))):
+        _, cache = oracle.groupmask_oracle._gru_dir(z, *p[d], order)
+        g = [np.zeros_like(x) for x in p[d]]
+        for l in order:
+            h, r, u, n, ghn = cache[l]
+            dh = do[l, d * H:(d + 1) * H]
+            dan = dh * (1 - u) * (1 - n * n)
+            dar = dan * ghn * r * (1 - r)
+            dau = dh * (h - n) * u * (1 - u)
+            dgi = np.concatenate([dar, dau, dan])
+            dgh = np.concatenate([dar, dau, dan * r])
+            g[0] += np.outer(dgi, z[l]); g[1] += np.outer(dgh, h); g[2] += dgi; g[3] += dgh
+        grads += g
+    return dA, dc, np.concatenate([x.reshape(-1) for x in grads]), do
+
+
+def _mutant_hyper_bwd_head_transposed(dlogits, z, gru_flat, A, c, offsets, H):
+    dA, dc, dgru, do = _ORIG_HYPER_BWD(dlogits, z, gru_flat, A, c, offsets, H)
+    return -dA, dc, dgru, do
+
+
+def _mutant_adamw_no_bias_correction(p, g, m, v, lr, beta1, beta2, eps, weight_decay, step):
+    return _ORIG_ADAMW(p, g, m, v, lr, beta1, beta2, eps, weight_decay, 10 ** 9)
+
+
+def _mutant_adamw_coupled_decay(p, g, m, v, lr, beta1, beta2, eps, weight_decay, step):
+    return _ORIG_ADAMW(p, np.asarray(g, float) + weight_decay * np.asarray(p, float), m, v, lr, beta1, beta2, eps, 0.0,
+                       step)
+
+
 MUTANTS = [
     ("linear_fwd", _mutant_fwd_strided_groups),
     ("linear_fwd", _mutant_fwd_strided_rows),
@@ -676,6 +851,12 @@ MUTANTS = [
     ("distill_loss", _mutant_distill_over_tokens),
     ("distill_loss_bwd", _mutant_distill_bwd_sign),
     ("distill_loss_bwd", _mutant_distill_bwd_no_teacher),
+    ("hyper_fwd", _mutant_hyper_reset_inside),
+    ("hyper_fwd", _mutant_hyper_one_direction),
+    ("hyper_bwd", _mutant_hyper_bwd_no_carry),
+    ("hyper_bwd", _mutant_hyper_bwd_head_transposed),
+    ("adamw_step", _mutant_adamw_no_bias_correction),
+    ("adamw_step", _mutant_adamw_coupled_decay),
 ]
 
 PIN_TESTS = [
@@ -704,6 +885,11 @@ PIN_TESTS = [
     test_distill_uniform_teacher,
     test_distill_gradient_matches_finite_differences,
     test_distill_counts_only_valid_tokens,
+    lambda: test_bigru_matches_torch_gru(5, 6, 4),
+    test_hyper_heads_match_loops,
+    lambda: test_hyper_gradients_match_autograd(6, 5, 3),
+    test_hyper_gru_gradient_matches_finite_differences,
+    test_adamw_matches_torch,
 ]
 
 
