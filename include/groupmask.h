@@ -271,6 +271,66 @@ gm_status gm_distill_fwd(const uint16_t* Ht, const uint16_t* Hs, const uint16_t*
 gm_status gm_distill_bwd(const uint16_t* W, int64_t N, int64_t d, int64_t V, uint16_t* dHs, void* ws,
                          size_t ws_bytes, gm_stream_t stream);
 
+/*
+ * Hypernetwork that generates the selector logits (Sec. 2.2, Eq. 3), trained
+ * with AdamW (Table 5).  The paper prints no sizes; this library builds:
+ *   z [L, D] fp32: the fixed random input, one D-vector per target layer;
+ *   a bidirectional GRU with H in {32, 64, 128} units per direction (standard
+ *   GRU cell: reset, update and candidate gates, the reset gate scaling the
+ *   recurrent candidate term W_hn h + b_hn, zero initial state); its output
+ *   for layer l is o_l = [forward; backward] (2H values);
+ *   layer-specific affine heads: logits[e] = A[e, :] . o_l + c[e] for the
+ *   selectors e in [offsets[l], offsets[l+1]) of layer l, with the heads of
+ *   all layers stacked in A [G_total, 2H] fp32 and c [G_total] fp32, in the
+ *   order of the flat selector array of the gate and the budget regulariser.
+ *   gru [2 P] fp32, P = 3H (D + H + 2): per direction (forward, then
+ *   backward) W_ih [3H, D], W_hh [3H, H], b_ih [3H], b_hh [3H], row-major,
+ *   gate rows in the order reset, update, candidate.
+ *   offsets [L + 1] int64 (device): nondecreasing, offsets[0] = 0,
+ *   offsets[L] = G_total (not checked).
+ * Limits: 1 <= L <= 65536, 1 <= D <= 4096, G_total >= 1.  A and its AdamW
+ * moments need 16-byte alignment, the other arrays 4 (offsets 8).
+ *
+ * gm_hyper_workspace_size -- host-only query of the workspace both calls need.
+ */
+gm_status gm_hyper_workspace_size(int64_t L, int64_t D, int64_t H, int64_t G_total, size_t* bytes);
+
+/*
+ * gm_hyper_fwd -- logits [G_total] fp32 (written in full).  The workspace
+ * keeps the GRU states and the row chunking of the heads for gm_hyper_bwd.
+ */
+gm_status gm_hyper_fwd(const float* z, const float* gru, const float* A, const float* c,
+                       const int64_t* offsets, int64_t L, int64_t D, int64_t H, int64_t G_total,
+                       float* logits, void* ws, size_t ws_bytes, gm_stream_t stream);
+
+/*
+ * gm_hyper_bwd -- backward of gm_hyper_fwd for the gradient dlogits
+ * [G_total] fp32 (the logit gradient of the gate backward), and one AdamW
+ * step on the heads, in place: with g the gradient of an element,
+ *   p <- p (1 - lr weight_decay);  m <- beta1 m + (1 - beta1) g;  v <- beta2 v + (1 - beta2) g^2;
+ *   p <- p - lr (m / (1 - beta1^step)) / (sqrt(v / (1 - beta2^step)) + eps)
+ * for A (moments mA, vA [G_total, 2H]) and c (mc, vc [G_total]); the GRU
+ * gradient goes to dgru [2 P] (apply gm_adamw to gru with it).  The GRU
+ * gradient uses the heads before this update.  Reads the workspace that the
+ * last gm_hyper_fwd on the same stream filled for the same z, gru, A, c and
+ * shapes.  lr >= 0, beta in [0, 1), eps > 0, weight_decay >= 0, step >= 1
+ * (else GM_ERR_VALUE).  The hyperparameters are taken in fp64; the update
+ * coefficients (1 - beta, the bias corrections, 1 - lr weight_decay) are
+ * formed in fp64 and rounded once to fp32.
+ */
+gm_status gm_hyper_bwd(const float* dlogits, const float* z, const float* gru, float* A, float* c,
+                       float* mA, float* vA, float* mc, float* vc, int64_t L, int64_t D, int64_t H,
+                       int64_t G_total, double lr, double beta1, double beta2, double eps,
+                       double weight_decay, int32_t step, float* dgru, void* ws, size_t ws_bytes,
+                       gm_stream_t stream);
+
+/*
+ * gm_adamw -- one AdamW step (as above) on n fp32 parameters p with gradient
+ * g and moments m, v, in place.  n = 0 is a no-op.
+ */
+gm_status gm_adamw(float* p, const float* g, float* m, float* v, int64_t n, double lr, double beta1,
+                   double beta2, double eps, double weight_decay, int32_t step, gm_stream_t stream);
+
 #ifdef __cplusplus
 } /* extern "C" */
 #endif

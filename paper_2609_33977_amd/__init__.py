@@ -9,4 +9,5 @@ from ._lib import (  # noqa: F401
     gm_masked_linear_fwd, gm_masked_linear_bwd,
     gm_pack_rows, gm_packed_linear_fwd,
     gm_distill_workspace_size, gm_distill_fwd, gm_distill_bwd,
+    gm_hyper_workspace_size, gm_hyper_fwd, gm_hyper_bwd, gm_adamw,
 )

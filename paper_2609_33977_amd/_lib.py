@@ -21,6 +21,7 @@ EXPORTS = (
     "gm_workspace_size",
     "gm_masked_linear_fwd", "gm_masked_linear_bwd", "gm_pack_rows", "gm_packed_linear_fwd",
     "gm_distill_workspace_size", "gm_distill_fwd", "gm_distill_bwd",
+    "gm_hyper_workspace_size", "gm_hyper_fwd", "gm_hyper_bwd", "gm_adamw",
 )
 
 
@@ -40,6 +41,7 @@ def _load() -> ctypes.CDLL:
     import torch  # noqa: F401
     lib = ctypes.CDLL(LIB_PATH)
     P, I64, I32, F32, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float, ctypes.c_size_t
+    F64 = ctypes.c_double
     sigs = {
         "gm_abi_version": ([], ctypes.c_int),
         "gm_status_string": ([ctypes.c_int], ctypes.c_char_p),
@@ -55,6 +57,11 @@ def _load() -> ctypes.CDLL:
         "gm_distill_workspace_size": ([I64, I64, I64, ctypes.POINTER(SZ)], ctypes.c_int),
         "gm_distill_fwd": ([P, P, P, P, I64, I64, I64, P, P, P, SZ, P], ctypes.c_int),
         "gm_distill_bwd": ([P, I64, I64, I64, P, P, SZ, P], ctypes.c_int),
+        "gm_hyper_workspace_size": ([I64, I64, I64, I64, ctypes.POINTER(SZ)], ctypes.c_int),
+        "gm_hyper_fwd": ([P, P, P, P, P, I64, I64, I64, I64, P, P, SZ, P], ctypes.c_int),
+        "gm_hyper_bwd": ([P, P, P, P, P, P, P, P, P, I64, I64, I64, I64, F64, F64, F64, F64, F64, I32, P, P, SZ, P],
+                         ctypes.c_int),
+        "gm_adamw": ([P, P, P, P, I64, F64, F64, F64, F64, F64, I32, P], ctypes.c_int),
     }
     for name, (args, res) in sigs.items():
         fn = getattr(lib, name)
@@ -173,3 +180,33 @@ def gm_distill_bwd(W, dHs, ws, stream=None) -> None:
     V = W.shape[0]
     _check(LIB.gm_distill_bwd(_ptr(W), N, d, V, _ptr(dHs), _ptr(ws), ws.numel() * ws.element_size(),
                               _stream(stream)), "gm_distill_bwd")
+
+
+def gm_hyper_workspace_size(L: int, D: int, H: int, G_total: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(LIB.gm_hyper_workspace_size(int(L), int(D), int(H), int(G_total), ctypes.byref(out)),
+           "gm_hyper_workspace_size")
+    return out.value
+
+
+def gm_hyper_fwd(z, gru, A, c, offsets, H: int, logits, ws, stream=None) -> None:
+    """Selector logits from the hypernetwork (see gm_hyper_fwd in the header)."""
+    L, D = z.shape
+    _check(LIB.gm_hyper_fwd(_ptr(z), _ptr(gru), _ptr(A), _ptr(c), _ptr(offsets), L, D, int(H), A.shape[0],
+                            _ptr(logits), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)), "gm_hyper_fwd")
+
+
+def gm_hyper_bwd(dlogits, z, gru, A, c, mA, vA, mc, vc, H: int, lr: float, beta1: float, beta2: float, eps: float,
+                 weight_decay: float, step: int, dgru, ws, stream=None) -> None:
+    """Backward of the hypernetwork with one AdamW step on its heads; the GRU gradient goes to dgru."""
+    L, D = z.shape
+    _check(LIB.gm_hyper_bwd(_ptr(dlogits), _ptr(z), _ptr(gru), _ptr(A), _ptr(c), _ptr(mA), _ptr(vA), _ptr(mc),
+                            _ptr(vc), L, D, int(H), A.shape[0], float(lr), float(beta1), float(beta2), float(eps),
+                            float(weight_decay), int(step), _ptr(dgru), _ptr(ws), ws.numel() * ws.element_size(),
+                            _stream(stream)), "gm_hyper_bwd")
+
+
+def gm_adamw(p, g, m, v, lr: float, beta1: float, beta2: float, eps: float, weight_decay: float, step: int,
+             stream=None) -> None:
+    _check(LIB.gm_adamw(_ptr(p), _ptr(g), _ptr(m), _ptr(v), p.numel(), float(lr), float(beta1), float(beta2),
+                        float(eps), float(weight_decay), int(step), _stream(stream)), "gm_adamw")

@@ -16,7 +16,7 @@ OBJ = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libgroupmask.so")
 ARCH = "gfx950"
 
-SOURCES = ["gate.hip", "budget.hip", "index.hip", "gemv.hip", "gemm.hip", "distill.hip", "abi.cpp"]
+SOURCES = ["gate.hip", "budget.hip", "index.hip", "gemv.hip", "gemm.hip", "distill.hip", "hyper.hip", "abi.cpp"]
 
 # Packed fp32 VALU ops are kept out of the generated code; the host pass
 # warns that it does not know the feature, which is harmless.

@@ -156,6 +156,74 @@ DistillLayout distill_layout(int64_t N, int64_t V) {
   return L;
 }
 
+// Hypernetwork sizes.
+constexpr int64_t kMaxLayers = 65536;
+constexpr int64_t kMaxZ = 4096;
+
+gm_status check_hyper_shape(int64_t L, int64_t D, int64_t H, int64_t G_total) {
+  if (L < 1 || L > kMaxLayers || D < 1 || D > kMaxZ) return GM_ERR_SHAPE;
+  if (H != 32 && H != 64 && H != 128) return GM_ERR_SHAPE;
+  if (G_total < 1 || G_total > (int64_t(1) << 40) / (2 * H)) return GM_ERR_SHAPE;
+  if (G_total / 2048 + L > int64_t(1) << 30) return GM_ERR_SHAPE;
+  return GM_OK;
+}
+
+gm_status check_adamw(double lr, double beta1, double beta2, double eps, double wd, int32_t step) {
+  if (!(std::isfinite(lr) && lr >= 0.0)) return GM_ERR_VALUE;
+  if (!(beta1 >= 0.0 && beta1 < 1.0 && beta2 >= 0.0 && beta2 < 1.0)) return GM_ERR_VALUE;
+  if (!(std::isfinite(eps) && eps > 0.0)) return GM_ERR_VALUE;
+  if (!(std::isfinite(wd) && wd >= 0.0)) return GM_ERR_VALUE;
+  if (step < 1) return GM_ERR_VALUE;
+  return GM_OK;
+}
+
+// Workspace of the hypernetwork calls, each part 256-byte aligned (see gm::HyperWs).
+struct HyperLayout {
+  size_t gi, cache, o, lay, start, end, first, count, part, dout, dgi, dgh, total;
+};
+
+HyperLayout hyper_layout(int64_t L, int64_t H, int64_t G_total) {
+  HyperLayout Y;
+  const size_t l = size_t(L), h = size_t(H), mc = size_t(gm::hyper_max_chunks(G_total, int(L)));
+  size_t off = 0;
+  auto take = [&](size_t& at, size_t bytes) {
+    at = off;
+    off = round_up(off + bytes, 256);
+  };
+  take(Y.gi, 2 * l * 3 * h * 4);
+  take(Y.cache, 2 * l * 5 * h * 4);
+  take(Y.o, l * 2 * h * 4);
+  take(Y.lay, mc * 4);
+  take(Y.start, mc * 8);
+  take(Y.end, mc * 8);
+  take(Y.first, (l + 1) * 4);
+  take(Y.count, 4);
+  take(Y.part, mc * 2 * h * 4);
+  take(Y.dout, l * 2 * h * 4);
+  take(Y.dgi, 2 * l * 3 * h * 4);
+  take(Y.dgh, 2 * l * 3 * h * 4);
+  Y.total = off;
+  return Y;
+}
+
+gm::HyperWs hyper_ws(void* ws, const HyperLayout& Y) {
+  char* b = static_cast<char*>(ws);
+  gm::HyperWs w;
+  w.gi = reinterpret_cast<float*>(b + Y.gi);
+  w.cache = reinterpret_cast<float*>(b + Y.cache);
+  w.o = reinterpret_cast<float*>(b + Y.o);
+  w.lay = reinterpret_cast<int*>(b + Y.lay);
+  w.start = reinterpret_cast<int64_t*>(b + Y.start);
+  w.end = reinterpret_cast<int64_t*>(b + Y.end);
+  w.first = reinterpret_cast<int*>(b + Y.first);
+  w.count = reinterpret_cast<int*>(b + Y.count);
+  w.part = reinterpret_cast<float*>(b + Y.part);
+  w.dout = reinterpret_cast<float*>(b + Y.dout);
+  w.dgi = reinterpret_cast<float*>(b + Y.dgi);
+  w.dgh = reinterpret_cast<float*>(b + Y.dgh);
+  return w;
+}
+
 }  // namespace
 
 GM_EXPORT int gm_abi_version(void) { return GM_ABI_VERSION; }
@@ -361,4 +429,55 @@ GM_EXPORT gm_status gm_distill_bwd(const uint16_t* W, int64_t N, int64_t d, int6
   auto f = [&](size_t off) { return reinterpret_cast<float*>(b + off); };
   return from_hip(gm::launch_distill_bwd(W, int(N), int(d), int(V), f(L.zt), f(L.zs), f(L.lse_t), f(L.lse_s),
                                          f(L.wtok), reinterpret_cast<uint16_t*>(b + L.dz), L.ldv, dHs, stream));
+}
+
+GM_EXPORT gm_status gm_hyper_workspace_size(int64_t L, int64_t D, int64_t H, int64_t G_total, size_t* bytes) {
+  if (!bytes) return GM_ERR_NULL;
+  if (gm_status st = check_hyper_shape(L, D, H, G_total)) return st;
+  *bytes = hyper_layout(L, H, G_total).total;
+  return GM_OK;
+}
+
+GM_EXPORT gm_status gm_hyper_fwd(const float* z, const float* gru, const float* A, const float* c,
+                                 const int64_t* offsets, int64_t L, int64_t D, int64_t H, int64_t G_total,
+                                 float* logits, void* ws, size_t ws_bytes, gm_stream_t stream) {
+  if (!z || !gru || !A || !c || !offsets || !logits || !ws) return GM_ERR_NULL;
+  if (gm_status st = check_hyper_shape(L, D, H, G_total)) return st;
+  if (!aligned4(z) || !aligned4(gru) || !aligned16(A) || !aligned4(c) || !aligned8(offsets) || !aligned4(logits) ||
+      !aligned16(ws))
+    return GM_ERR_ALIGN;
+  const HyperLayout Y = hyper_layout(L, H, G_total);
+  if (ws_bytes < Y.total) return GM_ERR_WORKSPACE;
+  if (gm_status st = check_device()) return st;
+  return from_hip(gm::launch_hyper_fwd(z, gru, A, c, offsets, int(L), int(D), int(H), G_total, logits,
+                                       hyper_ws(ws, Y), stream));
+}
+
+GM_EXPORT gm_status gm_hyper_bwd(const float* dlogits, const float* z, const float* gru, float* A, float* c,
+                                 float* mA, float* vA, float* mc, float* vc, int64_t L, int64_t D, int64_t H,
+                                 int64_t G_total, double lr, double beta1, double beta2, double eps,
+                                 double weight_decay, int32_t step, float* dgru, void* ws, size_t ws_bytes,
+                                 gm_stream_t stream) {
+  if (!dlogits || !z || !gru || !A || !c || !mA || !vA || !mc || !vc || !dgru || !ws) return GM_ERR_NULL;
+  if (gm_status st = check_hyper_shape(L, D, H, G_total)) return st;
+  if (gm_status st = check_adamw(lr, beta1, beta2, eps, weight_decay, step)) return st;
+  if (!aligned4(dlogits) || !aligned4(z) || !aligned4(gru) || !aligned16(A) || !aligned4(c) || !aligned16(mA) ||
+      !aligned16(vA) || !aligned4(mc) || !aligned4(vc) || !aligned4(dgru) || !aligned16(ws))
+    return GM_ERR_ALIGN;
+  const HyperLayout Y = hyper_layout(L, H, G_total);
+  if (ws_bytes < Y.total) return GM_ERR_WORKSPACE;
+  if (gm_status st = check_device()) return st;
+  return from_hip(gm::launch_hyper_bwd(dlogits, z, gru, A, c, mA, vA, mc, vc, int(L), int(D), int(H), G_total, lr,
+                                       beta1, beta2, eps, weight_decay, step, dgru, hyper_ws(ws, Y), stream));
+}
+
+GM_EXPORT gm_status gm_adamw(float* p, const float* g, float* m, float* v, int64_t n, double lr, double beta1,
+                             double beta2, double eps, double weight_decay, int32_t step, gm_stream_t stream) {
+  if (!p || !g || !m || !v) return GM_ERR_NULL;
+  if (n < 0) return GM_ERR_SHAPE;
+  if (gm_status st = check_adamw(lr, beta1, beta2, eps, weight_decay, step)) return st;
+  if (!aligned4(p) || !aligned4(g) || !aligned4(m) || !aligned4(v)) return GM_ERR_ALIGN;
+  if (n == 0) return GM_OK;
+  if (gm_status st = check_device()) return st;
+  return from_hip(gm::launch_adamw(p, g, m, v, n, lr, beta1, beta2, eps, weight_decay, step, stream));
 }

@@ -49,4 +49,29 @@ hipError_t launch_distill_bwd(const uint16_t* W, int N, int d, int V, const floa
                               const float* lse_t, const float* lse_s, const float* wtok, uint16_t* dz, int ldv,
                               uint16_t* dH, hipStream_t s);
 
+// Hypernetwork (Sec. 2.2, Eq. 3) and AdamW.
+struct HyperWs {
+  float* gi;       // [2][L][3H] input part of the gates
+  float* cache;    // [2][L][5H] h_prev, r, u, n, W_hn h_prev + b_hn
+  float* o;        // [L][2H] GRU outputs
+  int* lay;        // [max chunks] layer of each head chunk
+  int64_t* start;  // [max chunks] first row
+  int64_t* end;    // [max chunks] one past the last row
+  int* first;      // [L + 1] first chunk of each layer
+  int* count;      // [1] number of chunks
+  float* part;     // [max chunks][2H] chunk partials of do
+  float* dout;     // [L][2H] gradient of the GRU outputs
+  float* dgi;      // [2][L][3H] gate gradients, input side
+  float* dgh;      // [2][L][3H] gate gradients, recurrent side
+};
+int hyper_max_chunks(int64_t G_total, int L);
+hipError_t launch_hyper_fwd(const float* z, const float* gru, const float* A, const float* c, const int64_t* offsets,
+                            int L, int D, int H, int64_t G_total, float* logits, const HyperWs& w, hipStream_t s);
+hipError_t launch_hyper_bwd(const float* dlogits, const float* z, const float* gru, float* A, float* c, float* mA,
+                            float* vA, float* mc, float* vc, int L, int D, int H, int64_t G_total, double lr,
+                            double beta1, double beta2, double eps, double weight_decay, int step, float* dgru,
+                            const HyperWs& w, hipStream_t s);
+hipError_t launch_adamw(float* p, const float* g, float* m, float* v, int64_t n, double lr, double beta1,
+                        double beta2, double eps, double weight_decay, int step, hipStream_t s);
+
 }  // namespace gm

@@ -236,3 +236,37 @@ def test_distill_argument_errors():
     assert bwd(FAKE, 16, 256, 1001, FAKE, FAKE, need, None) == gm.GM_ERR_SHAPE
     assert bwd(FAKE, 16, 256, 1000, MISALIGNED, FAKE, need, None) == gm.GM_ERR_ALIGN
     assert bwd(FAKE, 16, 256, 1000, FAKE, FAKE, need - 256, None) == gm.GM_ERR_WORKSPACE
+
+
+def test_hyper_workspace_and_argument_errors():
+    L = gm.LIB
+    need = gm.gm_hyper_workspace_size(224, 64, 64, 25296896)
+    chunks = -(-25296896 // 2048) + 224
+    assert need > chunks * 128 * 4  # the chunk partials of do dominate
+    out = ctypes.c_size_t(0)
+    for args in ((0, 64, 64, 100), (4, 0, 64, 100), (4, 64, 48, 100), (4, 64, 64, 0), (70000, 64, 64, 100)):
+        assert L.gm_hyper_workspace_size(*args, ctypes.byref(out)) == gm.GM_ERR_SHAPE, args
+    ws = gm.gm_hyper_workspace_size(4, 8, 32, 100)
+    fwd = L.gm_hyper_fwd
+    assert fwd(FAKE, FAKE, FAKE, FAKE, None, 4, 8, 32, 100, FAKE, FAKE, ws, None) == gm.GM_ERR_NULL
+    assert fwd(FAKE, FAKE, MISALIGNED, FAKE, FAKE, 4, 8, 32, 100, FAKE, FAKE, ws, None) == gm.GM_ERR_ALIGN
+    assert fwd(FAKE, FAKE, FAKE, FAKE, FAKE, 4, 8, 32, 100, FAKE, FAKE, ws - 1, None) == gm.GM_ERR_WORKSPACE
+    bwd = L.gm_hyper_bwd
+    ok = [FAKE] * 9 + [4, 8, 32, 100, 1e-3, 0.9, 0.999, 1e-8, 0.05, 1, FAKE, FAKE, ws, None]
+
+    def call(i, val):
+        a = list(ok)
+        a[i] = val
+        return bwd(*a)
+
+    for i in range(9):
+        assert call(i, None) == gm.GM_ERR_NULL, i
+    assert call(19, None) == gm.GM_ERR_NULL
+    for i, bad in ((13, -1.0), (14, 1.0), (15, -0.5), (16, 0.0), (17, -0.1), (18, 0)):
+        assert call(i, bad) == gm.GM_ERR_VALUE, (i, bad)
+    assert call(5, MISALIGNED) == gm.GM_ERR_ALIGN
+    assert call(21, ws - 1) == gm.GM_ERR_WORKSPACE
+    assert L.gm_adamw(FAKE, FAKE, FAKE, None, 10, 1e-3, 0.9, 0.999, 1e-8, 0.05, 1, None) == gm.GM_ERR_NULL
+    assert L.gm_adamw(FAKE, FAKE, FAKE, FAKE, -1, 1e-3, 0.9, 0.999, 1e-8, 0.05, 1, None) == gm.GM_ERR_SHAPE
+    assert L.gm_adamw(FAKE, FAKE, FAKE, FAKE, 10, 1e-3, 0.9, 0.999, 1e-8, 0.05, 0, None) == gm.GM_ERR_VALUE
+    assert L.gm_adamw(FAKE, FAKE, FAKE, FAKE, 0, 1e-3, 0.9, 0.999, 1e-8, 0.05, 1, None) == gm.GM_OK

@@ -25,5 +25,7 @@ from .gen import (  # noqa: F401
     make_linear_case,
     DistillCase,
     make_distill_case,
+    HyperCase,
+    make_hyper_case,
 )
 from .configs import CONFIGS, LLAMA2_7B_LINEARS, LLAMA2_13B_LINEARS, config  # noqa: F401

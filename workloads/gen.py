@@ -181,6 +181,51 @@ def make_distill_case(key: Sequence[int], N: int, d: int, V: int, student_noise:
     return DistillCase(N, d, V, bf16_bits_from_f32(ht), bf16_bits_from_f32(hs), bf16_bits_from_f32(w), valid)
 
 
+@dataclasses.dataclass
+class HyperCase:
+    """Host copies of the hypernetwork's parameters, inputs and optimiser state (fp32)."""
+    L: int
+    D: int
+    H: int
+    offsets: np.ndarray  # int64 [L + 1]
+    z: np.ndarray        # [L, D]
+    gru: np.ndarray      # [2 * 3H (D + H + 2)]
+    A: np.ndarray        # [G, 2H]
+    c: np.ndarray        # [G]
+    dlogits: np.ndarray  # [G]
+    mA: np.ndarray       # [G, 2H]
+    vA: np.ndarray       # [G, 2H]
+    mc: np.ndarray       # [G]
+    vc: np.ndarray       # [G]
+
+
+def make_hyper_case(key: Sequence[int], sizes: Sequence[int], D: int, H: int, warm: bool = True) -> HyperCase:
+    """z ~ N(0, 1); GRU weights ~ U(-1/sqrt(H), 1/sqrt(H)) and heads ~ U(-1/sqrt(2H), 1/sqrt(2H)) (the
+    default initialisation of recurrent and linear layers); logit gradients ~ N(0, 0.01^2); with warm,
+    AdamW moments as after some steps (m ~ N(0, 1e-3^2), v ~ U(1e-7, 1e-5)), else zero."""
+    rng = _rng(*key)
+    L = len(sizes)
+    offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    G = int(offsets[-1])
+    P = 2 * 3 * H * (D + H + 2)
+    f32 = np.float32
+    z = rng.standard_normal((L, D), dtype=f32)
+    gru = rng.uniform(-1.0, 1.0, size=P).astype(f32) * f32(1.0 / np.sqrt(H))
+    a = f32(1.0 / np.sqrt(2 * H))
+    A = rng.uniform(-1.0, 1.0, size=(G, 2 * H)).astype(f32) * a
+    c = rng.uniform(-1.0, 1.0, size=G).astype(f32) * a
+    dl = rng.standard_normal(G, dtype=f32) * f32(0.01)
+    if warm:
+        mA = rng.standard_normal((G, 2 * H), dtype=f32) * f32(1e-3)
+        vA = rng.uniform(1e-7, 1e-5, size=(G, 2 * H)).astype(f32)
+        mc = rng.standard_normal(G, dtype=f32) * f32(1e-3)
+        vc = rng.uniform(1e-7, 1e-5, size=G).astype(f32)
+    else:
+        mA, vA = np.zeros((G, 2 * H), f32), np.zeros((G, 2 * H), f32)
+        mc, vc = np.zeros(G, f32), np.zeros(G, f32)
+    return HyperCase(L, D, H, offsets, z, gru, A, c, dl, mA, vA, mc, vc)
+
+
 def rng_for(*key: int) -> np.random.Generator:
     """A generator for ad-hoc draws in tests, derived from the shared seed."""
     return _rng(*key)
