@@ -14,7 +14,8 @@ The JSON line also carries the roofline of the dominant kernel (dgate), the
 fp64 oracle timed on the host cores as a reported baseline, the decode GEMV
 bandwidth on LLaMA-2-13B shapes, the sparsity-budget regulariser over the
 LLaMA-2-7B selectors, the same step with square g x g groups, and the
-distillation loss through the LLaMA-2-7B LM head.
+distillation loss through the LLaMA-2-7B LM head, and the hypernetwork that
+generates the LLaMA-2-7B selector logits (forward, and backward with AdamW).
 """
 from __future__ import annotations
 
@@ -70,6 +71,7 @@ def _parse():
     ap.add_argument("--no-gemv", action="store_true")
     ap.add_argument("--no-square", action="store_true")
     ap.add_argument("--no-distill", action="store_true")
+    ap.add_argument("--no-hyper", action="store_true")
     ap.add_argument("--gemv-layers", type=int, default=40)
     ap.add_argument("--profile-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this size (counter calibration runs)")
@@ -257,6 +259,50 @@ def _distill(reps):
             "logit_bytes_written": 8.0 * N * V, "loss": float(loss.item())}
 
 
+# ------------------------------------------------------------------ hypernetwork
+
+def _hyper(reps):
+    """Hypernetwork over the 224 LLaMA-2-7B selector matrices (1x256 groups), D = H = 64: forward and backward."""
+    import torch
+    import paper_2609_33977_amd as gm
+    import workloads
+    cfg = workloads.config("llama2_7b_step")
+    sizes = [do * di // cfg["g"] for _ in range(cfg["layers"]) for _, do, di in cfg["linears"]]
+    L, D, H = len(sizes), 64, 64
+    G = sum(sizes)
+    offsets = torch.tensor(np.concatenate([[0], np.cumsum(sizes)]), dtype=torch.int64, device="cuda")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(workloads.SEED)
+    P = 2 * 3 * H * (D + H + 2)
+    z = torch.randn(L, D, device="cuda", generator=gen)
+    gru = (torch.rand(P, device="cuda", generator=gen) * 2 - 1) / H ** 0.5
+    A = (torch.rand(G, 2 * H, device="cuda", generator=gen) * 2 - 1) / (2 * H) ** 0.5
+    c = (torch.rand(G, device="cuda", generator=gen) * 2 - 1) / (2 * H) ** 0.5
+    dl = torch.randn(G, device="cuda", generator=gen) * 0.01
+    mA, vA, mc, vc = torch.zeros_like(A), torch.zeros_like(A), torch.zeros_like(c), torch.zeros_like(c)
+    logits = torch.empty(G, device="cuda")
+    dgru = torch.empty(P, device="cuda")
+    ws = torch.empty(gm.gm_hyper_workspace_size(L, D, H, G), dtype=torch.uint8, device="cuda")
+    step = [0]
+
+    def fwd():
+        gm.gm_hyper_fwd(z, gru, A, c, offsets, H, logits, ws)
+
+    def bwd():
+        step[0] += 1
+        gm.gm_hyper_bwd(dl, z, gru, A, c, mA, vA, mc, vc, H, 1e-3, 0.9, 0.999, 1e-8, 0.05, step[0], dgru, ws)
+
+    fwd(); bwd()
+    torch.cuda.synchronize()
+    t_f = _events_ms(fwd, reps)
+    t_b = _events_ms(bwd, reps)
+    b_f = G * (2 * H * 4 + 4 + 4)                          # A, c read; logits written
+    b_b = G * (2 * H * 4 * 6 + 4 + 3 * 4 * 2)              # A, mA, vA read and written; dlogits; c, mc, vc
+    return {"workload": f"LLaMA-2-7B: {L} layers, {G} selectors, D {D}, H {H} (heads {G * 2 * H} fp32 weights)",
+            "fwd_ms": t_f, "fwd_GB/s": b_f / (t_f / 1e3) / 1e9, "bwd_adamw_ms": t_b,
+            "bwd_GB/s": b_b / (t_b / 1e3) / 1e9, "fwd_bytes": b_f, "bwd_bytes": b_b}
+
+
 # ------------------------------------------------------------------ decode GEMV
 
 def _gemv_bandwidth(n_layers, reps):
@@ -400,6 +446,10 @@ def main():
     if not args.no_distill:
         distill = _distill(max(3, args.steps // 4))
 
+    hyper = None
+    if not args.no_hyper:
+        hyper = _hyper(max(3, args.steps // 4))
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = _cpu_baseline(case, flops_step, args.cpu_seconds)
@@ -433,6 +483,7 @@ def main():
         "budget": budget,
         "square_groups": square,
         "distill": distill,
+        "hypernetwork": hyper,
     }
     print(json.dumps(out), flush=True)
 
