@@ -63,8 +63,8 @@ def _dgate_traffic_bytes():
 def _parse():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="approximate host time spent timing the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
