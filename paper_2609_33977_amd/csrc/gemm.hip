@@ -35,8 +35,9 @@
 
 namespace gm {
 
-// Waves per block of the forward and dgate GEMMs (wave tiles 128 x 128 with 4,
-// 128 x 64 with 8: two waves per SIMD hide each other's copy and barrier time).
+// Waves per block of the GEMMs: eight waves of 128 x 64 per 256 x 256 tile,
+// two per SIMD, so one wave's copy issue and barrier wait hide behind the
+// other's MFMAs.
 constexpr int kFwdWaves = 8;
 constexpr int kDgateWaves = 8;
 constexpr int kDxWaves = 8;

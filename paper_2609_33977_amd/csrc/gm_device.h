@@ -6,7 +6,6 @@
 
 namespace gm {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -65,13 +64,8 @@ __device__ __forceinline__ void transpose8x8_b16(const u32x4 (&in)[8], u32x4 (&o
 // Lane l supplies A row (l % 16), k slice [8 (l/16), 8 (l/16) + 8) and
 // B column (l % 16) over the same k slice; it receives C rows 4 (l/16) + j,
 // j = 0..3, of column (l % 16).
-__device__ __forceinline__ f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-}
-
-// The same MFMA accumulating in place, written in assembly with the
-// accumulator as one tied operand.  With the builtin, this clang often gives
+//
+// The MFMA is written in assembly with the accumulator as one tied operand.  With the builtin, this clang often gives
 // the result a different register from the accumulator input and moves it
 // back (up to one move per MFMA with 64 live accumulators), which cuts the
 // issue rate of a 128 x 128 wave tile by a third.  AGPR selects the register
@@ -117,12 +111,5 @@ __device__ __forceinline__ void acc_drain(f32x4 (&acc)[N]) {
     if (i < N_AGPR) acc_pin<true>(acc[i]); else acc_pin<false>(acc[i]);
   }
 }
-
-// ---------------------------------------------------------------- LDS tiles
-
-// A K-major bf16 tile of R rows x 64 k (128 bytes per row, eight 16-byte
-// chunks).  Chunk c of row r is stored at chunk position c ^ (r & 7), so eight
-// consecutive rows read at one logical chunk hit eight different bank groups.
-__device__ __forceinline__ int swz64(int row, int chunk) { return row * 8 + (chunk ^ (row & 7)); }
 
 }  // namespace gm
