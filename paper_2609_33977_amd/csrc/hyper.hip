@@ -53,12 +53,14 @@ __global__ __launch_bounds__(256) void gru_input_kernel(const float* __restrict_
 
 // One block per direction; thread i < 3H owns gate row i of W_hh (in
 // registers).  cache[dir][l] = (h_prev, r, u, n, W_hn h_prev + b_hn), each H.
+// The hidden state is double-buffered in LDS (two barriers per step), and the
+// input part of the next step's gates is loaded while this step runs.
 template <int H>
 __global__ __launch_bounds__(3 * H) void gru_fwd_kernel(const float* __restrict__ gi, const float* __restrict__ gru,
                                                         int L, int D, float* __restrict__ o,
                                                         float* __restrict__ cache) {
   constexpr int G3 = 3 * H;
-  __shared__ float s_h[H], s_gh[G3];
+  __shared__ float s_h[2][H], s_gh[G3];
   const int dir = blockIdx.x, i = threadIdx.x;
   const float* p = gru + int64_t(dir) * G3 * (D + H + 2);
   const float* Whh = p + int64_t(G3) * D;
@@ -66,24 +68,36 @@ __global__ __launch_bounds__(3 * H) void gru_fwd_kernel(const float* __restrict_
   float w[H];
 #pragma unroll
   for (int k = 0; k < H; ++k) w[k] = Whh[i * H + k];
-  if (i < H) s_h[i] = 0.0f;
+  auto gates_in = [&](int s, float (&x)[3]) {  // input part of step s's gates for unit i < H
+    const int l = dir == 0 ? s : L - 1 - s;
+    const float* g = gi + (int64_t(dir) * L + l) * G3;
+    x[0] = g[i];
+    x[1] = g[H + i];
+    x[2] = g[2 * H + i];
+  };
+  float xg[3] = {0.0f, 0.0f, 0.0f};
+  if (i < H) {
+    s_h[0][i] = 0.0f;
+    gates_in(0, xg);
+  }
   __syncthreads();
   for (int s = 0; s < L; ++s) {
     const int l = dir == 0 ? s : L - 1 - s;
-    const float* g = gi + (int64_t(dir) * L + l) * G3;
+    const float* hcur = s_h[s & 1];
     float a = bh;
 #pragma unroll
-    for (int k = 0; k < H; ++k) a += w[k] * s_h[k];
+    for (int k = 0; k < H; ++k) a += w[k] * hcur[k];
     s_gh[i] = a;
     __syncthreads();
-    float hn = 0.0f;
     if (i < H) {
-      const float r = sigmoidf(g[i] + s_gh[i]);
-      const float u = sigmoidf(g[H + i] + s_gh[H + i]);
+      float xn[3] = {0.0f, 0.0f, 0.0f};
+      if (s + 1 < L) gates_in(s + 1, xn);
+      const float r = sigmoidf(xg[0] + s_gh[i]);
+      const float u = sigmoidf(xg[1] + s_gh[H + i]);
       const float ghn = s_gh[2 * H + i];
-      const float n = tanhf(g[2 * H + i] + r * ghn);
-      const float hp = s_h[i];
-      hn = (1.0f - u) * n + u * hp;
+      const float n = tanhf(xg[2] + r * ghn);
+      const float hp = hcur[i];
+      const float hn = (1.0f - u) * n + u * hp;
       float* c = cache + (int64_t(dir) * L + l) * 5 * H;
       c[i] = hp;
       c[H + i] = r;
@@ -91,9 +105,11 @@ __global__ __launch_bounds__(3 * H) void gru_fwd_kernel(const float* __restrict_
       c[3 * H + i] = n;
       c[4 * H + i] = ghn;
       o[int64_t(l) * 2 * H + dir * H + i] = hn;
+      s_h[(s + 1) & 1][i] = hn;  // the other buffer: this step's readers are past the barrier above
+      xg[0] = xn[0];
+      xg[1] = xn[1];
+      xg[2] = xn[2];
     }
-    __syncthreads();  // every row has read s_h
-    if (i < H) s_h[i] = hn;
     __syncthreads();
   }
 }
@@ -245,7 +261,9 @@ __global__ __launch_bounds__(256) void head_do_kernel(const float* __restrict__ 
 // One block of 4H threads per direction.  Phase A (threads k < H): the gate
 // gradients of step l from dh = do + carried gradient; phase B (all
 // threads, four per hidden unit k): dh_prev[k] = u dh + sum_i W_hh[i, k] dgh[i]
-// over a quarter of the 3H rows each, combined with two shuffles.
+// over a quarter of the 3H rows each, combined with two shuffles.  The
+// carried gradient alternates between two LDS buffers, so a step needs two
+// barriers; the cached gates of the next step are loaded during this one.
 // dgi, dgh [dir][l][3H] are kept for the weight gradients.
 template <int H>
 __global__ __launch_bounds__(4 * H) void gru_bwd_kernel(const float* __restrict__ dout,
@@ -253,21 +271,34 @@ __global__ __launch_bounds__(4 * H) void gru_bwd_kernel(const float* __restrict_
                                                         int L, int D, float* __restrict__ dgi,
                                                         float* __restrict__ dgh) {
   constexpr int G3 = 3 * H, RPT = G3 / 4;
-  __shared__ float s_dh[H], s_carry[H], s_g[G3];
+  __shared__ float s_dh[2][H], s_carry[H], s_g[G3];  // s_dh double-buffered by step parity
   const int dir = blockIdx.x, tid = threadIdx.x;
   const float* Whh = gru + int64_t(dir) * G3 * (D + H + 2) + int64_t(G3) * D;
   const int k = tid >> 2, seg = tid & 3;
   float wc[RPT];  // W_hh[seg * RPT + j, k]
 #pragma unroll
   for (int j = 0; j < RPT; ++j) wc[j] = Whh[(seg * RPT + j) * H + k];
-  if (tid < H) s_dh[tid] = 0.0f;
+  // this unit's cached gates and output gradient of step s, loaded one step ahead
+  auto fetch = [&](int s, float (&v)[6]) {
+    const int l = dir == 0 ? s : L - 1 - s;
+    const float* c = cache + (int64_t(dir) * L + l) * 5 * H;
+#pragma unroll
+    for (int q = 0; q < 5; ++q) v[q] = c[q * H + tid];
+    v[5] = dout[int64_t(l) * 2 * H + dir * H + tid];
+  };
+  float cur[6] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+  if (tid < H) {
+    s_dh[(L - 1) & 1][tid] = 0.0f;
+    fetch(L - 1, cur);
+  }
   __syncthreads();
   for (int s = L - 1; s >= 0; --s) {
     const int l = dir == 0 ? s : L - 1 - s;
     if (tid < H) {
-      const float* c = cache + (int64_t(dir) * L + l) * 5 * H;
-      const float hp = c[tid], r = c[H + tid], u = c[2 * H + tid], n = c[3 * H + tid], ghn = c[4 * H + tid];
-      const float dh = s_dh[tid] + dout[int64_t(l) * 2 * H + dir * H + tid];
+      float nxt[6] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+      if (s > 0) fetch(s - 1, nxt);
+      const float hp = cur[0], r = cur[1], u = cur[2], n = cur[3], ghn = cur[4];
+      const float dh = s_dh[s & 1][tid] + cur[5];
       const float dan = dh * (1.0f - u) * (1.0f - n * n);
       const float dar = dan * ghn * r * (1.0f - r);
       const float dau = dh * (hp - n) * u * (1.0f - u);
@@ -283,6 +314,8 @@ __global__ __launch_bounds__(4 * H) void gru_bwd_kernel(const float* __restrict_
       s_g[H + tid] = dau;
       s_g[2 * H + tid] = dan * r;
       s_carry[tid] = dh * u;
+#pragma unroll
+      for (int q = 0; q < 6; ++q) cur[q] = nxt[q];
     }
     __syncthreads();
     float a = 0.0f;
@@ -290,8 +323,7 @@ __global__ __launch_bounds__(4 * H) void gru_bwd_kernel(const float* __restrict_
     for (int j = 0; j < RPT; ++j) a += wc[j] * s_g[seg * RPT + j];
     a += __shfl_xor(a, 1);
     a += __shfl_xor(a, 2);
-    __syncthreads();  // s_dh was read in phase A of this step
-    if (seg == 0) s_dh[k] = s_carry[k] + a;
+    if (seg == 0 && s > 0) s_dh[(s - 1) & 1][k] = s_carry[k] + a;  // the buffer phase A did not read
     __syncthreads();
   }
 }
