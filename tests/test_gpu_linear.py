@@ -202,3 +202,34 @@ def test_workspace_too_small_is_rejected_without_launch():
     with pytest.raises(gm.GroupMaskError) as ei:
         gm.gm_masked_linear_bwd(d["dY"], d["X"], d["W"], d["mask"], g, dX, None, small)
     assert ei.value.status == gm.GM_ERR_WORKSPACE
+
+
+@pytest.mark.parametrize("T,d_in,d_out,g", [
+    (17, 64, 8, 64),          # smallest GEMM-path token count, one group column, eight output rows
+    (300, 32768, 256, 64),    # 512 group columns per row: the forward's per-tile limit
+    (16, 32768, 264, 64),     # the same row width on the decode path
+    (40, 2048, 8, 512),       # a single 8-row tile row, groups spanning two dgate tiles
+])
+def test_edge_shapes(T, d_in, d_out, g):
+    say(f"edge shape: T={T} d_in={d_in} d_out={d_out} g={g}")
+    case = workloads.make_linear_case((210, T, d_in, d_out, g), T, d_in, d_out, g, None)
+    d = _dev_case(case)
+    Y = _fwd(d, g)
+    Yr, dXr, dgr = _oracle_all(case)
+    assert_close("Y", host_f64_from_bf16(Y), Yr)
+    if T > 16:
+        dX, dgate = _bwd(d, g)
+        assert_close("dX", host_f64_from_bf16(dX), dXr)
+        assert_close("dgate", dgate.cpu().numpy(), dgr)
+
+
+def test_decode_and_gemm_paths_agree_at_the_boundary():
+    # T = 16 runs the GEMV, T = 17 the GEMM: the first 16 rows of the larger
+    # batch must match the smaller batch's rows to rounding
+    d_in, d_out, g = 1024, 256, 256
+    case = workloads.make_linear_case((211,), 17, d_in, d_out, g, None)
+    d17 = _dev_case(case)
+    d16 = dict(d17, X=d17["X"][:16].contiguous())
+    Y17 = host_f64_from_bf16(_fwd(d17, g))[:16]
+    Y16 = host_f64_from_bf16(_fwd(d16, g))
+    assert_close("Y (GEMV vs GEMM)", Y16, Y17, 1e-2)

@@ -216,3 +216,21 @@ def test_square_llama2_7b_down_projection(g):
     assert_close("dX (sampled tokens)", host_f64_from_bf16(dX)[t_s], oracle.linear_bwd_dx(dY[t_s], W, m, g, g))
     assert_close("dgate (sampled group rows)", dgate.cpu().numpy()[u_s],
                  oracle.linear_bwd_dgate(dY[:, rows], X, W[rows], g, g))
+
+
+def test_square_16_widest_rows():
+    # 16 x 16 groups over 16384 inputs: 1024 selectors per mask row, the
+    # forward's and the decode GEMV's largest per-row lists
+    T, d_in, d_out, g = 130, 16384, 128, 16
+    say(f"square 16x16 widest rows: T={T} d_in={d_in}")
+    case = _case((231,), T, d_in, d_out, g)
+    d = _dev(case)
+    Y = _fwd(d, g)
+    dX, dgate = _bwd(d, g)
+    Yr, dXr, dgr = _oracle(case)
+    assert_close("Y", host_f64_from_bf16(Y), Yr)
+    assert_close("dX", host_f64_from_bf16(dX), dXr)
+    assert_close("dgate", dgate.cpu().numpy(), dgr)
+    case1 = _case((232,), 3, d_in, d_out, g)
+    Y1 = _fwd(_dev(case1), g)
+    assert_close("Y (decode)", host_f64_from_bf16(Y1), _oracle(case1)[0])
