@@ -187,7 +187,7 @@ def test_packed_forward(T):
     Yr, _, _ = _oracle_all(case)
     assert_close("Y", host_f64_from_bf16(Y), Yr)
     Y2 = _fwd(d, g)
-    if T <= 16:  # same GEMV kernel over the two layouts: identical results
+    if T == 1:  # the same one-wave-per-row kernel reads both layouts: identical results
         assert np.array_equal(host_bits(Y), host_bits(Y2))
 
 

@@ -191,7 +191,7 @@ def test_square_export_and_packed_forward(g):
     sync()
     Yr, _, _ = _oracle(case, soft)
     assert_close("Y (packed)", host_f64_from_bf16(Y), Yr)
-    assert np.array_equal(host_bits(Y), host_bits(_fwd(d, g)))  # the same GEMV over both layouts
+    assert_close("Y (in place, 16-token MFMA path)", host_f64_from_bf16(_fwd(d, g)), Yr)
 
 
 @pytest.mark.parametrize("g", [16, 64])
