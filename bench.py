@@ -72,6 +72,8 @@ def _parse():
     ap.add_argument("--no-square", action="store_true")
     ap.add_argument("--no-distill", action="store_true")
     ap.add_argument("--no-hyper", action="store_true")
+    ap.add_argument("--no-model", action="store_true", help="skip the MLP-trio and whole-LLaMA-2-7B steps")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the LLaMA-2-13B T=8192 sweep and T=512 forward")
     ap.add_argument("--gemv-layers", type=int, default=40)
     ap.add_argument("--profile-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this size (counter calibration runs)")
@@ -171,6 +173,193 @@ def _events_batch_ms(fn, n):
     end.record()
     torch.cuda.synchronize()
     return float(start.elapsed_time(end)) / n
+
+
+class ModelStep:
+    """One mask-learning step over several masked linears whose selectors share one flat array: one gate
+    call over all of them, every linear's forward, every linear's backward (dX and dgate, last linear
+    first), one STE call.  Each linear has its own X, W and dY (drawn on the device); the kept set of
+    every selector matrix is drawn with its budget and encoded in the gate inputs."""
+
+    def __init__(self, T, shapes, kept, g, tau, key):
+        import torch
+        import paper_2609_33977_amd as gm
+        import workloads
+        self.gm, self.g, self.tau, self.T = gm, g, tau, T
+        self.shapes = list(shapes)
+        sizes = [d_out * (d_in // g) for d_out, d_in in self.shapes]
+        self.offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+        n = int(self.offsets[-1])
+        r = workloads.gen.rng_for(*key)
+        logits, noise = np.empty(n, np.float32), np.empty(n, np.float32)
+        for l, (G, k) in enumerate(zip(sizes, kept)):
+            lo, hi = self.offsets[l], self.offsets[l + 1]
+            logits[lo:hi], noise[lo:hi] = workloads.budgeted_gate_inputs(r, workloads.random_kept_mask(r, G, k))
+        self.kept_total = int(sum(kept))
+        dev = "cuda"
+        self.logits, self.noise = torch.from_numpy(logits).to(dev), torch.from_numpy(noise).to(dev)
+        self.mask, self.soft, self.dgate, self.dlogits = (torch.empty(n, device=dev) for _ in range(4))
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(workloads.SEED + 1000 * key[0] + key[1])
+        self.lin = []
+        fws = bws = 16
+        for l, (d_out, d_in) in enumerate(self.shapes):
+            lo, hi = int(self.offsets[l]), int(self.offsets[l + 1])
+            X = torch.randn(T, d_in, device=dev, generator=gen).to(torch.bfloat16)
+            W = (torch.randn(d_out, d_in, device=dev, generator=gen) * 0.02).to(torch.bfloat16)
+            dY = torch.randn(T, d_out, device=dev, generator=gen).to(torch.bfloat16)
+            Y = torch.empty(T, d_out, dtype=torch.bfloat16, device=dev)
+            dX = torch.empty(T, d_in, dtype=torch.bfloat16, device=dev)
+            view = lambda t, lo=lo, hi=hi, d_out=d_out, d_in=d_in: t[lo:hi].view(d_out, d_in // g)
+            self.lin.append((X, W, dY, Y, dX, view(self.mask), view(self.dgate)))
+            fws = max(fws, gm.gm_workspace_size(gm.GM_OP_FWD, T, d_in, d_out, g))
+            bws = max(bws, gm.gm_workspace_size(gm.GM_OP_BWD, T, d_in, d_out, g))
+        self.fws = torch.empty(fws, dtype=torch.uint8, device=dev)
+        self.ws = torch.empty(bws, dtype=torch.uint8, device=dev)
+        kept_params = [k * g for k in kept]
+        self.flops = {"fwd": sum(2.0 * T * p for p in kept_params), "dx": sum(2.0 * T * p for p in kept_params),
+                      "dgate": sum(2.0 * T * d_out * d_in for d_out, d_in in self.shapes)}
+
+    def gate(self):
+        self.gm.gm_gate(self.logits, self.noise, self.tau, True, self.mask, self.soft)
+
+    def fwd(self):
+        for X, W, _, Y, _, m, _ in self.lin:
+            self.gm.gm_masked_linear_fwd(X, W, m, self.g, Y, self.fws)
+
+    def bwd(self):
+        for X, W, dY, _, dX, m, dg in reversed(self.lin):
+            self.gm.gm_masked_linear_bwd(dY, X, W, m, self.g, dX, dg, self.ws)
+
+    def gate_bwd(self):
+        self.gm.gm_gate_bwd(self.dgate, self.soft, self.tau, self.dlogits)
+
+    def __call__(self):
+        self.gate()
+        self.fwd()
+        self.bwd()
+        self.gate_bwd()
+
+
+def _model_step(step, reps, workload):
+    import torch
+    for _ in range(2):
+        step()
+    torch.cuda.synchronize()
+    if int(step.mask.sum().item()) != step.kept_total:
+        raise RuntimeError("gate kept count differs from the budget")
+    ms = _events_batch_ms(step, reps)
+    fwd = _events_batch_ms(step.fwd, reps)
+    bwd = _events_batch_ms(step.bwd, reps)
+    fl = step.flops
+    total = sum(fl.values())
+    return {"workload": workload, "linears": len(step.shapes), "selectors": int(step.offsets[-1]),
+            "kept": step.kept_total, "TFLOP_per_step": total / 1e12, "ms_per_step": ms,
+            "TFLOP/s": total / (ms / 1e3) / 1e12, "frac_of_bf16_peak": total / (ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
+            "fwd_ms": fwd, "fwd_kept_TFLOP/s": fl["fwd"] / (fwd / 1e3) / 1e12,
+            "bwd_ms": bwd, "bwd_TFLOP/s": (fl["dx"] + fl["dgate"]) / (bwd / 1e3) / 1e12}
+
+
+def _mlp_trio(reps):
+    """LLaMA-2-7B MLP trio (gate/up 11008x4096, down 4096x11008), T 4096, per-matrix sparsity ~ U(0.3, 0.7)."""
+    import workloads
+    cfg = workloads.config("mlp_trio_7b")
+    g = cfg["g"]
+    shapes = [(d_out, d_in) for _, d_out, d_in in cfg["linears"]]
+    kept, s = workloads.kept_counts_uniform_law(workloads.gen.rng_for(3, 0), [o * (i // g) for o, i in shapes],
+                                                *cfg["law"][1:])
+    step = ModelStep(cfg["T"], shapes, kept, g, cfg["tau"], (3, 1))
+    out = _model_step(step, reps, "LLaMA-2-7B MLP trio: gate/up 11008x4096, down 4096x11008, T 4096, "
+                                  "1x256 groups, sparsity ~ U(0.3, 0.7) per matrix")
+    out["sparsity"] = [round(float(x), 4) for x in s]
+    return out
+
+
+def _llama2_7b_step(reps):
+    """Every masked linear of LLaMA-2-7B (32 layers x 7 = 224), T 4096, Beta(2,2) budgets at 50 % overall."""
+    import workloads
+    cfg = workloads.config("llama2_7b_step")
+    g = cfg["g"]
+    shapes = [(d_out, d_in) for _ in range(cfg["layers"]) for _, d_out, d_in in cfg["linears"]]
+    sizes = [o * (i // g) for o, i in shapes]
+    kept, _ = workloads.kept_counts_beta_law(workloads.gen.rng_for(4, 0), sizes, [o * i for o, i in shapes], 0.5)
+    step = ModelStep(cfg["T"], shapes, kept, g, cfg["tau"], (4, 1))
+    return _model_step(step, reps, "LLaMA-2-7B, all 224 masked linears (32 layers x q,k,v,o,gate,up,down), "
+                                   "T 4096, 1x256 groups, Beta(2,2) per-matrix budgets, 50% of 25,296,896 kept; "
+                                   "one gate and one STE call over all selectors")
+
+
+def _sweep_13b(reps):
+    """LLaMA-2-13B shapes at T 8192: forward and backward per call for g in {64, 128, 256, 512}, half kept."""
+    import torch
+    import paper_2609_33977_amd as gm
+    import workloads
+    cfg = workloads.config("llama2_13b_infer")
+    T = cfg["T_sweep"]
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(workloads.SEED + 5)
+    out = {"workload": f"LLaMA-2-13B q (5120x5120), gate (13824x5120), down (5120x13824), T {T}, 1xg groups, "
+                       "50% kept at random"}
+    for name, d_out, d_in in (cfg["linears"][0], cfg["linears"][4], cfg["linears"][6]):
+        X = torch.randn(T, d_in, device="cuda", generator=gen).to(torch.bfloat16)
+        W = (torch.randn(d_out, d_in, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
+        dY = torch.randn(T, d_out, device="cuda", generator=gen).to(torch.bfloat16)
+        Y = torch.empty(T, d_out, dtype=torch.bfloat16, device="cuda")
+        dX = torch.empty(T, d_in, dtype=torch.bfloat16, device="cuda")
+        for g in cfg["g_sweep"]:
+            G = d_out * (d_in // g)
+            m = torch.zeros(G, device="cuda")
+            m[torch.randperm(G, device="cuda", generator=gen)[: G // 2]] = 1.0
+            m = m.view(d_out, d_in // g)
+            dg = torch.empty(d_out, d_in // g, device="cuda")
+            ws = torch.empty(gm.gm_workspace_size(gm.GM_OP_BWD, T, d_in, d_out, g), dtype=torch.uint8, device="cuda")
+            fwd = lambda: gm.gm_masked_linear_fwd(X, W, m, g, Y)
+            bwd = lambda: gm.gm_masked_linear_bwd(dY, X, W, m, g, dX, dg, ws)
+            for _ in range(3):
+                fwd()
+                bwd()
+            torch.cuda.synchronize()
+            tf, tb = _events_ms(fwd, reps), _events_ms(bwd, reps)
+            kept_fl, dense_fl = 2.0 * T * (G // 2) * g, 2.0 * T * d_out * d_in
+            out[f"{name}_g{g}"] = {"fwd_ms": tf, "bwd_ms": tb, "fwd_kept_TFLOP/s": kept_fl / (tf / 1e3) / 1e12,
+                                   "bwd_TFLOP/s": (kept_fl + dense_fl) / (tb / 1e3) / 1e12,
+                                   "TFLOP/s": (2 * kept_fl + dense_fl) / ((tf + tb) / 1e3) / 1e12}
+        del X, W, dY, Y, dX
+    return out
+
+
+def _prefill_13b(reps):
+    """LLaMA-2-13B forward at T 512 over the seven linears of one layer: 40 to 108 output tiles, so the
+    forward splits K (its workspace is passed)."""
+    import torch
+    import paper_2609_33977_amd as gm
+    import workloads
+    cfg = workloads.config("llama2_13b_infer")
+    T, g = 512, cfg["g"]
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(workloads.SEED + 6)
+    mats, fl, by = [], 0.0, 0.0
+    ws = torch.empty(max(max(gm.gm_workspace_size(gm.GM_OP_FWD, T, d_in, d_out, g) for _, d_out, d_in in cfg["linears"]),
+                         16), dtype=torch.uint8, device="cuda")
+    for _, d_out, d_in in cfg["linears"]:
+        X = torch.randn(T, d_in, device="cuda", generator=gen).to(torch.bfloat16)
+        W = (torch.randn(d_out, d_in, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
+        G = d_out * (d_in // g)
+        m = torch.zeros(G, device="cuda")
+        m[torch.randperm(G, device="cuda", generator=gen)[: G // 2]] = 1.0
+        mats.append((X, W, m.view(d_out, d_in // g), torch.empty(T, d_out, dtype=torch.bfloat16, device="cuda")))
+        fl += 2.0 * T * (G // 2) * g
+        by += (G // 2) * g * 2 + G * 4 + 2 * T * (d_in + d_out)
+
+    def run():
+        for X, W, m, Y in mats:
+            gm.gm_masked_linear_fwd(X, W, m, g, Y, ws)
+    for _ in range(3):
+        run()
+    torch.cuda.synchronize()
+    ms = _events_ms(run, reps)
+    return {"workload": "LLaMA-2-13B q,k,v,o,gate,up,down forward, T 512, 1x256 groups, 50% kept",
+            "ms_per_layer": ms, "kept_TFLOP/s": fl / (ms / 1e3) / 1e12, "GB/s": by / (ms / 1e3) / 1e9}
 
 
 # ------------------------------------------------------------------ CPU baseline
@@ -429,6 +618,26 @@ def _gemv_bandwidth(n_layers, reps):
         del graph
     out.update({"GB/s": total / (best / 1e3) / 1e9, "frac_of_peak": total / (best / 1e3) / 1e9 / PEAK_HBM_GBS,
                 "ms_per_pass": best, "schedule": best_name})
+    # 8 and 16 tokens over the same weights and masks, seven launches per layer (eager)
+    for T in (8, 16):
+        xs, ys, extra = {}, [], 0
+        for mats in layers:
+            for X1, W, m, _ in mats:
+                key = id(X1)
+                if key not in xs:
+                    xs[key] = torch.randn(T, X1.shape[1], device="cuda", generator=gen).to(torch.bfloat16)
+                ys.append((xs[key], W, m, torch.empty(T, W.shape[0], dtype=torch.bfloat16, device="cuda")))
+                extra += 2 * (T - 1) * (W.shape[0] + W.shape[1])
+
+        def serial_t():
+            for mat in ys:
+                run(mat)
+        serial_t()
+        torch.cuda.synchronize()
+        t = _events_ms(serial_t, reps)
+        out[f"T{T}_GB/s"] = (total + extra) / (t / 1e3) / 1e9
+        out[f"T{T}_ms_per_pass"] = t
+        del ys, xs
     return out
 
 
@@ -541,6 +750,16 @@ def main():
     if not args.no_hyper:
         hyper = _hyper(max(3, args.steps // 4))
 
+    mlp = model = None
+    if not args.no_model:
+        mlp = _mlp_trio(max(5, args.steps // 4))
+        model = _llama2_7b_step(max(3, args.steps // 40))
+
+    sweep = prefill = None
+    if not args.no_sweep:
+        sweep = _sweep_13b(max(5, args.steps // 10))
+        prefill = _prefill_13b(max(5, args.steps // 4))
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = _cpu_baseline(case, flops_step, args.cpu_seconds)
@@ -575,6 +794,10 @@ def main():
         "square_groups": square,
         "distill": distill,
         "hypernetwork": hyper,
+        "mlp_trio": mlp,
+        "llama2_7b_step": model,
+        "sweep_13b": sweep,
+        "prefill_13b": prefill,
     }
     print(json.dumps(out), flush=True)
 

@@ -40,7 +40,7 @@
 extern "C" {
 #endif
 
-#define GM_ABI_VERSION 2
+#define GM_ABI_VERSION 3
 
 /* Same object as a hipStream_t, declared here so that callers need no HIP headers. */
 typedef struct ihipStream_t* gm_stream_t;
@@ -147,7 +147,10 @@ gm_status gm_gate_bwd_budget(const float* dgate, const float* soft, int64_t n, f
 /*
  * gm_workspace_size -- host-only query of the workspace (bytes) that
  * gm_masked_linear_fwd (op = GM_OP_FWD) or gm_masked_linear_bwd
- * (op = GM_OP_BWD) needs for the given shape.  No device work.
+ * (op = GM_OP_BWD) needs for the given shape.  No device work.  The forward
+ * needs one only for launches of few output tiles (at most 128 tiles of
+ * 256 x 256, e.g. T = 512 with d_out = 5120), where it splits K: then
+ * ksplit * T * d_out fp32 for the partial tiles (ksplit <= 8); otherwise 0.
  *   bytes: HOST pointer, required.
  */
 gm_status gm_workspace_size(int op, int64_t T, int64_t d_in, int64_t d_out, int32_t g, int32_t g_out,
@@ -168,8 +171,13 @@ gm_status gm_workspace_size(int op, int64_t T, int64_t d_in, int64_t d_out, int3
  *   d_out a multiple of g_out; each of X, W, Y (T rounded up to a multiple
  *   of 8) below 2^30 - 2^22 elements.  Mask values must be finite and >= 0
  *   (not checked).
- *   ws / ws_bytes: workspace of at least gm_workspace_size(GM_OP_FWD, ...)
- *   bytes (ws may be NULL when that size is 0).
+ *   ws / ws_bytes: optional workspace (16-byte aligned).  NULL: the GEMM
+ *   runs unsplit.  Otherwise at least gm_workspace_size(GM_OP_FWD, ...) bytes
+ *   (GM_ERR_WORKSPACE if smaller), and shapes with few output tiles split K
+ *   over several blocks whose fp32 partial tiles are added in a fixed order
+ *   before the one rounding to bf16 (the same Y up to fp32 summation order;
+ *   deterministic for a given shape).  The workspace is scratch: its contents
+ *   are not used across calls.
  */
 gm_status gm_masked_linear_fwd(const uint16_t* X, const uint16_t* W, const float* mask, int64_t T,
                                int64_t d_in, int64_t d_out, int32_t g, int32_t g_out, uint16_t* Y,

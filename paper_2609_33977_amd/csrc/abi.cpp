@@ -3,6 +3,7 @@
 // every entry point checks all of its arguments before the first launch.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
@@ -76,6 +77,28 @@ gm_status check_linear_shape(int64_t T, int64_t d_in, int64_t d_out, int32_t g, 
   const int64_t t8 = (T + 7) / 8 * 8;
   if (t8 * d_in > kMaxElems || t8 * d_out > kMaxElems || d_out * d_in > kMaxElems) return GM_ERR_SHAPE;
   return GM_OK;
+}
+
+// Split K of the forward GEMM: a launch of 256 x 256 tiles with at most 128
+// tiles (half the CUs or fewer, e.g. T = 512 at LLaMA-2-13B shapes) spreads
+// each tile's K range over ksplit blocks, up to 256 blocks in all, at most 8
+// shares and at least two column units per share.  The partial tiles take
+// ksplit * T * d_out fp32 of workspace.
+constexpr int64_t kSplitMaxTiles = 128, kSplitBlocks = 256, kSplitMax = 8;
+
+int fwd_splits(int64_t T, int64_t d_in, int64_t d_out, int32_t g) {
+  if (T <= kDecodeTokens) return 1;
+  const int64_t tiles = ((T + 255) / 256) * ((d_out + 255) / 256);
+  if (tiles > kSplitMaxTiles) return 1;
+  int64_t ks = kSplitBlocks / tiles;
+  ks = std::min(ks, kSplitMax);
+  ks = std::min(ks, d_in / unit_width(g) / 2);
+  return int(std::max<int64_t>(ks, 1));
+}
+
+size_t fwd_workspace(int64_t T, int64_t d_in, int64_t d_out, int32_t g) {
+  const int ks = fwd_splits(T, d_in, d_out, g);
+  return ks > 1 ? round_up(size_t(ks) * size_t(T) * size_t(d_out) * sizeof(float), 256) : 0;
 }
 
 // Workspace of the backward, each part 256-byte aligned, over NL = d_in / lc
@@ -299,23 +322,26 @@ GM_EXPORT gm_status gm_workspace_size(int op, int64_t T, int64_t d_in, int64_t d
   if (!bytes) return GM_ERR_NULL;
   if (op != GM_OP_FWD && op != GM_OP_BWD) return GM_ERR_VALUE;
   if (gm_status st = check_linear_shape(T, d_in, d_out, g, g_out)) return st;
-  *bytes = op == GM_OP_FWD ? 0 : bwd_layout(T, d_in, d_out, g).total;
+  *bytes = op == GM_OP_FWD ? fwd_workspace(T, d_in, d_out, g) : bwd_layout(T, d_in, d_out, g).total;
   return GM_OK;
 }
 
 GM_EXPORT gm_status gm_masked_linear_fwd(const uint16_t* X, const uint16_t* W, const float* mask, int64_t T,
                                          int64_t d_in, int64_t d_out, int32_t g, int32_t g_out, uint16_t* Y,
                                          void* ws, size_t ws_bytes, gm_stream_t stream) {
-  (void)ws;
-  (void)ws_bytes;
   if (!X || !W || !mask || !Y) return GM_ERR_NULL;
   if (gm_status st = check_linear_shape(T, d_in, d_out, g, g_out)) return st;
-  if (!aligned16(X) || !aligned16(W) || !aligned16(mask) || !aligned16(Y)) return GM_ERR_ALIGN;
+  if (!aligned16(X) || !aligned16(W) || !aligned16(mask) || !aligned16(Y) || (ws && !aligned16(ws)))
+    return GM_ERR_ALIGN;
+  const size_t need = fwd_workspace(T, d_in, d_out, g);
+  if (ws && ws_bytes < need) return GM_ERR_WORKSPACE;
   if (gm_status st = check_device()) return st;
   const int t = int(T), di = int(d_in), dout = int(d_out);
   if (T <= kDecodeTokens && d_in / g <= gm::gemv_max_groups_per_row())
     return from_hip(gm::launch_gemv_inplace(X, W, mask, t, di, dout, g, g_out, Y, stream));
-  return from_hip(gm::launch_fwd(X, W, mask, t, di, dout, g, g_out, Y, stream));
+  // Without a workspace the forward runs unsplit (the same Y up to fp32 summation order).
+  const int ks = ws && need ? fwd_splits(T, d_in, d_out, g) : 1;
+  return from_hip(gm::launch_fwd(X, W, mask, t, di, dout, g, g_out, Y, ks, static_cast<float*>(ws), stream));
 }
 
 GM_EXPORT gm_status gm_masked_linear_bwd(const uint16_t* dY, const uint16_t* X, const uint16_t* W,

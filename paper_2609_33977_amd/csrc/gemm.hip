@@ -58,10 +58,16 @@ constexpr int kStagesDx = 4;
 // group shares its 32-deep slice with its neighbour) and visits only the
 // units that some row of the tile keeps; inside a visited unit each 16-byte
 // chunk of W whose group is pruned for its row is zero-filled instead of read.
+//
+// Split K (ksplit > 1, for launches with fewer tiles than half the CUs):
+// block b works on tile b / ksplit and takes share b % ksplit of the tile's
+// list of visited units (contiguous, in order), and stores its fp32 partial
+// tile into part[share][t][o]; fwd_reduce_kernel then adds the shares in
+// order and rounds once.
 template <int G, int GO>
 __global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
                                                   const float* __restrict__ mask, int T, int d_in, int d_out,
-                                                  uint16_t* __restrict__ Y) {
+                                                  uint16_t* __restrict__ Y, int ksplit, float* __restrict__ part) {
   constexpr int NW = kFwdWaves, WN = NW / 2;  // waves per block; wave grid 2 (M) x WN (N)
   constexpr int BM = 256, BN = 256, MB = 8, NB = BN / WN / 16;
   constexpr int U = G < kBK ? kBK : G;        // input columns of one unit
@@ -87,8 +93,9 @@ __global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __r
   const int wm = wave / WN, wn = wave % WN;
   const int G_in = d_in / G, NU = d_in / U;
   const int tiles_m = (d_out + BM - 1) / BM, tiles_n = (T + BN - 1) / BN;
+  const int share = int(blockIdx.x) % ksplit;
   int tm, tn;
-  tile_coords(gridDim.x, tiles_m, tiles_n, tm, tn);
+  tile_coords(int(blockIdx.x) / ksplit, int(gridDim.x) / ksplit, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
 
   // Prologue: kept bits of every mask row of the tile, the units some row keeps, soft values.
@@ -163,7 +170,11 @@ __global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __r
     if (lane == 0) s_ncols = cnt;
   }
   __syncthreads();
-  const int nst = s_ncols * SUB;
+  // this block's share of the visited units: list entries [c0, c1)
+  const int c0 = share * s_ncols / ksplit, c1 = (share + 1) * s_ncols / ksplit;
+  const int nst = (c1 - c0) * SUB;
+  const int cb = c0 < s_ncols ? c0 : 0;  // an empty share reads (never consumes) entry 0
+  const int* cols = s_cols + cb;
 
   // This lane's CA DMA rows (the same in both tiles): row = 16 (CA wave + j) + lane / 4,
   // their mask rows within the tile, the group of their chunk within a unit,
@@ -190,8 +201,8 @@ __global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __r
   const uint32_t ldsA = lds_addr(As), ldsB = lds_addr(Bs);
   auto col_of = [&](int st) { return st < nst ? st / SUB : 0; };  // slices past the end reuse unit 0
   auto group_of = [&](int un, int j) { return un * UG + gsub[j]; };
-  int v_cur = __builtin_amdgcn_readfirstlane(s_cols[0]);
-  int v_nxt = __builtin_amdgcn_readfirstlane(s_cols[col_of(1)]);
+  int v_cur = __builtin_amdgcn_readfirstlane(cols[0]);
+  int v_nxt = __builtin_amdgcn_readfirstlane(cols[col_of(1)]);
   // Square groups of 32 rows and more: fragment rows of this wave that keep
   // the unit of the slice consumed next (slice st - STAGES + 1 when
   // prepare(st) runs).  With 16 x 16 groups a fragment row skips a 32-deep
@@ -214,9 +225,9 @@ __global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __r
 #pragma unroll
     for (int j = 0; j < CA; ++j) bits_cur[j] = s_bits[brow[j]][group_of(v_nxt, j) >> 5];
     v_cur = v_nxt;
-    v_nxt = __builtin_amdgcn_readfirstlane(s_cols[col_of(st + 2)]);
+    v_nxt = __builtin_amdgcn_readfirstlane(cols[col_of(st + 2)]);
     if constexpr (SKIP)
-      live_nxt = (__builtin_amdgcn_readfirstlane(s_live[col_of(max(st - STAGES + 1, 0))]) >> (wm * 8)) & 0xffu;
+      live_nxt = (__builtin_amdgcn_readfirstlane(s_live[cb + col_of(max(st - STAGES + 1, 0))]) >> (wm * 8)) & 0xffu;
   };
   auto live = [&](int) { return live_nxt; };
   // copies 0..CA-1 fill this wave's row blocks of the W tile, CA..2CA-1 of the X tile
@@ -230,7 +241,7 @@ __global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __r
   };
   // Soft selectors: scale this lane's freshly landed W chunks by their mask value.
   auto rescale = [&](int st) {
-    const int un = s_cols[st / SUB];
+    const int un = cols[st / SUB];
     u32x4* A = As[st % STAGES];
     float m[CA];
 #pragma unroll
@@ -260,8 +271,31 @@ __global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __r
     for (int nb = 0; nb < NB; ++nb) {
       const int o = m0 + wm * 128 + mb * 16 + 4 * (lane >> 4);
       const int t = n0 + wn * NB * 16 + nb * 16 + (lane & 15);
-      if (t < T && o < d_out) store4_bf16(Y + int64_t(t) * d_out + o, acc[mb][nb]);
+      if (t < T && o < d_out) {
+        if (part)
+          *reinterpret_cast<f32x4*>(part + (int64_t(share) * T + t) * d_out + o) = acc[mb][nb];
+        else
+          store4_bf16(Y + int64_t(t) * d_out + o, acc[mb][nb]);
+      }
     }
+}
+
+// Y = bf16(sum over shares s = 0 .. ksplit-1 of part[s]), eight outputs per thread.
+__global__ __launch_bounds__(256) void fwd_reduce_kernel(const float* __restrict__ part, int ksplit, int64_t n,
+                                                         uint16_t* __restrict__ Y) {
+  const int64_t e = (int64_t(blockIdx.x) * 256 + threadIdx.x) * 8;
+  if (e >= n) return;
+  f32x4 a = *reinterpret_cast<const f32x4*>(part + e), b = *reinterpret_cast<const f32x4*>(part + e + 4);
+  for (int s = 1; s < ksplit; ++s) {
+    a += *reinterpret_cast<const f32x4*>(part + int64_t(s) * n + e);
+    b += *reinterpret_cast<const f32x4*>(part + int64_t(s) * n + e + 4);
+  }
+  uint4 w;
+  w.x = pack_bf16x2(a[0], a[1]);
+  w.y = pack_bf16x2(a[2], a[3]);
+  w.z = pack_bf16x2(b[0], b[1]);
+  w.w = pack_bf16x2(b[2], b[3]);
+  *reinterpret_cast<uint4*>(Y + e) = w;
 }
 
 // ============================================================================ dgate
@@ -654,9 +688,15 @@ __global__ __launch_bounds__(256) void transpose_kernel(const uint16_t* __restri
   }
 
 hipError_t launch_fwd(const uint16_t* X, const uint16_t* W, const float* mask, int T, int d_in, int d_out, int g,
-                      int go, uint16_t* Y, hipStream_t s) {
+                      int go, uint16_t* Y, int ksplit, float* part, hipStream_t s) {
+  if (ksplit < 1 || (ksplit > 1 && part == nullptr)) return hipErrorInvalidValue;
   const int tiles = ((T + 255) / 256) * ((d_out + 255) / 256);
-  GM_LAUNCH_G(fwd_kernel, tiles, 64 * kFwdWaves, X, W, mask, T, d_in, d_out, Y)
+  float* p = ksplit > 1 ? part : nullptr;
+  GM_LAUNCH_G(fwd_kernel, tiles * ksplit, 64 * kFwdWaves, X, W, mask, T, d_in, d_out, Y, ksplit, p)
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || ksplit == 1) return e;
+  const int64_t n = int64_t(T) * d_out;  // a multiple of 8 (d_out is)
+  hipLaunchKernelGGL(fwd_reduce_kernel, dim3(unsigned((n / 8 + 255) / 256)), dim3(256), 0, s, part, ksplit, n, Y);
   return hipGetLastError();
 }
 

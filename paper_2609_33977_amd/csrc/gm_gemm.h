@@ -23,14 +23,18 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
   return (bid % 8) * per + bid / 8;
 }
 
-__device__ __forceinline__ void tile_coords(int nblocks, int tiles_m, int tiles_n, int& tm, int& tn) {
-  const int t = xcd_remap(blockIdx.x, nblocks);
+__device__ __forceinline__ void tile_coords(int bid, int nblocks, int tiles_m, int tiles_n, int& tm, int& tn) {
+  const int t = xcd_remap(bid, nblocks);
   const int group = t / (kGroupM * tiles_n);
   const int first_m = group * kGroupM;
   const int gm = min(tiles_m - first_m, kGroupM);
   const int r = t - group * kGroupM * tiles_n;
   tm = first_m + r % gm;
   tn = r / gm;
+}
+
+__device__ __forceinline__ void tile_coords(int nblocks, int tiles_m, int tiles_n, int& tm, int& tn) {
+  tile_coords(int(blockIdx.x), nblocks, tiles_m, tiles_n, tm, tn);
 }
 
 // Accumulator rows mb < kAgprRows<MB> live in AGPRs, the others in arch VGPRs.

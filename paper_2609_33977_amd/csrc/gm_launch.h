@@ -31,8 +31,10 @@ hipError_t launch_gemv_packed(const uint16_t* X, const uint16_t* Wp, const int* 
                               const int* rowptr, int T, int d_in, int d_out, int g, uint16_t* Y, hipStream_t s);
 int gemv_max_groups_per_row();
 
+// ksplit > 1 splits each tile's K range over that many blocks, which store fp32
+// partial tiles into part [ksplit][T][d_out]; a second kernel adds them in order.
 hipError_t launch_fwd(const uint16_t* X, const uint16_t* W, const float* mask, int T, int d_in, int d_out, int g,
-                      int go, uint16_t* Y, hipStream_t s);
+                      int go, uint16_t* Y, int ksplit, float* part, hipStream_t s);
 hipError_t launch_dgate(const uint16_t* dY, const uint16_t* X, const uint16_t* W, int T, int d_in, int d_out, int g,
                         int go, float* dgate, uint16_t* dYt, int ldt, hipStream_t s);
 hipError_t launch_transpose(const uint16_t* dY, int T, int d_out, uint16_t* dYt, int ldt, hipStream_t s);

@@ -30,7 +30,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_abi_version_and_status_strings():
-    assert gm.gm_abi_version() == 2
+    assert gm.gm_abi_version() == 3
     for s in range(7):
         assert gm.status_string(s)
     assert gm.status_string(99) == "unknown status"
@@ -61,7 +61,37 @@ def test_workspace_size_square_groups(g, nsub):
     expect = (2 * r256(NL * 4) + r256(lst * 4) + r256(lst * nsub * 4) + (r256(lst * 4) if nsub > 1 else 0)
               + r256(d_out * 1000 * 2))
     assert gm.gm_workspace_size(gm.GM_OP_BWD, T, d_in, d_out, g, g) == expect
-    assert gm.gm_workspace_size(gm.GM_OP_FWD, T, d_in, d_out, g, g) == 0
+    # 4 x 8 output tiles: the forward splits K over 8 shares
+    assert gm.gm_workspace_size(gm.GM_OP_FWD, T, d_in, d_out, g, g) == _fwd_split_bytes(T, d_in, d_out, g)
+    assert gm.gm_workspace_size(gm.GM_OP_FWD, T, d_in, d_out, g, g) == r256(8 * T * d_out * 4)
+
+
+def _fwd_split_bytes(T, d_in, d_out, g):
+    """The documented rule: at most 128 output tiles of 256 x 256 (and T > 16) split K into
+    min(256 // tiles, 8, units // 2) shares of fp32 partial tiles; units of max(g, 32) columns."""
+    if T <= 16:
+        return 0
+    tiles = -(-T // 256) * -(-d_out // 256)
+    if tiles > 128:
+        return 0
+    ks = min(256 // tiles, 8, d_in // max(g, 32) // 2)
+    return 0 if ks <= 1 else (ks * T * d_out * 4 + 255) // 256 * 256
+
+
+@pytest.mark.parametrize("T,d_in,d_out,g,expect", [
+    (4096, 4096, 4096, 256, 0),                       # 256 tiles: unsplit
+    (16, 5120, 5120, 256, 0),                         # decode path
+    (512, 5120, 5120, 256, 6 * 512 * 5120 * 4),       # 40 tiles: 6 shares
+    (512, 5120, 13824, 256, 2 * 512 * 13824 * 4),     # 108 tiles: 2 shares
+    (512, 13824, 5120, 256, 6 * 512 * 5120 * 4),
+    (2048, 4096, 4096, 256, 2 * 2048 * 4096 * 4),     # 128 tiles: 2 shares
+    (2048, 4096, 4352, 256, 0),                       # 136 tiles: unsplit
+    (17, 4096, 4096, 256, 8 * 17 * 4096 * 4),         # 16 tiles, 16 units: 8 shares
+    (300, 1024, 1024, 512, 0),                        # two units: a share would hold one
+    (300, 2048, 1024, 512, 2 * 300 * 1024 * 4),
+])
+def test_forward_split_workspace(T, d_in, d_out, g, expect):
+    assert gm.gm_workspace_size(gm.GM_OP_FWD, T, d_in, d_out, g) == expect == _fwd_split_bytes(T, d_in, d_out, g)
 
 
 @pytest.mark.parametrize("args,code", [
@@ -171,6 +201,11 @@ def test_linear_argument_errors():
     assert fwd(FAKE, FAKE, FAKE, 16, 256, 264, 16, 16, FAKE, None, 0, None) == gm.GM_ERR_SHAPE
     assert fwd(FAKE, MISALIGNED, FAKE, 16, 256, 256, 256, 1, FAKE, None, 0, None) == gm.GM_ERR_ALIGN
     assert fwd(FAKE, FAKE, MISALIGNED, 16, 256, 256, 32, 32, FAKE, None, 0, None) == gm.GM_ERR_ALIGN
+    # a workspace, when given, must be aligned and at least the split size
+    need = gm.gm_workspace_size(gm.GM_OP_FWD, 512, 1024, 1024, 256)
+    assert need > 0
+    assert fwd(FAKE, FAKE, FAKE, 512, 1024, 1024, 256, 1, FAKE, FAKE, need - 1, None) == gm.GM_ERR_WORKSPACE
+    assert fwd(FAKE, FAKE, FAKE, 512, 1024, 1024, 256, 1, FAKE, MISALIGNED, need, None) == gm.GM_ERR_ALIGN
 
     bwd = L.gm_masked_linear_bwd
     # dX requested without a mask
