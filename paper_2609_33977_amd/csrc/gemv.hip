@@ -147,30 +147,32 @@ __global__ __launch_bounds__(256) void gemv_kernel(const uint16_t* __restrict__ 
 // ---------------------------------------------------------------- 2..16 tokens
 
 // For a batch of 2..16 tokens the one-wave-per-row kernel re-reads X for
-// every row.  This variant computes 16 output rows per block with
+// every row.  This variant computes 16 RT output rows per block with
 // v_mfma_f32_16x16x32_bf16 (M = rows, N = tokens padded to 16, K = 32 input
-// columns per instruction), so a 16-byte chunk of X feeds 16 rows.  The eight
-// waves of the block split the input columns and sum their 16 x 16 partial
-// tiles in LDS in wave order.  The mask rows of the block are staged in LDS
-// first; a lane reads a W chunk only when its group is kept (pruned chunks
-// are zeros), so HBM traffic is the kept weights, as in the GEMV.
+// columns per instruction): a 16-byte chunk of X feeds the RT row tiles of 16
+// rows, so X is read from L2 once per 16 RT rows instead of once per row.  The
+// eight waves of the block split the input columns and sum their partial tiles
+// in LDS in wave order.  The mask rows of the block are staged in LDS first; a
+// lane reads a W chunk only when its group is kept (pruned chunks are zeros),
+// so HBM traffic is the kept weights, as in the GEMV.
 constexpr int kMmaWaves = 8;
-constexpr int kMmaMaskFloats = 8192;  // 16 mask rows of up to 512 selectors, or one of up to 1024
+constexpr int kMmaMaskFloats = 8192;  // staged mask floats per block: mask rows of the block x selectors per row
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
+template <int RT>
 __global__ __launch_bounds__(64 * kMmaWaves) void gemv_mfma_kernel(const uint16_t* __restrict__ X,
                                                                   const uint16_t* __restrict__ W,
                                                                   const float* __restrict__ mask, int T, int d_in,
                                                                   int d_out, int g, int go,
                                                                   uint16_t* __restrict__ Y) {
+  constexpr int R = 16 * RT;
   __shared__ float s_m[kMmaMaskFloats];
-  __shared__ f32x4 s_part[kMmaWaves][64];
+  __shared__ f32x4 s_part[kMmaWaves][RT][64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int o0 = blockIdx.x * 16;
+  const int o0 = blockIdx.x * R;
   const int G_in = d_in / g;
-  // mask rows of the block: 16 (1 x g groups) or the one shared by all 16 rows (g_out >= 16)
-  const int mrows = go == 1 ? 16 : 1;
+  const int mrows = go == 1 ? R : (R > go ? R / go : 1);
   const int u0 = o0 / go;
   const int G_out = (d_out + go - 1) / go;
   for (int e = tid; e < mrows * G_in; e += 64 * kMmaWaves) {
@@ -179,43 +181,57 @@ __global__ __launch_bounds__(64 * kMmaWaves) void gemv_mfma_kernel(const uint16_
   }
   __syncthreads();
 
-  const int r = lane & 15, kc = lane >> 4;  // A: row o0 + r; B: token r; both the k chunk kc of a slice
-  const int o = o0 + r;
-  const bool orow = o < d_out;
-  const float* mrow = s_m + (go == 1 ? r : 0) * G_in;
-  const uint16_t* wrow = W + int64_t(orow ? o : 0) * d_in + 8 * kc;
+  const int r = lane & 15, kc = lane >> 4;
+  const float* mrow[RT];
+  const uint16_t* wrow[RT];
+  bool orow[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    const int o = o0 + rt * 16 + r;
+    orow[rt] = o < d_out;
+    mrow[rt] = s_m + (go == 1 ? rt * 16 + r : (o0 + rt * 16) / go - u0) * G_in;
+    wrow[rt] = W + int64_t(orow[rt] ? o : 0) * d_in + 8 * kc;
+  }
   const bool tok = r < T;
   const uint16_t* xrow = X + int64_t(tok ? r : 0) * d_in + 8 * kc;
   const int nsl = d_in / 32;
   const int s0 = wave * nsl / kMmaWaves, s1 = (wave + 1) * nsl / kMmaWaves;
-  f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-  constexpr int U = 4;  // slices whose loads are issued together
+  f32x4 acc[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) acc[rt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  constexpr int U = 4;
   for (int sb = s0; sb < s1; sb += U) {
-    u32x4 a[U], b[U];
-    float m[U];
+    u32x4 av[RT][U], bv[U];
+    float m[RT][U];
 #pragma unroll
     for (int q = 0; q < U; ++q) {
       const int k = (sb + q) * 32;
       const bool live = sb + q < s1;
-      m[q] = live && orow ? mrow[(k + 8 * kc) / g] : 0.0f;
-      a[q] = m[q] != 0.0f ? ld16(wrow + k) : zero16();
-      b[q] = live && tok ? ld16(xrow + k) : zero16();
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        m[rt][q] = live && orow[rt] ? mrow[rt][(k + 8 * kc) / g] : 0.0f;
+        av[rt][q] = m[rt][q] != 0.0f ? ld16(wrow[rt] + k) : zero16();
+      }
+      bv[q] = live && tok ? ld16(xrow + k) : zero16();
     }
 #pragma unroll
-    for (int q = 0; q < U; ++q) {
-      const u32x4 aq = (m[q] != 0.0f && m[q] != 1.0f) ? scale_bf16x8(a[q], m[q]) : a[q];
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, aq), __builtin_bit_cast(bf16x8, b[q]),
-                                                    acc, 0, 0, 0);
-    }
+    for (int q = 0; q < U; ++q)
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        const u32x4 aq = (m[rt][q] != 0.0f && m[rt][q] != 1.0f) ? scale_bf16x8(av[rt][q], m[rt][q]) : av[rt][q];
+        acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, aq),
+                                                          __builtin_bit_cast(bf16x8, bv[q]), acc[rt], 0, 0, 0);
+      }
   }
-  s_part[wave][lane] = acc;
-  __syncthreads();
-  if (wave == 0) {
-    f32x4 sum = s_part[0][lane];
 #pragma unroll
-    for (int w = 1; w < kMmaWaves; ++w) sum += s_part[w][lane];
-    // lane (kc, r) holds rows o0 + 4 kc .. + 3 of token r
-    const int ob = o0 + 4 * kc;
+  for (int rt = 0; rt < RT; ++rt) s_part[wave][rt][lane] = acc[rt];
+  __syncthreads();
+  if (wave < RT) {
+    const int rt = wave;
+    f32x4 sum = s_part[0][rt][lane];
+#pragma unroll
+    for (int w = 1; w < kMmaWaves; ++w) sum += s_part[w][rt][lane];
+    const int ob = o0 + rt * 16 + 4 * kc;
     if (r < T && ob < d_out) {
       uint2 v;
       v.x = pack_bf16x2(sum[0], sum[1]);
@@ -252,10 +268,23 @@ static hipError_t gemv_passes(const uint16_t* X, const uint16_t* W, const float*
 
 hipError_t launch_gemv_inplace(const uint16_t* X, const uint16_t* W, const float* mask, int T, int d_in, int d_out,
                                int g, int go, uint16_t* Y, hipStream_t s) {
-  if (T >= 2 && T <= 16 && (go == 1 ? 16 * (d_in / g) : d_in / g) <= kMmaMaskFloats) {
-    hipLaunchKernelGGL(gemv_mfma_kernel, dim3(unsigned((d_out + 15) / 16)), dim3(64 * kMmaWaves), 0, s, X, W, mask, T,
-                       d_in, d_out, g, go, Y);
-    return hipGetLastError();
+  if (T >= 2 && T <= 16) {
+    // four row tiles while that still gives 192 blocks or more, else two; fewer
+    // when the block's mask rows do not fit in LDS
+    const int G_in = d_in / g;
+    auto fits = [&](int R) { return (go == 1 ? R : (R > go ? R / go : 1)) * G_in <= kMmaMaskFloats; };
+    int rt = (d_out + 63) / 64 >= 192 ? 4 : 2;
+    while (rt > 1 && !fits(16 * rt)) rt /= 2;
+    if (fits(16 * rt)) {
+      const dim3 grid(unsigned((d_out + 16 * rt - 1) / (16 * rt))), block(64 * kMmaWaves);
+      if (rt == 4)
+        hipLaunchKernelGGL(gemv_mfma_kernel<4>, grid, block, 0, s, X, W, mask, T, d_in, d_out, g, go, Y);
+      else if (rt == 2)
+        hipLaunchKernelGGL(gemv_mfma_kernel<2>, grid, block, 0, s, X, W, mask, T, d_in, d_out, g, go, Y);
+      else
+        hipLaunchKernelGGL(gemv_mfma_kernel<1>, grid, block, 0, s, X, W, mask, T, d_in, d_out, g, go, Y);
+      return hipGetLastError();
+    }
   }
   if (d_in / g <= 512)
     return gemv_passes<false, 512>(X, W, mask, nullptr, nullptr, nullptr, nullptr, T, d_in, d_out, g, go, Y, s);

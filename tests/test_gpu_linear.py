@@ -139,6 +139,23 @@ def test_decode_forward(T, g):
     assert_close("Y", host_f64_from_bf16(Y), Yr)
 
 
+@pytest.mark.parametrize("T,d_out,g_out", [(8, 12296, 1), (16, 12296, 1), (5, 12304, 16), (12, 12416, 64)])
+def test_decode_four_row_tiles(T, d_out, g_out):
+    # d_out / 64 >= 192 blocks: the MFMA decode path takes four 16-row tiles per
+    # block; the last block holds 8, 16 or all 64 of its rows
+    d_in = 1024
+    g = 256 if g_out == 1 else g_out
+    say(f"decode, four row tiles: T={T} d_out={d_out} groups {g_out}x{g}")
+    case = workloads.make_linear_case((212, T, d_out, g_out), T, d_in, d_out, g, None, g_out=g_out)
+    d = _dev_case(case)
+    import paper_2609_33977_amd as gm
+    Y = empty_bf16(T, d_out)
+    gm.gm_masked_linear_fwd(d["X"], d["W"], d["mask"], g, Y, g_out=g_out)
+    sync()
+    Yr = oracle.linear_fwd(oracle.from_bf16(case.X), oracle.from_bf16(case.W), case.mask, g, g_out)
+    assert_close("Y", host_f64_from_bf16(Y), Yr)
+
+
 def _pack(d, g):
     import torch
     import paper_2609_33977_amd as gm
