@@ -154,7 +154,8 @@ __global__ __launch_bounds__(256) void gemv_kernel(const uint16_t* __restrict__ 
 // eight waves of the block split the input columns and sum their partial tiles
 // in LDS in wave order.  The mask rows of the block are staged in LDS first; a
 // lane reads a W chunk only when its group is kept (pruned chunks are zeros),
-// so HBM traffic is the kept weights, as in the GEMV.
+// so HBM traffic is the kept weights, as in the GEMV; the weights are loaded
+// nontemporal (each is read once).
 constexpr int kMmaWaves = 8;
 constexpr int kMmaMaskFloats = 8192;  // staged mask floats per block: mask rows of the block x selectors per row
 
@@ -210,7 +211,7 @@ __global__ __launch_bounds__(64 * kMmaWaves) void gemv_mfma_kernel(const uint16_
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) {
         m[rt][q] = live && orow[rt] ? mrow[rt][(k + 8 * kc) / g] : 0.0f;
-        av[rt][q] = m[rt][q] != 0.0f ? ld16(wrow[rt] + k) : zero16();
+        av[rt][q] = m[rt][q] != 0.0f ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wrow[rt] + k)) : zero16();
       }
       bv[q] = live && tok ? ld16(xrow + k) : zero16();
     }
@@ -239,6 +240,102 @@ __global__ __launch_bounds__(64 * kMmaWaves) void gemv_mfma_kernel(const uint16_
       *reinterpret_cast<uint2*>(Y + int64_t(r) * d_out + ob) = v;
     }
   }
+}
+
+// ---------------------------------------------------------------- one token
+
+// One token: one wave per output row.  The lane's groups of the row are the
+// kept groups with index k = slot, slot + gps, slot + 2 gps, ... in column
+// order, and the weight loads of up to kT1Steps such steps (512 bytes per
+// lane when the row has enough kept groups) are issued together.  In place
+// (rows of at most 64 groups), the lanes read the row's selectors at once and
+// compact the kept ones into a per-wave LDS list (column, selector) by rank;
+// packed, the row's pieces are contiguous from rowptr[o] with their column in
+// chunk[] and selector in scale[].  Weights are streamed once, so they are
+// loaded nontemporal (they would only evict the input vector and the
+// selectors from the caches); X is read through the caches (every row reuses
+// it).  Both layouts accumulate the same products in the same order, and the
+// row sum is a fixed-order 64-lane reduction, so their results are identical.
+constexpr int kT1Steps = 8;
+
+template <bool PACKED>
+__global__ __launch_bounds__(256) void gemv_t1_kernel(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
+                                                      const float* __restrict__ mask,
+                                                      const uint16_t* __restrict__ Wp, const int* __restrict__ chunk,
+                                                      const float* __restrict__ scale,
+                                                      const int* __restrict__ rowptr, int d_in, int d_out, int g,
+                                                      int go, uint16_t* __restrict__ Y) {
+  __shared__ int s_v[4][PACKED ? 1 : 64];
+  __shared__ float s_m[4][PACKED ? 1 : 64];
+  const int lane = threadIdx.x & 63;
+  const int wv = threadIdx.x >> 6;
+  const int o = int(blockIdx.x) * 4 + wv;
+  if (o >= d_out) return;  // whole wave leaves together; no block barrier below
+  const int G_in = d_in / g;  // at most 64 in place
+  const int lpg = g >> 3;     // lanes per group (16 bytes each)
+  const int gps = 64 / lpg;   // groups per step
+  const int slot = lane / lpg;
+  const int e = (lane % lpg) * 8;
+  int nk;
+  int64_t pb = 0;
+  if constexpr (PACKED) {
+    pb = rowptr[o];
+    nk = rowptr[o + 1] - int(pb);
+  } else {
+    const float mv = lane < G_in ? mask[int64_t(o / go) * G_in + lane] : 0.0f;
+    const uint64_t bits = __ballot(mv != 0.0f);
+    nk = __popcll(bits);
+    if (mv != 0.0f) {
+      const int r = __builtin_amdgcn_mbcnt_hi(uint32_t(bits >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(bits), 0u));
+      s_v[wv][r] = lane;
+      s_m[wv][r] = mv;
+    }
+    // LDS writes of this wave become visible to its other lanes before the list is read.
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+  const uint16_t* wrow = PACKED ? Wp + pb * g + e : W + int64_t(o) * d_in + e;
+  float acc = 0.0f;
+  for (int k0 = 0; k0 < nk; k0 += kT1Steps * gps) {
+    u32x4 w[kT1Steps], x[kT1Steps];
+    float m[kT1Steps];
+#pragma unroll
+    for (int c = 0; c < kT1Steps; ++c) {
+      const int k = k0 + c * gps + slot;
+      const bool live = k < nk;
+      int v = 0;
+      m[c] = 0.0f;
+      w[c] = zero16();
+      x[c] = zero16();
+      if (live) {
+        if constexpr (PACKED) {
+          v = chunk[pb + k];
+          m[c] = scale[pb + k];
+          w[c] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wrow + int64_t(k) * g));
+        } else {
+          v = s_v[wv][k];
+          m[c] = s_m[wv][k];
+          w[c] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wrow + v * g));
+        }
+        x[c] = ld16(X + v * g + e);
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < kT1Steps; ++c) acc += m[c] * dot8_bf16(w[c], x[c]);
+  }
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) acc += __shfl_xor(acc, d);
+  if (lane == 0) Y[o] = uint16_t(f32_to_bf16_bits(acc));
+}
+
+template <bool PACKED>
+static hipError_t launch_t1(const uint16_t* X, const uint16_t* W, const float* mask, const uint16_t* Wp,
+                            const int* chunk, const float* scale, const int* rowptr, int d_in, int d_out, int g,
+                            int go, uint16_t* Y, hipStream_t s) {
+  hipLaunchKernelGGL(gemv_t1_kernel<PACKED>, dim3(unsigned((d_out + 3) / 4)), dim3(256), 0, s, X, W, mask, Wp, chunk,
+                     scale, rowptr, d_in, d_out, g, go, Y);
+  return hipGetLastError();
 }
 
 template <bool PACKED, int MAXG>
@@ -286,6 +383,8 @@ hipError_t launch_gemv_inplace(const uint16_t* X, const uint16_t* W, const float
       return hipGetLastError();
     }
   }
+  if (T == 1 && d_in / g <= 64)
+    return launch_t1<false>(X, W, mask, nullptr, nullptr, nullptr, nullptr, d_in, d_out, g, go, Y, s);
   if (d_in / g <= 512)
     return gemv_passes<false, 512>(X, W, mask, nullptr, nullptr, nullptr, nullptr, T, d_in, d_out, g, go, Y, s);
   return gemv_passes<false, kMaxGroupsPerRow>(X, W, mask, nullptr, nullptr, nullptr, nullptr, T, d_in, d_out, g, go,
@@ -294,6 +393,7 @@ hipError_t launch_gemv_inplace(const uint16_t* X, const uint16_t* W, const float
 
 hipError_t launch_gemv_packed(const uint16_t* X, const uint16_t* Wp, const int* chunk, const float* scale,
                               const int* rowptr, int T, int d_in, int d_out, int g, uint16_t* Y, hipStream_t s) {
+  if (T == 1) return launch_t1<true>(X, nullptr, nullptr, Wp, chunk, scale, rowptr, d_in, d_out, g, 1, Y, s);
   return gemv_passes<true, 1>(X, nullptr, nullptr, Wp, chunk, scale, rowptr, T, d_in, d_out, g, 1, Y, s);
 }
 
