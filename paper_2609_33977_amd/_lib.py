@@ -33,7 +33,7 @@ class GroupMaskError(RuntimeError):
 
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is missing: build it first (python -m paper_2609_33977_amd.build)")
+        raise ImportError(f"{LIB_PATH} is missing: build it first (python paper_2609_33977_amd/build.py)")
     # torch carries its own copy of the HIP runtime and names it without the
     # version suffix, so the dynamic linker would load the system copy for
     # this library if it came first; a second runtime in the process sees no

@@ -1,6 +1,6 @@
 """Build libgroupmask.so (gfx950 HIP kernels + C-ABI layer) in-tree with hipcc.
 
-Usage: python -m paper_2609_33977_amd.build   (or build() from Python)
+Usage: python paper_2609_33977_amd/build.py   (or build() from Python)
 """
 from __future__ import annotations
 
