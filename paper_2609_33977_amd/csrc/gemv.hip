@@ -154,8 +154,10 @@ __global__ __launch_bounds__(256) void gemv_kernel(const uint16_t* __restrict__ 
 // eight waves of the block split the input columns and sum their partial tiles
 // in LDS in wave order.  The mask rows of the block are staged in LDS first; a
 // lane reads a W chunk only when its group is kept (pruned chunks are zeros),
-// so HBM traffic is the kept weights, as in the GEMV; the weights are loaded
-// nontemporal (each is read once).
+// so HBM traffic is the kept weights, as in the GEMV.  The weights go through
+// the caches: a lane reads 64 bytes of each of 16 rows per instruction, and the
+// other half of each 128-byte line comes with the next slice (nontemporal
+// loads measured 3-8 % slower here).
 constexpr int kMmaWaves = 8;
 constexpr int kMmaMaskFloats = 8192;  // staged mask floats per block: mask rows of the block x selectors per row
 
@@ -211,7 +213,7 @@ __global__ __launch_bounds__(64 * kMmaWaves) void gemv_mfma_kernel(const uint16_
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) {
         m[rt][q] = live && orow[rt] ? mrow[rt][(k + 8 * kc) / g] : 0.0f;
-        av[rt][q] = m[rt][q] != 0.0f ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wrow[rt] + k)) : zero16();
+        av[rt][q] = m[rt][q] != 0.0f ? ld16(wrow[rt] + k) : zero16();
       }
       bv[q] = live && tok ? ld16(xrow + k) : zero16();
     }
