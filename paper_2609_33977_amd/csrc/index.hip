@@ -18,51 +18,80 @@
 
 namespace gm {
 
-// One 1024-thread block per list column c; scans the rows in blocks of 1024
-// and compacts the kept ones with a wave ballot plus a 16-entry LDS prefix.
+// One 1024-thread block per list column c.  The rows go in chunks of 4096:
+// thread t owns rows 4t .. 4t + 3 of the chunk and loads all of their
+// selectors before any of them is used (one memory round trip per chunk, not
+// one per 1024 rows), counts its kept rows, and finds where they go with a
+// block-wide exclusive scan of the counts (a shuffle scan inside each wave,
+// then the 16 wave totals in LDS).  Rows stay in increasing order.
+constexpr int kListRowsPerThread = 4;
+
 __global__ __launch_bounds__(1024) void col_lists_kernel(const float* __restrict__ mask, int d_out, int G_in,
                                                         int go, int nsub, int* __restrict__ colcount,
                                                         int* __restrict__ colsoft, int* __restrict__ rows,
                                                         float* __restrict__ scales, int* __restrict__ subbits) {
+  constexpr int R = kListRowsPerThread;
   const int c = blockIdx.x;
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
-  __shared__ int wave_cnt[16];
+  __shared__ int wave_tot[16];
   __shared__ int s_soft;
   if (threadIdx.x == 0) s_soft = 0;
-  __syncthreads();
+  bool soft = false;
   int base = 0;
-  for (int o0 = 0; o0 < d_out; o0 += 1024) {
-    const int o = o0 + threadIdx.x;
-    float m[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-    int bits = 0;
-    bool soft = false;
+  for (int o0 = 0; o0 < d_out; o0 += 1024 * R) {
+    const int ob = o0 + int(threadIdx.x) * R;
+    float m[R][4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (q < nsub && o < d_out) {
-        m[q] = mask[int64_t(o / go) * G_in + c * nsub + q];
-        bits |= int(m[q] != 0.0f) << q;
-        soft |= m[q] != 0.0f && m[q] != 1.0f;
-      }
-    const bool keep = bits != 0;
-    const uint64_t bal = __ballot(keep);
-    const int rank = __popcll(bal & ((uint64_t(1) << lane) - 1));
-    if (lane == 0) wave_cnt[w] = __popcll(bal);
-    __syncthreads();
-    int off = base;
-    for (int q = 0; q < w; ++q) off += wave_cnt[q];
-    if (keep) {
-      const int64_t e = int64_t(c) * d_out + off + rank;
-      rows[e] = o;
+    for (int r = 0; r < R; ++r)
 #pragma unroll
       for (int q = 0; q < 4; ++q)
-        if (q < nsub) scales[e * nsub + q] = m[q];
-      if (nsub > 1) subbits[e] = bits;
-      if (soft) s_soft = 1;
+        m[r][q] = (q < nsub && ob + r < d_out) ? mask[int64_t((ob + r) / go) * G_in + c * nsub + q] : 0.0f;
+    int bits[R];
+    int cnt = 0;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      bits[r] = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        bits[r] |= int(m[r][q] != 0.0f) << q;
+        soft |= m[r][q] != 0.0f && m[r][q] != 1.0f;
+      }
+      cnt += bits[r] != 0;
     }
-    for (int q = 0; q < 16; ++q) base += wave_cnt[q];
+    // inclusive scan of the counts within the wave
+    int inc = cnt;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int up = __shfl_up(inc, d);
+      if (lane >= d) inc += up;
+    }
+    if (lane == 63) wave_tot[w] = inc;
     __syncthreads();
+    int off = base + inc - cnt;
+    int chunk_total = 0;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int t = wave_tot[q];
+      if (q < w) off += t;
+      chunk_total += t;
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+      if (bits[r]) {
+        const int64_t e = int64_t(c) * d_out + off;
+        rows[e] = ob + r;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (q < nsub) scales[e * nsub + q] = m[r][q];
+        if (nsub > 1) subbits[e] = bits[r];
+        ++off;
+      }
+    base += chunk_total;
+    __syncthreads();  // wave_tot is rewritten by the next chunk
   }
+  if (soft) s_soft = 1;
+  __syncthreads();
   if (threadIdx.x == 0) {
     colcount[c] = base;
     colsoft[c] = s_soft;
