@@ -197,6 +197,7 @@ __global__ __launch_bounds__(64 * kMmaWaves) void gemv_mfma_kernel(const uint16_
   }
   const bool tok = r < T;
   const uint16_t* xrow = X + int64_t(tok ? r : 0) * d_in + 8 * kc;
+  const int lg = __builtin_ctz(unsigned(g));  // g is a power of two: the group of a column by shift
   const int nsl = d_in / 32;
   const int s0 = wave * nsl / kMmaWaves, s1 = (wave + 1) * nsl / kMmaWaves;
   f32x4 acc[RT];
@@ -212,7 +213,7 @@ __global__ __launch_bounds__(64 * kMmaWaves) void gemv_mfma_kernel(const uint16_
       const bool live = sb + q < s1;
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) {
-        m[rt][q] = live && orow[rt] ? mrow[rt][(k + 8 * kc) / g] : 0.0f;
+        m[rt][q] = live && orow[rt] ? mrow[rt][(k + 8 * kc) >> lg] : 0.0f;
         av[rt][q] = m[rt][q] != 0.0f ? ld16(wrow[rt] + k) : zero16();
       }
       bv[q] = live && tok ? ld16(xrow + k) : zero16();
