@@ -250,3 +250,50 @@ def test_decode_and_gemm_paths_agree_at_the_boundary():
     Y17 = host_f64_from_bf16(_fwd(d17, g))[:16]
     Y16 = host_f64_from_bf16(_fwd(d16, g))
     assert_close("Y (GEMV vs GEMM)", Y16, Y17, 1e-2)
+
+
+@pytest.mark.parametrize("T", [1, 5, 16])
+@pytest.mark.parametrize("g", [64, 256])
+def test_decode_soft_selectors_in_place_and_packed(T, g):
+    # fractional selectors (a group scaled by its mask value, skipped at 0) on
+    # the decode paths: the one-token kernel (in place and packed) and the
+    # 2-16 token MFMA kernel (in place), against the oracle
+    d_in, d_out = 4096, 136
+    say(f"decode soft selectors: T={T} g={g}")
+    case = workloads.make_linear_case((213, T, g), T, d_in, d_out, g, None)
+    r = workloads.gen.rng_for(214, T, g)
+    soft = r.uniform(0.05, 1.5, size=case.mask.shape).astype(np.float32)
+    soft[r.uniform(size=soft.shape) < 0.4] = 0.0
+    d = _dev_case(case, soft)
+    Yr, _, _ = _oracle_all(case, soft)
+    assert_close("Y in place", host_f64_from_bf16(_fwd(d, g)), Yr)
+    import paper_2609_33977_amd as gm
+    Wp, chunk, scale, rowptr = _pack(d, g)
+    Yp = empty_bf16(T, d_out)
+    gm.gm_packed_linear_fwd(d["X"], Wp, chunk, scale, rowptr, d_out, g, Yp)
+    sync()
+    assert_close("Y packed", host_f64_from_bf16(Yp), Yr)
+
+
+@pytest.mark.parametrize("T", [1, 8])
+def test_decode_degenerate_rows(T):
+    # rows with every group kept (64 groups: the one-token kernel's longest
+    # in-place list), rows with none (exact zero outputs), rows with a single
+    # kept group (first, last), and an all-zero mask
+    d_in, d_out, g = 4096, 64, 64
+    say(f"decode degenerate rows: T={T}")
+    case = workloads.make_linear_case((215, T), T, d_in, d_out, g, None)
+    m = case.mask.copy()
+    m[0:8] = 1.0
+    m[8:16] = 0.0
+    m[16:24] = 0.0
+    m[16:20, 0] = 1.0
+    m[20:24, d_in // g - 1] = 1.0
+    d = _dev_case(case, m)
+    Y = _fwd(d, g)
+    Yr, _, _ = _oracle_all(case, m)
+    assert_close("Y", host_f64_from_bf16(Y), Yr)
+    assert not np.any(host_bits(Y)[:, 8:16] & 0x7FFF), "pruned rows must be exactly zero"
+    zeros = np.zeros_like(m)
+    Yz = _fwd(_dev_case(case, zeros), g)
+    assert not np.any(host_bits(Yz) & 0x7FFF)
