@@ -1,4 +1,4 @@
-"""GPU parity at the largest matrix the library accepts: every GEMM addresses
+"""GPU parity at the largest sizes the library accepts: every GEMM addresses
 a matrix with 32-bit byte offsets, so W may hold at most 2^30 - 2^22 bf16
 elements (just under 2 GiB); W [32640, 32768] is exactly that.  The forward
 (GEMM and decode paths, in place and packed), dX and dgate are checked against
@@ -117,3 +117,48 @@ def test_one_row_past_the_limit_is_rejected():
     st = gm.LIB.gm_masked_linear_fwd(X.data_ptr(), W.data_ptr(), m.data_ptr(), 1, D_IN, D_OUT + 8, G, 1,
                                      Y.data_ptr(), None, 0, None)
     assert st == gm.GM_ERR_SHAPE
+
+
+def test_longest_token_batch_forward_and_backward():
+    # the token dimension at the same limit: X and dX [32640, 32768] hold
+    # 2^30 - 2^22 elements each (T a multiple of 8, so the padded dY^T rows
+    # of the backward stay inside the limit too); a narrow W keeps the
+    # products small.  Sampled tokens for Y and dX, sampled groups for dgate.
+    import torch
+    import paper_2609_33977_amd as gm
+    T, d_in, d_out, g = 32640, 32768, 256, 256
+    say(f"longest token batch: X [{T}, {d_in}], W [{d_out}, {d_in}]")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(workloads.SEED + 501)
+    X = torch.empty(T, d_in, dtype=torch.bfloat16, device="cuda")
+    for r0 in range(0, T, 4096):
+        r1 = min(T, r0 + 4096)
+        X[r0:r1] = torch.randn(r1 - r0, d_in, device="cuda", generator=gen).to(torch.bfloat16)
+    W = (torch.randn(d_out, d_in, device="cuda", generator=gen) * 0.02).to(torch.bfloat16)
+    dY = torch.randn(T, d_out, device="cuda", generator=gen).to(torch.bfloat16)
+    Gn = d_out * (d_in // g)
+    m = torch.zeros(Gn, device="cuda")
+    m[torch.randperm(Gn, device="cuda", generator=gen)[: Gn // 2]] = 1.0
+    m = m.view(d_out, d_in // g)
+    Y = empty_bf16(T, d_out)
+    gm.gm_masked_linear_fwd(X, W, m, g, Y, workspace(gm.gm_workspace_size(gm.GM_OP_FWD, T, d_in, d_out, g)))
+    dX = empty_bf16(T, d_in)
+    dgate = empty_f32(d_out, d_in // g)
+    gm.gm_masked_linear_bwd(dY, X, W, m, g, dX, dgate, workspace(gm.gm_workspace_size(gm.GM_OP_BWD, T, d_in, d_out, g)))
+    sync()
+    Wo, mo = oracle.from_bf16(host_bits(W)), m.cpu().numpy()
+    toks = np.sort(rng_for(501, 1).choice(T, 48, replace=False))
+    toks[-1] = T - 1  # the last token touches the end of X's and dX's addressable range
+    idx = torch.as_tensor(toks, device="cuda")
+    Xs, dYs = oracle.from_bf16(host_bits(X[idx])), oracle.from_bf16(host_bits(dY[idx]))
+    assert_close("Y (sampled tokens)", oracle.from_bf16(host_bits(Y[idx])), oracle.linear_fwd(Xs, Wo, mo, g))
+    dX_ref, _ = oracle.linear_bwd(dYs, Xs, Wo, mo, g)
+    assert_close("dX (sampled tokens)", oracle.from_bf16(host_bits(dX[idx])), dX_ref)
+    dYo = oracle.from_bf16(host_bits(dY))
+    for v in (0, d_in // g - 1):  # every token, two group columns (all rows of W)
+        cols = slice(v * g, (v + 1) * g)
+        Xc = oracle.from_bf16(host_bits(X[:, cols].contiguous()))
+        _, dg_ref = oracle.linear_bwd(dYo, Xc, Wo[:, cols], mo[:, v: v + 1], g)
+        assert_close(f"dgate (group column {v})", dgate.cpu().numpy()[:, v: v + 1], dg_ref)
+    del X, dX
+    torch.cuda.empty_cache()
