@@ -618,6 +618,37 @@ def _gemv_bandwidth(n_layers, reps):
         del graph
     out.update({"GB/s": total / (best / 1e3) / 1e9, "frac_of_peak": total / (best / 1e3) / 1e9 / PEAK_HBM_GBS,
                 "ms_per_pass": best, "schedule": best_name})
+    # The group-compacted export (App. F) of the stacked layout: each row's kept
+    # pieces contiguous, with their column and selector (8 bytes per piece) and
+    # a row pointer instead of the dense selector array.  Same kept weights;
+    # outputs checked bit for bit against the in-place stacked launches.
+    packed, packed_bytes = [], 0
+    for mats in fused:
+        for X1, W, m, Y in mats:
+            d_o, d_i = W.shape
+            cap = int((m != 0).sum().item())
+            Wp = torch.empty(cap, g, dtype=torch.bfloat16, device="cuda")
+            chunk = torch.empty(cap, dtype=torch.int32, device="cuda")
+            scale = torch.empty(cap, dtype=torch.float32, device="cuda")
+            rowptr = torch.empty(d_o + 1, dtype=torch.int32, device="cuda")
+            gm.gm_pack_rows(W, m, g, cap, Wp, chunk, scale, rowptr)
+            packed.append((X1, Wp, chunk, scale, rowptr, d_o, torch.empty_like(Y), Y))
+            packed_bytes += cap * (2 * g + 8) + 4 * (d_o + 1) + 2 * (d_i + d_o)
+
+    def serial_packed():
+        for X1, Wp, chunk, scale, rowptr, d_o, Yp, _ in packed:
+            gm.gm_packed_linear_fwd(X1, Wp, chunk, scale, rowptr, d_o, g, Yp)
+
+    serial_fused()
+    serial_packed()
+    torch.cuda.synchronize()
+    if all(torch.equal(Yp, Y) for *_, Yp, Y in packed):
+        t = _events_ms(serial_packed, reps)
+        out["packed_stacked"] = {"bytes_per_pass": packed_bytes, "GB/s": packed_bytes / (t / 1e3) / 1e9,
+                                 "frac_of_peak": packed_bytes / (t / 1e3) / 1e9 / PEAK_HBM_GBS, "ms_per_pass": t}
+    else:
+        out["packed_stacked"] = None
+    del packed
     # 8 and 16 tokens over the same weights and masks, seven launches per layer (eager)
     for T in (8, 16):
         xs, ys, extra = {}, [], 0

@@ -253,16 +253,35 @@ __global__ __launch_bounds__(64 * kMmaWaves) void gemv_mfma_kernel(const uint16_
 // each) are issued together.  Four steps keep the kernel at 62 registers, so
 // eight waves per SIMD are resident: on the LLaMA-2-13B projections that
 // streams 8 % faster than eight steps per chunk at four waves per SIMD (more
-// rows in flight beats more loads per row).  In place
-// (rows of at most 64 groups), the lanes read the row's selectors at once and
-// compact the kept ones into a per-wave LDS list (column, selector) by rank;
-// packed, the row's pieces are contiguous from rowptr[o] with their column in
-// chunk[] and selector in scale[].  Weights are streamed once, so they are
-// loaded nontemporal (they would only evict the input vector and the
-// selectors from the caches); X is read through the caches (every row reuses
-// it).  Both layouts accumulate the same products in the same order, and the
-// row sum is a fixed-order 64-lane reduction, so their results are identical.
+// rows in flight beats more loads per row).  In place (rows of at most 64
+// groups), the lanes read the row's selectors at once and compact the kept
+// ones into a per-wave LDS list (column, selector) by rank; the weight and
+// input loads of a step then go out together.  Packed, the row's pieces are
+// contiguous from rowptr[o] with their column in chunk[] and selector in
+// scale[]: the piece addresses need only the row pointer, so a chunk's weight
+// loads are issued before its (column, selector) list arrives, through buffer
+// loads whose out-of-range offsets read zeros (no branches, so the compiler
+// can wait for the list without waiting for the weights).  Weights are
+// streamed once, so they are loaded nontemporal (they would only evict the
+// input vector and the selectors from the caches); X is read through the
+// caches (every row reuses it).  Both layouts accumulate the same products in
+// the same order, and the row sum is a fixed-order 64-lane reduction, so
+// their results are identical.
 constexpr int kT1Steps = 4;
+
+// 16 bytes through a buffer resource; an offset past the resource's range
+// reads zeros.  cpol: cache policy bits (kCpolNt: nontemporal).
+constexpr uint32_t kOutOfRange = 0x80000000u;
+constexpr int kCpolNt = 2;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t t1_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), short(0), int(bytes), 0x00020000);
+}
+
+__device__ __forceinline__ u32x4 ld16_rsrc(__amdgpu_buffer_rsrc_t r, uint32_t off, int cpol) {
+  return cpol == kCpolNt ? __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCpolNt))
+                         : __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
 
 template <bool PACKED>
 __global__ __launch_bounds__(256) void gemv_t1_kernel(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
@@ -274,7 +293,7 @@ __global__ __launch_bounds__(256) void gemv_t1_kernel(const uint16_t* __restrict
   __shared__ int s_v[4][PACKED ? 1 : 64];
   __shared__ float s_m[4][PACKED ? 1 : 64];
   const int lane = threadIdx.x & 63;
-  const int wv = threadIdx.x >> 6;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform, so the row's resource is too
   const int o = int(blockIdx.x) * 4 + wv;
   if (o >= d_out) return;  // whole wave leaves together; no block barrier below
   const int G_in = d_in / g;  // at most 64 in place
@@ -282,53 +301,97 @@ __global__ __launch_bounds__(256) void gemv_t1_kernel(const uint16_t* __restrict
   const int gps = 64 / lpg;   // groups per step
   const int slot = lane / lpg;
   const int e = (lane % lpg) * 8;
+  // The row's kept groups as a list (column, selector), 64 entries at a time:
+  // in place from a ballot over the row's selectors (at most 64, one batch),
+  // kept in LDS; packed from chunk[] and scale[] with one coalesced load per
+  // batch, kept in registers and read across lanes.
   int nk;
   int64_t pb = 0;
+  uint64_t bits = 0;
+  float mv = 0.0f;
   if constexpr (PACKED) {
-    pb = rowptr[o];
-    nk = rowptr[o + 1] - int(pb);
+    const int p0 = __builtin_amdgcn_readfirstlane(rowptr[o]);  // the same for every lane
+    pb = p0;
+    nk = __builtin_amdgcn_readfirstlane(rowptr[o + 1]) - p0;
   } else {
-    const float mv = lane < G_in ? mask[int64_t(o / go) * G_in + lane] : 0.0f;
-    const uint64_t bits = __ballot(mv != 0.0f);
+    mv = lane < G_in ? mask[int64_t(o / go) * G_in + lane] : 0.0f;
+    bits = __ballot(mv != 0.0f);
     nk = __popcll(bits);
-    if (mv != 0.0f) {
-      const int r = __builtin_amdgcn_mbcnt_hi(uint32_t(bits >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(bits), 0u));
-      s_v[wv][r] = lane;
-      s_m[wv][r] = mv;
-    }
-    // LDS writes of this wave become visible to its other lanes before the list is read.
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
-  const uint16_t* wrow = PACKED ? Wp + pb * g + e : W + int64_t(o) * d_in + e;
+  // Packed: byte ranges of the row's weights and of X (loads at an offset
+  // past the range return zeros: dead steps need no branch).
+  const uint16_t* wrow = PACKED ? Wp + pb * g : W + int64_t(o) * d_in;  // wave-uniform
+  const __amdgpu_buffer_rsrc_t rw = t1_rsrc(wrow, PACKED ? uint32_t(nk * g) * 2u : 0u);
+  const __amdgpu_buffer_rsrc_t rx = t1_rsrc(X, PACKED ? uint32_t(d_in) * 2u : 0u);
   float acc = 0.0f;
-  for (int k0 = 0; k0 < nk; k0 += kT1Steps * gps) {
-    u32x4 w[kT1Steps], x[kT1Steps];
-    float m[kT1Steps];
-#pragma unroll
-    for (int c = 0; c < kT1Steps; ++c) {
-      const int k = k0 + c * gps + slot;
-      const bool live = k < nk;
-      int v = 0;
-      m[c] = 0.0f;
-      w[c] = zero16();
-      x[c] = zero16();
-      if (live) {
-        if constexpr (PACKED) {
-          v = chunk[pb + k];
-          m[c] = scale[pb + k];
-          w[c] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wrow + int64_t(k) * g));
-        } else {
-          v = s_v[wv][k];
-          m[c] = s_m[wv][k];
-          w[c] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wrow + v * g));
-        }
-        x[c] = ld16(X + v * g + e);
+  for (int kb = 0; kb < nk; kb += 64) {
+    // packed: lane j holds entry kb + j of the row's list (one coalesced load);
+    // in place: the list goes to LDS by rank
+    int cv = 0;
+    float cs = 0.0f;
+    if constexpr (PACKED) {
+      if (kb + lane < nk) {
+        cv = chunk[pb + kb + lane];
+        cs = scale[pb + kb + lane];
       }
+    } else {
+      if (mv != 0.0f) {
+        const int r = __builtin_amdgcn_mbcnt_hi(uint32_t(bits >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(bits), 0u));
+        s_v[wv][r] = lane;
+        s_m[wv][r] = mv;
+      }
+      // LDS writes of this wave become visible to its other lanes before the list is read.
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
+    const int nb = min(64, nk - kb);
+    for (int k0 = 0; k0 < nb; k0 += kT1Steps * gps) {
+      u32x4 w[kT1Steps], x[kT1Steps];
+      float m[kT1Steps];
+      int v[kT1Steps];
+      if constexpr (PACKED) {
+        // the weights need only the row pointer: issued before the list arrives
+        // (branch-free, so the list can be waited for without the weights)
 #pragma unroll
-    for (int c = 0; c < kT1Steps; ++c) acc += m[c] * dot8_bf16(w[c], x[c]);
+        for (int c = 0; c < kT1Steps; ++c) {
+          const int kk = k0 + c * gps + slot;
+          w[c] = ld16_rsrc(rw, kk < nb ? (uint32_t(kb + kk) * uint32_t(g) + uint32_t(e)) * 2u : kOutOfRange, kCpolNt);
+        }
+        // every lane takes part in both reads (a lane reads from a lane whose
+        // own step may be past the list), then dead steps drop their selector
+#pragma unroll
+        for (int c = 0; c < kT1Steps; ++c) {
+          const int kk = k0 + c * gps + slot;
+          const int k = min(kk, 63);
+          v[c] = __shfl(cv, k);
+          const float ms = __shfl(cs, k);
+          m[c] = kk < nb ? ms : 0.0f;
+        }
+#pragma unroll
+        for (int c = 0; c < kT1Steps; ++c)
+          x[c] = ld16_rsrc(rx, k0 + c * gps + slot < nb ? uint32_t(v[c] * g + e) * 2u : kOutOfRange, 0);
+      } else {
+        // in place the weights wait for the list anyway: plain loads, weight and input together
+#pragma unroll
+        for (int c = 0; c < kT1Steps; ++c) {
+          const int k = k0 + c * gps + slot;
+          const bool live = k < nb;
+          v[c] = 0;
+          m[c] = 0.0f;
+          w[c] = zero16();
+          x[c] = zero16();
+          if (live) {
+            v[c] = s_v[wv][k];
+            m[c] = s_m[wv][k];
+            w[c] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wrow + v[c] * g + e));
+            x[c] = ld16(X + v[c] * g + e);
+          }
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < kT1Steps; ++c) acc += m[c] * dot8_bf16(w[c], x[c]);
+    }
   }
 #pragma unroll
   for (int d = 32; d >= 1; d >>= 1) acc += __shfl_xor(acc, d);
