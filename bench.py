@@ -362,6 +362,35 @@ def _prefill_13b(reps):
             "ms_per_layer": ms, "kept_TFLOP/s": fl / (ms / 1e3) / 1e12, "GB/s": by / (ms / 1e3) / 1e9}
 
 
+def _dense_context(d, breakdown, reps):
+    """Context, not a target: the vendor dense GEMM (hipBLASLt through torch.matmul) on the three dense products
+    of the same training step on the headline tensors, Y = X W^T, dX = dY W and the weight gradient dW = dY^T X,
+    every operand contiguous and row-major (the transposed ones copied beforehand).  The masked step computes
+    the forward on kept groups, dX over kept groups and the per-group gradient instead of dW; the ratio of the
+    dense time to the masked forward + backward time is the figure to set beside a dense layer."""
+    import torch
+    X, W, dY = d["X"], d["W"], d["dY"]
+    Wt = W.t().contiguous()
+    dYt = dY.t().contiguous()
+    T, d_in = X.shape
+    d_out = W.shape[0]
+    prods = {"fwd": lambda: torch.matmul(X, Wt), "dX": lambda: torch.matmul(dY, W),
+             "dW": lambda: torch.matmul(dYt, X)}
+    out = {"workload": f"dense bf16 GEMMs of the same step: {T} tokens, W {d_out}x{d_in} (hipBLASLt via torch.matmul)"}
+    total = 0.0
+    for name, fn in prods.items():
+        for _ in range(10):
+            fn()
+        torch.cuda.synchronize()
+        ms = _events_batch_ms(fn, reps)
+        total += ms
+        out[name + "_ms"] = ms
+        out[name + "_TFLOP/s"] = 2.0 * T * d_in * d_out / (ms / 1e3) / 1e12
+    masked = breakdown["fwd"] + breakdown["bwd"]
+    out.update({"dense_fwd_bwd_ms": total, "masked_fwd_bwd_ms": masked, "speedup": total / masked})
+    return out
+
+
 # ------------------------------------------------------------------ CPU baseline
 
 def _cpu_baseline(case, flops_per_step, budget_s):
@@ -763,6 +792,8 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
 
+    dense = _dense_context(d, breakdown, reps)
+
     gemv = None
     if not args.no_gemv:
         gemv = _gemv_bandwidth(args.gemv_layers, max(3, args.steps // 4))
@@ -820,6 +851,7 @@ def main():
                     "sources_sha256": _sources_digest(),
                     "fwd_kept_tflops": fwd_tflops, "breakdown_ms": breakdown},
         "cpu_baseline": cpu,
+        "dense_context": dense,
         "gemv": gemv,
         "budget": budget,
         "square_groups": square,
