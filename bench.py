@@ -73,7 +73,8 @@ def _parse():
     ap.add_argument("--no-distill", action="store_true")
     ap.add_argument("--no-hyper", action="store_true")
     ap.add_argument("--no-model", action="store_true", help="skip the MLP-trio and whole-LLaMA-2-7B steps")
-    ap.add_argument("--no-sweep", action="store_true", help="skip the LLaMA-2-13B T=8192 sweep and T=512 forward")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the LLaMA-2-13B T=8192 sweep")
+    ap.add_argument("--no-prefill", action="store_true", help="skip the LLaMA-2-13B T=512 forward")
     ap.add_argument("--gemv-layers", type=int, default=40)
     ap.add_argument("--profile-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this size (counter calibration runs)")
@@ -820,6 +821,7 @@ def main():
     sweep = prefill = None
     if not args.no_sweep:
         sweep = _sweep_13b(max(5, args.steps // 10))
+    if not args.no_prefill:
         prefill = _prefill_13b(max(5, args.steps // 4))
 
     cpu = None
