@@ -68,27 +68,27 @@ def test_workspace_size_square_groups(g, nsub):
 
 def _fwd_split_bytes(T, d_in, d_out, g):
     """The documented rule: at most 128 output tiles of 256 x 256 (and T > 16) split K into
-    min(256 // tiles, 8, units // 2) shares of fp32 partial tiles; units of max(g, 32) columns."""
+    min(256 // tiles, 8, units // 4) shares of fp32 partial tiles; units of max(g, 32) columns."""
     if T <= 16:
         return 0
     tiles = -(-T // 256) * -(-d_out // 256)
     if tiles > 128:
         return 0
-    ks = min(256 // tiles, 8, d_in // max(g, 32) // 2)
+    ks = min(256 // tiles, 8, d_in // max(g, 32) // 4)
     return 0 if ks <= 1 else (ks * T * d_out * 4 + 255) // 256 * 256
 
 
 @pytest.mark.parametrize("T,d_in,d_out,g,expect", [
     (4096, 4096, 4096, 256, 0),                       # 256 tiles: unsplit
     (16, 5120, 5120, 256, 0),                         # decode path
-    (512, 5120, 5120, 256, 6 * 512 * 5120 * 4),       # 40 tiles: 6 shares
+    (512, 5120, 5120, 256, 5 * 512 * 5120 * 4),       # 40 tiles, 20 units: 5 shares
     (512, 5120, 13824, 256, 2 * 512 * 13824 * 4),     # 108 tiles: 2 shares
     (512, 13824, 5120, 256, 6 * 512 * 5120 * 4),
     (2048, 4096, 4096, 256, 2 * 2048 * 4096 * 4),     # 128 tiles: 2 shares
     (2048, 4096, 4352, 256, 0),                       # 136 tiles: unsplit
-    (17, 4096, 4096, 256, 8 * 17 * 4096 * 4),         # 16 tiles, 16 units: 8 shares
-    (300, 1024, 1024, 512, 0),                        # two units: a share would hold one
-    (300, 2048, 1024, 512, 2 * 300 * 1024 * 4),
+    (17, 4096, 4096, 256, 4 * 17 * 4096 * 4),         # 16 tiles, 16 units: 4 shares
+    (300, 2048, 1024, 512, 0),                        # four units: a share would hold fewer
+    (300, 4096, 1024, 512, 2 * 300 * 1024 * 4),
 ])
 def test_forward_split_workspace(T, d_in, d_out, g, expect):
     assert gm.gm_workspace_size(gm.GM_OP_FWD, T, d_in, d_out, g) == expect == _fwd_split_bytes(T, d_in, d_out, g)
@@ -202,10 +202,10 @@ def test_linear_argument_errors():
     assert fwd(FAKE, MISALIGNED, FAKE, 16, 256, 256, 256, 1, FAKE, None, 0, None) == gm.GM_ERR_ALIGN
     assert fwd(FAKE, FAKE, MISALIGNED, 16, 256, 256, 32, 32, FAKE, None, 0, None) == gm.GM_ERR_ALIGN
     # a workspace, when given, must be aligned and at least the split size
-    need = gm.gm_workspace_size(gm.GM_OP_FWD, 512, 1024, 1024, 256)
+    need = gm.gm_workspace_size(gm.GM_OP_FWD, 512, 2048, 1024, 256)
     assert need > 0
-    assert fwd(FAKE, FAKE, FAKE, 512, 1024, 1024, 256, 1, FAKE, FAKE, need - 1, None) == gm.GM_ERR_WORKSPACE
-    assert fwd(FAKE, FAKE, FAKE, 512, 1024, 1024, 256, 1, FAKE, MISALIGNED, need, None) == gm.GM_ERR_ALIGN
+    assert fwd(FAKE, FAKE, FAKE, 512, 2048, 1024, 256, 1, FAKE, FAKE, need - 1, None) == gm.GM_ERR_WORKSPACE
+    assert fwd(FAKE, FAKE, FAKE, 512, 2048, 1024, 256, 1, FAKE, MISALIGNED, need, None) == gm.GM_ERR_ALIGN
 
     bwd = L.gm_masked_linear_bwd
     # dX requested without a mask

@@ -45,10 +45,10 @@ def _check(case, mask, g_out=1):
 
 
 @pytest.mark.parametrize("T,d_in,d_out,g", [
-    (512, 1024, 1024, 256),    # 8 tiles, 2 shares of 2 units
-    (300, 4096, 520, 256),     # ragged T and d_out, 8 shares
+    (512, 2048, 1024, 256),    # 8 tiles, 2 shares of 4 units
+    (300, 4096, 520, 256),     # ragged T and d_out, 4 shares
     (17, 4096, 4096, 256),     # smallest GEMM token count, 16 tiles
-    (257, 2048, 1024, 512),    # 2-unit shares of 512-wide groups
+    (257, 4096, 1024, 512),    # 4-unit shares of 512-wide groups
     (700, 3072, 768, 64),      # 64-wide groups, 48 units
     (2048, 1024, 4096, 128),   # 128 tiles: 2 shares
 ])
