@@ -367,6 +367,48 @@ def test_preserved_rate_counts_active_weights():
     assert (d_out * d_in) / B.size == gold["reduction_factor"]
 
 
+def test_kept_count_and_preserved_rate_away_from_one_half():
+    """At 3 of 8 kept, counting the pruned groups (5) or the pruned weights (5/8) instead fails."""
+    B = np.array([[1, 0, 0, 1], [0, 0, 0.25, 0]])  # a fractional selector is kept too (only zeros prune)
+    assert oracle.kept_count(B) == 3
+    assert oracle.preserved_rate(B, 3) == pytest.approx(3 / 8)
+    # 2-D groups: each selector covers g_out x g weights, so the rate is still 3 of 8 selectors
+    assert oracle.preserved_rate(B, 4, 2) == pytest.approx(3 / 8)
+    # element count after the Kronecker expansion, one weight at a time
+    M = oracle.expand_mask((B != 0).astype(float), 5, 3)
+    assert M.shape == (6, 20) and int(M.sum()) == 3 * 15
+    # Eq. 2 on the same matrix: s = 1 - 3/8 (a layer of 6 x 20 weights, one layer)
+    s_l, s = oracle.sparsity([B], [(6, 20)])
+    assert s_l == [pytest.approx(5 / 8)] and s == pytest.approx(5 / 8)
+
+
+# ------------------------------------------------------------- bf16 widening
+
+def _bf16_closed_form(bits: int) -> float:
+    """Value of a finite bf16 pattern from its fields: sign, 8-bit exponent (bias 127), 7-bit fraction."""
+    sign = -1.0 if bits >> 15 else 1.0
+    e, f = (bits >> 7) & 0xFF, bits & 0x7F
+    if e == 0:
+        return sign * math.ldexp(f / 128.0, -126)  # subnormal (and signed zero)
+    return sign * math.ldexp(1.0 + f / 128.0, e - 127)
+
+
+def test_from_bf16_is_exact_over_every_bit_pattern():
+    """Every one of the 65,536 patterns: equal to torch's bfloat16 -> float64 widening (NaNs stay NaN),
+    and every finite one equal to the value its sign, exponent and fraction fields define."""
+    import torch
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    got = oracle.from_bf16(bits)
+    ref = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(got, ref)  # NaN positions must agree as well
+    assert np.array_equal(np.signbit(got), np.signbit(ref))  # -0 stays -0
+    finite = ((bits >> 7) & 0xFF) != 0xFF
+    assert int(finite.sum()) == 65536 - 256  # exponent field all ones: 2 signs x 128 fractions
+    closed = np.array([_bf16_closed_form(int(b)) for b in bits[finite]])
+    np.testing.assert_array_equal(got[finite], closed)
+    assert np.all(np.isinf(got[((bits & 0x7FFF) == 0x7F80)]))
+
+
 # ------------------------------------------- sparsity-budget regulariser (Sec. 2.3)
 
 def _budget_layers():
@@ -831,6 +873,26 @@ def _mutant_adamw_coupled_decay(p, g, m, v, lr, beta1, beta2, eps, weight_decay,
                        step)
 
 
+def _mutant_from_bf16_as_half(bits):
+    # the 16 bits read as IEEE half precision instead of the top half of an fp32
+    return np.asarray(bits, dtype=np.uint16).view(np.float16).astype(np.float64)
+
+
+def _mutant_from_bf16_shift15(bits):
+    b = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(15)
+    return b.view(np.float32).astype(np.float64)
+
+
+def _mutant_kept_count_pruned(B):
+    B = np.asarray(B)
+    return int(B.size - np.count_nonzero(B))
+
+
+def _mutant_preserved_rate_pruned(B, g_in, g_out=1):
+    M = oracle.expand_mask((np.asarray(B) == 0).astype(np.float64), g_in, g_out)
+    return float(M.sum() / M.size)
+
+
 MUTANTS = [
     ("linear_fwd", _mutant_fwd_strided_groups),
     ("linear_fwd", _mutant_fwd_strided_rows),
@@ -857,6 +919,10 @@ MUTANTS = [
     ("hyper_bwd", _mutant_hyper_bwd_head_transposed),
     ("adamw_step", _mutant_adamw_no_bias_correction),
     ("adamw_step", _mutant_adamw_coupled_decay),
+    ("from_bf16", _mutant_from_bf16_as_half),
+    ("from_bf16", _mutant_from_bf16_shift15),
+    ("kept_count", _mutant_kept_count_pruned),
+    ("preserved_rate", _mutant_preserved_rate_pruned),
 ]
 
 PIN_TESTS = [
@@ -890,6 +956,8 @@ PIN_TESTS = [
     lambda: test_hyper_gradients_match_autograd(6, 5, 3),
     test_hyper_gru_gradient_matches_finite_differences,
     test_adamw_matches_torch,
+    test_kept_count_and_preserved_rate_away_from_one_half,
+    test_from_bf16_is_exact_over_every_bit_pattern,
 ]
 
 
