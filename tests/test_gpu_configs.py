@@ -2,14 +2,21 @@
 configuration the benchmark times.  The oracle checks whole tensors where it
 finishes in seconds and otherwise sampled rows, columns and groups, computed
 from the same inputs restricted to the sample (row and column slices of a
-product are products of slices)."""
+product are products of slices).
+
+Gate inputs are independent draws, logits ~ N(0, 1) and u ~ U(0, 1), shifted
+per selector matrix by one offset that the oracle picks so that the budgeted
+number of groups is kept.  The hard mask is compared with the oracle's gate
+(bit-exact outside the 1e-6 band around the threshold, gates inside it counted
+and reported); the products are then checked on the mask the GPU produced."""
 import numpy as np
 import pytest
 
 import oracle
 import workloads
-from gpu_support import (assert_close, dev_bf16, dev_f32, empty_bf16, empty_f32, host_bits, host_f64_from_bf16, say,
-                         sync, workspace)
+from gpu_support import (assert_close, assert_dgate, assert_dx, assert_fwd, budgeted_independent_inputs, check_gate,
+                         dev_bf16, dev_f32, empty_bf16, empty_f32, host_bits, host_f64_from_bf16, independent_case,
+                         ref_dgate, ref_dx, ref_fwd, say, sync, workspace)
 
 pytestmark = pytest.mark.gpu
 
@@ -25,7 +32,8 @@ def _step(d, g, tau):
     mask, soft = empty_f32(d_out, d_in // g), empty_f32(d_out, d_in // g)
     gm.gm_gate(d["logits"], d["noise"], tau, True, mask, soft)
     Y = empty_bf16(T, d_out)
-    gm.gm_masked_linear_fwd(d["X"], d["W"], mask, g, Y)
+    fws = workspace(gm.gm_workspace_size(gm.GM_OP_FWD, T, d_in, d_out, g))
+    gm.gm_masked_linear_fwd(d["X"], d["W"], mask, g, Y, fws)
     dX, dgate = empty_bf16(T, d_in), empty_f32(d_out, d_in // g)
     ws = workspace(gm.gm_workspace_size(gm.GM_OP_BWD, T, d_in, d_out, g))
     gm.gm_masked_linear_bwd(d["dY"], d["X"], d["W"], mask, g, dX, dgate, ws)
@@ -41,20 +49,45 @@ def _device(case):
                 logits=dev_f32(case.logits), noise=dev_f32(case.noise))
 
 
-def _check_sampled(case, mask, Y, dX, dgate, key, n_rows=N_SAMPLE_ROWS):
-    r = workloads.gen.rng_for(300, *key)
-    T, d_in, d_out, g = case.T, case.d_in, case.d_out, case.g
+def _check_gate_and_budget(case, mask):
+    m_gpu = mask.cpu().numpy()
+    m_ref, y_ref, near = check_gate(m_gpu, case.logits, case.noise, case.tau)
+    assert int(m_ref.sum()) == case.kept, "the oracle's gate misses the budget"
+    assert abs(int(m_gpu.sum()) - case.kept) <= int(near.sum())  # only near-threshold gates may differ
+    return m_gpu.astype(np.float64), y_ref
+
+
+def _check_full(case, mask, Y, dX, dgate, dlog):
+    m, y_ref = _check_gate_and_budget(case, mask)
     X, W, dY = oracle.from_bf16(case.X), oracle.from_bf16(case.W), oracle.from_bf16(case.dY)
-    m = case.mask.astype(np.float64)
-    assert np.array_equal(mask.cpu().numpy(), case.mask), "hard mask differs from the budgeted selection"
+    assert_fwd("Y", host_f64_from_bf16(Y), X, W, m, case.g)
+    assert_dx("dX", host_f64_from_bf16(dX), dY, W, m, case.g)
+    dgr, bdg = ref_dgate(dY, X, W, case.g)
+    assert_close("dgate", dgate.cpu().numpy(), dgr, bound=bdg)
+    assert_close("dlogits", dlog.cpu().numpy().reshape(dgr.shape),
+                 oracle.gate_bwd(dgate.cpu().numpy(), y_ref.reshape(dgr.shape), case.tau), 1e-5)
+
+
+def _check_sampled(case, mask, Y, dX, dgate, key, n_rows=N_SAMPLE_ROWS):
+    m, _ = _check_gate_and_budget(case, mask)
+    r = workloads.gen.rng_for(300, *key)
+    T, d_out, g = case.T, case.d_out, case.g
+    X, W, dY = oracle.from_bf16(case.X), oracle.from_bf16(case.W), oracle.from_bf16(case.dY)
     t_s = np.sort(r.choice(T, size=min(n_rows, T), replace=False))
     o_s = np.sort(r.choice(d_out, size=min(n_rows, d_out), replace=False))
-    Yg = host_f64_from_bf16(Y)[t_s]
-    assert_close("Y (sampled tokens)", Yg, oracle.linear_fwd(X[t_s], W, m, g))
-    dXg = host_f64_from_bf16(dX)[t_s]
-    assert_close("dX (sampled tokens)", dXg, oracle.linear_bwd_dx(dY[t_s], W, m, g))
-    dgg = dgate.cpu().numpy()[o_s]
-    assert_close("dgate (sampled rows)", dgg, oracle.linear_bwd_dgate(dY[:, o_s], X, W[o_s], g))
+    assert_fwd("Y (sampled tokens)", host_f64_from_bf16(Y)[t_s], X, W, m, g, rows=t_s)
+    assert_dx("dX (sampled tokens)", host_f64_from_bf16(dX)[t_s], dY, W, m, g, rows=t_s)
+    assert_dgate("dgate (sampled rows)", dgate.cpu().numpy()[o_s], dY[:, o_s], X, W[o_s], g)
+
+
+def test_single_linear_128_tokens_full_tensors():
+    cfg = workloads.config("single_1024")
+    T, g, tau = cfg["T"], cfg["g"], cfg["tau"]
+    _, d_out, d_in = cfg["linears"][0]
+    say(f"single linear: T={T} {d_out}x{d_in} g={g}, half of the groups kept")
+    case = independent_case((1, 0, 0), T, d_in, d_out, g, None, tau=tau)
+    mask, _, Y, dX, dgate, dlog = _step(_device(case), g, tau)
+    _check_full(case, mask, Y, dX, dgate, dlog)
 
 
 def test_attention_projection_4096_full_tensors():
@@ -62,18 +95,9 @@ def test_attention_projection_4096_full_tensors():
     T, g, tau = cfg["T"], cfg["g"], cfg["tau"]
     _, d_out, d_in = cfg["linears"][0]
     say(f"attn 4096: T={T} {d_out}x{d_in} g={g}")
-    case = workloads.make_linear_case((2, 0, 0), T, d_in, d_out, g, None, tau=tau)
-    mask, soft, Y, dX, dgate, dlog = _step(_device(case), g, tau)
-    m_ref, y_ref = oracle.gate(case.logits, case.noise, tau, True)
-    assert np.array_equal(mask.cpu().numpy(), m_ref)
-    assert int(m_ref.sum()) == d_out * (d_in // g) // 2
-    X, W, dY = oracle.from_bf16(case.X), oracle.from_bf16(case.W), oracle.from_bf16(case.dY)
-    assert_close("Y", host_f64_from_bf16(Y), oracle.linear_fwd(X, W, m_ref, g))
-    dXr, dgr = oracle.linear_bwd(dY, X, W, m_ref, g)
-    assert_close("dX", host_f64_from_bf16(dX), dXr)
-    assert_close("dgate", dgate.cpu().numpy(), dgr)
-    assert_close("dlogits", dlog.cpu().numpy().reshape(dgr.shape), oracle.gate_bwd(dgate.cpu().numpy(), y_ref, tau),
-                 1e-5)
+    case = independent_case((2, 0, 0), T, d_in, d_out, g, None, tau=tau)
+    mask, _, Y, dX, dgate, dlog = _step(_device(case), g, tau)
+    _check_full(case, mask, Y, dX, dgate, dlog)
 
 
 def test_mlp_trio_layer_adaptive():
@@ -83,9 +107,8 @@ def test_mlp_trio_layer_adaptive():
     kept, s = workloads.kept_counts_uniform_law(workloads.gen.rng_for(3, 1), groups, 0.3, 0.7)
     for j, (name, d_out, d_in) in enumerate(cfg["linears"]):
         say(f"mlp {name}: T={T} {d_out}x{d_in} sparsity {s[j]:.3f}")
-        case = workloads.make_linear_case((3, 0, j), T, d_in, d_out, g, kept[j], tau=tau)
+        case = independent_case((3, 0, j), T, d_in, d_out, g, kept[j], tau=tau)
         mask, _, Y, dX, dgate, _ = _step(_device(case), g, tau)
-        assert int(mask.sum().item()) == kept[j]
         _check_sampled(case, mask, Y, dX, dgate, (3, j))
 
 
@@ -98,23 +121,46 @@ def _llama2_7b_budget():
     return cfg, shapes, groups, kept
 
 
-def test_llama2_7b_batched_gate_meets_global_budget():
+def _run_gate(logits, noise, tau):
     import paper_2609_33977_amd as gm
+    d_m, d_y = empty_f32(logits.size), empty_f32(logits.size)
+    gm.gm_gate(dev_f32(logits), dev_f32(noise), tau, True, d_m, d_y)
+    sync()
+    return d_m.cpu().numpy(), d_y.cpu().numpy()
+
+
+def test_llama2_7b_batched_gate_meets_global_budget():
     cfg, shapes, groups, kept = _llama2_7b_budget()
     assert sum(kept) * 2 == sum(groups)
-    # One batched gate over all 224 selector matrices, as in the mask-learning step.
+    # One batched gate over all 224 selector matrices, as in the mask-learning step;
+    # each matrix's independent draws are shifted to its budget.
     r = workloads.gen.rng_for(4, 1)
-    flat = np.concatenate([workloads.random_kept_mask(r, G, k) for G, k in zip(groups, kept)])
-    logits, noise = workloads.budgeted_gate_inputs(r, flat)
-    say(f"llama2-7b: batched gate over {flat.size} groups")
-    d_m, d_y = empty_f32(flat.size), empty_f32(flat.size)
-    gm.gm_gate(dev_f32(logits), dev_f32(noise), cfg["tau"], True, d_m, d_y)
-    sync()
-    mg = d_m.cpu().numpy()
-    assert np.array_equal(mg, flat)
-    s_layer, s_glob = oracle.sparsity(np.split(mg, np.cumsum(groups)[:-1]), shapes)
+    parts = [budgeted_independent_inputs(r, G, k, cfg["tau"]) for G, k in zip(groups, kept)]
+    logits = np.concatenate([p[0] for p in parts])
+    noise = np.concatenate([p[1] for p in parts])
+    say(f"llama2-7b: batched gate over {logits.size} groups")
+    mg, _ = _run_gate(logits, noise, cfg["tau"])
+    m_ref, _, near = check_gate(mg, logits, noise, cfg["tau"])
+    assert np.array_equal(m_ref, np.concatenate([p[2] for p in parts]))
+    s_layer, s_glob = oracle.sparsity(np.split(m_ref, np.cumsum(groups)[:-1]), shapes)
     assert s_glob == pytest.approx(0.5, abs=1e-12)
     assert min(s_layer) < 0.35 and max(s_layer) > 0.65  # budgets really are layer-adaptive
+
+
+def test_llama2_7b_size_gate_on_unshifted_independent_draws():
+    # 25,296,896 selectors (every group of LLaMA-2-7B's 224 masked linears) with
+    # logits ~ N(0, 1) and u ~ U(0, 1) independent and unshifted: gates land
+    # within 1e-6 of the threshold at their natural rate (about 6e-7 per gate)
+    cfg, _, groups, _ = _llama2_7b_budget()
+    n = sum(groups)
+    logits, noise = workloads.independent_gate_inputs(workloads.gen.rng_for(4, 2), n)
+    say(f"llama2-7b size: gate over {n} independent draws, tau {cfg['tau']}")
+    mg, yg = _run_gate(logits, noise, cfg["tau"])
+    m_ref, y_ref, near = check_gate(mg, logits, noise, cfg["tau"])
+    say(f"  kept {int(m_ref.sum())} of {n} ({m_ref.mean():.5f}); soft value max |gpu - oracle| "
+        f"{float(np.max(np.abs(yg - y_ref))):.2e}")
+    assert abs(m_ref.mean() - 0.5) < 5 * 0.5 / np.sqrt(n)
+    assert float(np.max(np.abs(yg - y_ref))) < 1e-5
 
 
 @pytest.mark.parametrize("layer", [0, 31])
@@ -124,7 +170,7 @@ def test_llama2_7b_layer_linears(layer):
     for j, (name, d_out, d_in) in enumerate(cfg["linears"]):
         idx = layer * len(cfg["linears"]) + j
         say(f"llama2-7b layer {layer} {name}: {d_out}x{d_in} kept {kept[idx]}/{groups[idx]}")
-        case = workloads.make_linear_case((4, layer, j), T, d_in, d_out, g, kept[idx], tau=tau)
+        case = independent_case((4, layer, j), T, d_in, d_out, g, kept[idx], tau=tau)
         mask, _, Y, dX, dgate, _ = _step(_device(case), g, tau)
         _check_sampled(case, mask, Y, dX, dgate, (4, layer, j), n_rows=32)
 
@@ -140,7 +186,8 @@ def test_llama2_13b_inference_path(T):
         case = workloads.make_linear_case((5, T, d_out, d_in), T, d_in, d_out, g, None, tau=cfg["tau"])
         X, W, mask = dev_bf16(case.X), dev_bf16(case.W), dev_f32(case.mask)
         Y = empty_bf16(T, d_out)
-        gm.gm_masked_linear_fwd(X, W, mask, g, Y)
+        fws = workspace(gm.gm_workspace_size(gm.GM_OP_FWD, T, d_in, d_out, g))
+        gm.gm_masked_linear_fwd(X, W, mask, g, Y, fws)
         cap = d_out * (d_in // g)
         Wp = torch.empty(cap, g, dtype=torch.bfloat16, device="cuda")
         chunk = torch.empty(cap, dtype=torch.int32, device="cuda")
@@ -153,12 +200,12 @@ def test_llama2_13b_inference_path(T):
         sync()
         assert int(rowptr[-1].item()) == cap // 2
         t_s = np.arange(T) if T <= 64 else np.sort(workloads.gen.rng_for(5, T).choice(T, 64, replace=False))
-        ref = oracle.linear_fwd(oracle.from_bf16(case.X)[t_s], oracle.from_bf16(case.W), case.mask, g)
-        assert_close("Y", host_f64_from_bf16(Y)[t_s], ref)
+        ref, b = ref_fwd(oracle.from_bf16(case.X)[t_s], oracle.from_bf16(case.W), case.mask, g)
+        assert_close("Y", host_f64_from_bf16(Y)[t_s], ref, bound=b)
         if T == 1:  # one kernel reads both layouts: identical results
             assert np.array_equal(host_bits(Yp), host_bits(Y))
         elif T <= 16:  # the packed layout keeps the per-row GEMV; in place, 2..16 tokens run on MFMA
-            assert_close("Y (packed)", host_f64_from_bf16(Yp)[t_s], ref)
+            assert_close("Y (packed)", host_f64_from_bf16(Yp)[t_s], ref, bound=b)
 
 
 @pytest.mark.parametrize("g", [64, 128, 256, 512])
@@ -167,6 +214,6 @@ def test_llama2_13b_group_size_sweep(g):
     T = cfg["T_sweep"]
     for name, d_out, d_in in (cfg["linears"][0], cfg["linears"][4], cfg["linears"][6]):
         say(f"13b sweep {name}: T={T} {d_out}x{d_in} g={g}")
-        case = workloads.make_linear_case((5, 99, d_out, g), T, d_in, d_out, g, None, tau=cfg["tau"])
+        case = independent_case((5, 99, d_out, g), T, d_in, d_out, g, None, tau=cfg["tau"])
         mask, _, Y, dX, dgate, _ = _step(_device(case), g, cfg["tau"])
         _check_sampled(case, mask, Y, dX, dgate, (5, g, d_out), n_rows=32)

@@ -10,7 +10,8 @@ import pytest
 import oracle
 import workloads
 from workloads.gen import rng_for
-from gpu_support import assert_close, empty_bf16, empty_f32, host_bits, say, sync, workspace
+from gpu_support import (assert_close, assert_dgate, assert_dx, assert_fwd, empty_bf16, empty_f32, host_bits, ref_fwd,
+                         say, sync, workspace)
 
 pytestmark = pytest.mark.gpu
 
@@ -67,16 +68,14 @@ def test_largest_matrix_forward_and_backward(big):
     rows[-1] = D_OUT - 1  # the last row touches the end of the addressable range
     Wr, mr = _rows_host(big, rows)
     Xo, dYo = oracle.from_bf16(host_bits(X)), oracle.from_bf16(host_bits(dY))
-    assert_close("Y (sampled rows)", oracle.from_bf16(host_bits(Y))[:, rows], oracle.linear_fwd(Xo, Wr, mr, G))
-    _, dg_r = oracle.linear_bwd(dYo[:, rows], Xo, Wr, mr, G)
-    assert_close("dgate (sampled rows)", dgate.cpu().numpy()[rows], dg_r)
+    assert_fwd("Y (sampled rows)", oracle.from_bf16(host_bits(Y))[:, rows], Xo, Wr, mr, G)
+    assert_dgate("dgate (sampled rows)", dgate.cpu().numpy()[rows], dYo[:, rows], Xo, Wr, G)
     # dX on two group columns (the first and the last): all rows of W over those columns
     for v in (0, D_IN // G - 1):
         cols = slice(v * G, (v + 1) * G)
         Wc = oracle.from_bf16(host_bits(big["W"][:, cols].contiguous()))
         mc = big["mask"][:, v: v + 1].cpu().numpy()
-        ref = oracle.linear_bwd(dYo, Xo[:, cols], Wc, mc, G)[0]
-        assert_close(f"dX (group column {v})", oracle.from_bf16(host_bits(dX))[:, cols], ref)
+        assert_dx(f"dX (group column {v})", oracle.from_bf16(host_bits(dX))[:, cols], dYo, Wc, mc, G)
 
 
 def test_largest_matrix_decode_in_place_and_packed(big):
@@ -99,9 +98,9 @@ def test_largest_matrix_decode_in_place_and_packed(big):
     rows = np.sort(rng_for(500, 2).choice(D_OUT, 128, replace=False))
     rows[-1] = D_OUT - 1
     Wr, mr = _rows_host(big, rows)
-    ref = oracle.linear_fwd(oracle.from_bf16(host_bits(x)), Wr, mr, G)
-    assert_close("Y in place (sampled rows)", oracle.from_bf16(host_bits(Y))[:, rows], ref)
-    assert_close("Y packed (sampled rows)", oracle.from_bf16(host_bits(Yp))[:, rows], ref)
+    ref, b = ref_fwd(oracle.from_bf16(host_bits(x)), Wr, mr, G)
+    assert_close("Y in place (sampled rows)", oracle.from_bf16(host_bits(Y))[:, rows], ref, bound=b)
+    assert_close("Y packed (sampled rows)", oracle.from_bf16(host_bits(Yp))[:, rows], ref, bound=b)
     del Wp
 
 
@@ -151,14 +150,12 @@ def test_longest_token_batch_forward_and_backward():
     toks[-1] = T - 1  # the last token touches the end of X's and dX's addressable range
     idx = torch.as_tensor(toks, device="cuda")
     Xs, dYs = oracle.from_bf16(host_bits(X[idx])), oracle.from_bf16(host_bits(dY[idx]))
-    assert_close("Y (sampled tokens)", oracle.from_bf16(host_bits(Y[idx])), oracle.linear_fwd(Xs, Wo, mo, g))
-    dX_ref, _ = oracle.linear_bwd(dYs, Xs, Wo, mo, g)
-    assert_close("dX (sampled tokens)", oracle.from_bf16(host_bits(dX[idx])), dX_ref)
+    assert_fwd("Y (sampled tokens)", oracle.from_bf16(host_bits(Y[idx])), Xs, Wo, mo, g)
+    assert_dx("dX (sampled tokens)", oracle.from_bf16(host_bits(dX[idx])), dYs, Wo, mo, g)
     dYo = oracle.from_bf16(host_bits(dY))
     for v in (0, d_in // g - 1):  # every token, two group columns (all rows of W)
         cols = slice(v * g, (v + 1) * g)
         Xc = oracle.from_bf16(host_bits(X[:, cols].contiguous()))
-        _, dg_ref = oracle.linear_bwd(dYo, Xc, Wo[:, cols], mo[:, v: v + 1], g)
-        assert_close(f"dgate (group column {v})", dgate.cpu().numpy()[:, v: v + 1], dg_ref)
+        assert_dgate(f"dgate (group column {v})", dgate.cpu().numpy()[:, v: v + 1], dYo, Xc, Wo[:, cols], g)
     del X, dX
     torch.cuda.empty_cache()

@@ -5,8 +5,8 @@ import pytest
 
 import oracle
 import workloads
-from gpu_support import (assert_close, dev_bf16, dev_f32, empty_bf16, empty_f32, host_bits, host_f64_from_bf16, say,
-                         sync, workspace)
+from gpu_support import (assert_close, dev_bf16, dev_f32, empty_bf16, empty_f32, host_bits, host_f64_from_bf16,
+                         ref_dgate, ref_dx, ref_fwd, say, sync, workspace)
 
 pytestmark = pytest.mark.gpu
 
@@ -40,11 +40,13 @@ def _bwd(d, g, want_dx=True, want_dgate=True):
 
 
 def _oracle_all(case, mask=None):
+    """Oracle Y, dX, dgate and their elementwise error bounds."""
     m = case.mask if mask is None else mask
     X, W, dY = oracle.from_bf16(case.X), oracle.from_bf16(case.W), oracle.from_bf16(case.dY)
-    Y = oracle.linear_fwd(X, W, m, case.g)
-    dX, dgate = oracle.linear_bwd(dY, X, W, m, case.g)
-    return Y, dX, dgate
+    Y, bY = ref_fwd(X, W, m, case.g)
+    dX, bdX = ref_dx(dY, W, m, case.g)
+    dgate, bdg = ref_dgate(dY, X, W, case.g)
+    return Y, dX, dgate, bY, bdX, bdg
 
 
 SHAPES = [  # (T, d_in, d_out, g): several tiles in every dimension plus ragged tails
@@ -64,10 +66,10 @@ def test_fwd_bwd_parity(T, d_in, d_out, g):
     d = _dev_case(case)
     Y = _fwd(d, g)
     dX, dgate = _bwd(d, g)
-    Yr, dXr, dgr = _oracle_all(case)
-    assert_close("Y", host_f64_from_bf16(Y), Yr)
-    assert_close("dX", host_f64_from_bf16(dX), dXr)
-    assert_close("dgate", dgate.cpu().numpy(), dgr)
+    Yr, dXr, dgr, bY, bdX, bdg = _oracle_all(case)
+    assert_close("Y", host_f64_from_bf16(Y), Yr, bound=bY)
+    assert_close("dX", host_f64_from_bf16(dX), dXr, bound=bdX)
+    assert_close("dgate", dgate.cpu().numpy(), dgr, bound=bdg)
 
 
 @pytest.mark.parametrize("T,d_in,d_out,g", [(200, 1024, 512, 256), (96, 512, 128, 64)])
@@ -80,10 +82,10 @@ def test_soft_mask_scales_groups(T, d_in, d_out, g):
     d = _dev_case(case, soft)
     Y = _fwd(d, g)
     dX, dgate = _bwd(d, g)
-    Yr, dXr, dgr = _oracle_all(case, soft)
-    assert_close("Y", host_f64_from_bf16(Y), Yr)
-    assert_close("dX", host_f64_from_bf16(dX), dXr)
-    assert_close("dgate", dgate.cpu().numpy(), dgr)
+    Yr, dXr, dgr, bY, bdX, bdg = _oracle_all(case, soft)
+    assert_close("Y", host_f64_from_bf16(Y), Yr, bound=bY)
+    assert_close("dX", host_f64_from_bf16(dX), dXr, bound=bdX)
+    assert_close("dgate", dgate.cpu().numpy(), dgr, bound=bdg)
 
 
 def test_all_ones_is_dense_and_all_zeros_is_exact_zero():
@@ -96,9 +98,9 @@ def test_all_ones_is_dense_and_all_zeros_is_exact_zero():
     d = _dev_case(case, ones)
     Y = _fwd(d, g)
     dX, _ = _bwd(d, g, want_dgate=False)
-    Yr, dXr, _ = _oracle_all(case, ones)
-    assert_close("Y (dense)", host_f64_from_bf16(Y), Yr)
-    assert_close("dX (dense)", host_f64_from_bf16(dX), dXr)
+    Yr, dXr, _, bY, bdX, _ = _oracle_all(case, ones)
+    assert_close("Y (dense)", host_f64_from_bf16(Y), Yr, bound=bY)
+    assert_close("dX (dense)", host_f64_from_bf16(dX), dXr, bound=bdX)
     # the dense product of the same bf16 values in fp32
     ref32 = (d["X"].float() @ d["W"].float().t()).cpu().numpy()
     assert_close("Y vs fp32 dense product", host_f64_from_bf16(Y), ref32)
@@ -108,8 +110,8 @@ def test_all_ones_is_dense_and_all_zeros_is_exact_zero():
     dX, dgate = _bwd(d, g)
     assert not np.any(host_bits(Y) & 0x7FFF)
     assert not np.any(host_bits(dX) & 0x7FFF)
-    _, _, dgr = _oracle_all(case, zeros)
-    assert_close("dgate (all pruned)", dgate.cpu().numpy(), dgr)
+    _, _, dgr, _, _, bdg = _oracle_all(case, zeros)
+    assert_close("dgate (all pruned)", dgate.cpu().numpy(), dgr, bound=bdg)
     del torch
 
 
@@ -135,8 +137,8 @@ def test_decode_forward(T, g):
     case = workloads.make_linear_case((205, T, g), T, d_in, d_out, g, None)
     d = _dev_case(case)
     Y = _fwd(d, g)
-    Yr, _, _ = _oracle_all(case)
-    assert_close("Y", host_f64_from_bf16(Y), Yr)
+    Yr, _, _, bY, _, _ = _oracle_all(case)
+    assert_close("Y", host_f64_from_bf16(Y), Yr, bound=bY)
 
 
 @pytest.mark.parametrize("T,d_out,g_out", [(8, 12296, 1), (16, 12296, 1), (5, 12304, 16), (12, 12416, 64)])
@@ -153,7 +155,7 @@ def test_decode_four_row_tiles(T, d_out, g_out):
     gm.gm_masked_linear_fwd(d["X"], d["W"], d["mask"], g, Y, g_out=g_out)
     sync()
     Yr = oracle.linear_fwd(oracle.from_bf16(case.X), oracle.from_bf16(case.W), case.mask, g, g_out)
-    assert_close("Y", host_f64_from_bf16(Y), Yr)
+    assert_close("Y", host_f64_from_bf16(Y), Yr, bound=bY)
 
 
 def _pack(d, g):
@@ -201,8 +203,8 @@ def test_packed_forward(T):
     Y = empty_bf16(T, d_out)
     gm.gm_packed_linear_fwd(d["X"], Wp, chunk, scale, rowptr, d_out, g, Y)
     sync()
-    Yr, _, _ = _oracle_all(case)
-    assert_close("Y", host_f64_from_bf16(Y), Yr)
+    Yr, _, _, bY, _, _ = _oracle_all(case)
+    assert_close("Y", host_f64_from_bf16(Y), Yr, bound=bY)
     Y2 = _fwd(d, g)
     if T == 1:  # the same one-wave-per-row kernel reads both layouts: identical results
         assert np.array_equal(host_bits(Y), host_bits(Y2))
@@ -232,12 +234,12 @@ def test_edge_shapes(T, d_in, d_out, g):
     case = workloads.make_linear_case((210, T, d_in, d_out, g), T, d_in, d_out, g, None)
     d = _dev_case(case)
     Y = _fwd(d, g)
-    Yr, dXr, dgr = _oracle_all(case)
-    assert_close("Y", host_f64_from_bf16(Y), Yr)
+    Yr, dXr, dgr, bY, bdX, bdg = _oracle_all(case)
+    assert_close("Y", host_f64_from_bf16(Y), Yr, bound=bY)
     if T > 16:
         dX, dgate = _bwd(d, g)
-        assert_close("dX", host_f64_from_bf16(dX), dXr)
-        assert_close("dgate", dgate.cpu().numpy(), dgr)
+        assert_close("dX", host_f64_from_bf16(dX), dXr, bound=bdX)
+        assert_close("dgate", dgate.cpu().numpy(), dgr, bound=bdg)
 
 
 def test_decode_and_gemm_paths_agree_at_the_boundary():
@@ -265,14 +267,14 @@ def test_decode_soft_selectors_in_place_and_packed(T, g):
     soft = r.uniform(0.05, 1.5, size=case.mask.shape).astype(np.float32)
     soft[r.uniform(size=soft.shape) < 0.4] = 0.0
     d = _dev_case(case, soft)
-    Yr, _, _ = _oracle_all(case, soft)
-    assert_close("Y in place", host_f64_from_bf16(_fwd(d, g)), Yr)
+    Yr, _, _, bY, _, _ = _oracle_all(case, soft)
+    assert_close("Y in place", host_f64_from_bf16(_fwd(d, g)), Yr, bound=bY)
     import paper_2609_33977_amd as gm
     Wp, chunk, scale, rowptr = _pack(d, g)
     Yp = empty_bf16(T, d_out)
     gm.gm_packed_linear_fwd(d["X"], Wp, chunk, scale, rowptr, d_out, g, Yp)
     sync()
-    assert_close("Y packed", host_f64_from_bf16(Yp), Yr)
+    assert_close("Y packed", host_f64_from_bf16(Yp), Yr, bound=bY)
 
 
 @pytest.mark.parametrize("T", [1, 8])
@@ -291,8 +293,8 @@ def test_decode_degenerate_rows(T):
     m[20:24, d_in // g - 1] = 1.0
     d = _dev_case(case, m)
     Y = _fwd(d, g)
-    Yr, _, _ = _oracle_all(case, m)
-    assert_close("Y", host_f64_from_bf16(Y), Yr)
+    Yr, _, _, bY, _, _ = _oracle_all(case, m)
+    assert_close("Y", host_f64_from_bf16(Y), Yr, bound=bY)
     assert not np.any(host_bits(Y)[:, 8:16] & 0x7FFF), "pruned rows must be exactly zero"
     zeros = np.zeros_like(m)
     Yz = _fwd(_dev_case(case, zeros), g)

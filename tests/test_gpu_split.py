@@ -10,7 +10,8 @@ import pytest
 
 import oracle
 import workloads
-from gpu_support import assert_close, dev_bf16, dev_f32, empty_bf16, host_bits, host_f64_from_bf16, say, sync, workspace
+from gpu_support import (assert_close, assert_fwd, dev_bf16, dev_f32, empty_bf16, host_bits, host_f64_from_bf16, ref_fwd,
+                         say, sync, workspace)
 
 pytestmark = pytest.mark.gpu
 
@@ -37,9 +38,9 @@ def _check(case, mask, g_out=1):
     Ys = _run(X, W, m, g, g_out, T, d_out, ws)
     Ys2 = _run(X, W, m, g, g_out, T, d_out, ws)
     Yu = _run(X, W, m, g, g_out, T, d_out, None)
-    ref = oracle.linear_fwd(oracle.from_bf16(case.X), oracle.from_bf16(case.W), mask, g, g_out)
-    assert_close("Y (split K)", host_f64_from_bf16(Ys), ref)
-    assert_close("Y (unsplit)", host_f64_from_bf16(Yu), ref)
+    ref, b = ref_fwd(oracle.from_bf16(case.X), oracle.from_bf16(case.W), mask, g, g_out)
+    assert_close("Y (split K)", host_f64_from_bf16(Ys), ref, bound=b)
+    assert_close("Y (unsplit)", host_f64_from_bf16(Yu), ref, bound=b)
     assert np.array_equal(host_bits(Ys), host_bits(Ys2)), "split-K forward is not deterministic"
     return Ys
 
@@ -108,6 +109,5 @@ def test_split_forward_llama2_13b_t512(name, d_out, d_in):
     Y = _run(dev_bf16(X), dev_bf16(W), dev_f32(mask), g, 1, T, d_out, workspace(_split_bytes(T, d_in, d_out, g)))
     rows = np.sort(r.choice(d_out, size=96, replace=False))
     Wr = oracle.from_bf16(W[rows])
-    ref = oracle.linear_fwd(oracle.from_bf16(X), Wr, mask[rows], g)
-    assert_close("Y (sampled rows)", host_f64_from_bf16(Y)[:, rows], ref)
+    assert_fwd("Y (sampled rows)", host_f64_from_bf16(Y)[:, rows], oracle.from_bf16(X), Wr, mask[rows], g)
     del torch, gm

@@ -8,8 +8,8 @@ import pytest
 
 import oracle
 import workloads
-from gpu_support import (assert_close, dev_bf16, dev_f32, empty_bf16, empty_f32, host_bits, host_f64_from_bf16, say,
-                         sync, workspace)
+from gpu_support import (assert_close, assert_dgate, assert_dx, assert_fwd, dev_bf16, dev_f32, empty_bf16, empty_f32,
+                         host_bits, host_f64_from_bf16, ref_dgate, ref_dx, ref_fwd, say, sync, workspace)
 
 pytestmark = pytest.mark.gpu
 
@@ -41,11 +41,13 @@ def _bwd(d, g, want_dx=True, want_dgate=True):
 
 
 def _oracle(case, mask=None):
+    """Oracle Y, dX, dgate and their elementwise error bounds."""
     m = case.mask if mask is None else mask
     X, W, dY = oracle.from_bf16(case.X), oracle.from_bf16(case.W), oracle.from_bf16(case.dY)
-    Y = oracle.linear_fwd(X, W, m, case.g, case.g_out)
-    dX, dgate = oracle.linear_bwd(dY, X, W, m, case.g, case.g_out)
-    return Y, dX, dgate
+    Y, bY = ref_fwd(X, W, m, case.g, case.g_out)
+    dX, bdX = ref_dx(dY, W, m, case.g, case.g_out)
+    dgate, bdg = ref_dgate(dY, X, W, case.g, case.g_out)
+    return Y, dX, dgate, bY, bdX, bdg
 
 
 def _case(key, T, d_in, d_out, g, kept=None):
@@ -69,10 +71,10 @@ def test_square_fwd_bwd_parity(T, d_in, d_out, g):
     d = _dev(case)
     Y = _fwd(d, g)
     dX, dgate = _bwd(d, g)
-    Yr, dXr, dgr = _oracle(case)
-    assert_close("Y", host_f64_from_bf16(Y), Yr)
-    assert_close("dX", host_f64_from_bf16(dX), dXr)
-    assert_close("dgate", dgate.cpu().numpy(), dgr)
+    Yr, dXr, dgr, bY, bdX, bdg = _oracle(case)
+    assert_close("Y", host_f64_from_bf16(Y), Yr, bound=bY)
+    assert_close("dX", host_f64_from_bf16(dX), dXr, bound=bdX)
+    assert_close("dgate", dgate.cpu().numpy(), dgr, bound=bdg)
 
 
 @pytest.mark.parametrize("g", [16, 32, 64, 128])
@@ -86,10 +88,10 @@ def test_square_soft_mask(g):
     d = _dev(case, soft)
     Y = _fwd(d, g)
     dX, dgate = _bwd(d, g)
-    Yr, dXr, dgr = _oracle(case, soft)
-    assert_close("Y", host_f64_from_bf16(Y), Yr)
-    assert_close("dX", host_f64_from_bf16(dX), dXr)
-    assert_close("dgate", dgate.cpu().numpy(), dgr)
+    Yr, dXr, dgr, bY, bdX, bdg = _oracle(case, soft)
+    assert_close("Y", host_f64_from_bf16(Y), Yr, bound=bY)
+    assert_close("dX", host_f64_from_bf16(dX), dXr, bound=bdX)
+    assert_close("dgate", dgate.cpu().numpy(), dgr, bound=bdg)
 
 
 @pytest.mark.parametrize("g", [16, 128])
@@ -101,17 +103,17 @@ def test_square_dense_and_empty_masks(g):
     d = _dev(case, ones)
     Y = _fwd(d, g)
     dX, _ = _bwd(d, g, want_dgate=False)
-    Yr, dXr, _ = _oracle(case, ones)
-    assert_close("Y (dense)", host_f64_from_bf16(Y), Yr)
-    assert_close("dX (dense)", host_f64_from_bf16(dX), dXr)
+    Yr, dXr, _, bY, bdX, _ = _oracle(case, ones)
+    assert_close("Y (dense)", host_f64_from_bf16(Y), Yr, bound=bY)
+    assert_close("dX (dense)", host_f64_from_bf16(dX), dXr, bound=bdX)
     say(f"square {g}x{g}: all-zeros mask")
     d = _dev(case, zeros)
     Y = _fwd(d, g)
     dX, dgate = _bwd(d, g)
     assert not np.any(host_bits(Y) & 0x7FFF)
     assert not np.any(host_bits(dX) & 0x7FFF)
-    _, _, dgr = _oracle(case, zeros)
-    assert_close("dgate (all pruned)", dgate.cpu().numpy(), dgr)
+    _, _, dgr, _, _, bdg = _oracle(case, zeros)
+    assert_close("dgate (all pruned)", dgate.cpu().numpy(), dgr, bound=bdg)
 
 
 def test_square_one_group_per_unit_kept():
@@ -126,10 +128,10 @@ def test_square_one_group_per_unit_kept():
     d = _dev(case, checker)
     Y = _fwd(d, g)
     dX, dgate = _bwd(d, g)
-    Yr, dXr, dgr = _oracle(case, checker)
-    assert_close("Y", host_f64_from_bf16(Y), Yr)
-    assert_close("dX", host_f64_from_bf16(dX), dXr)
-    assert_close("dgate", dgate.cpu().numpy(), dgr)
+    Yr, dXr, dgr, bY, bdX, bdg = _oracle(case, checker)
+    assert_close("Y", host_f64_from_bf16(Y), Yr, bound=bY)
+    assert_close("dX", host_f64_from_bf16(dX), dXr, bound=bdX)
+    assert_close("dgate", dgate.cpu().numpy(), dgr, bound=bdg)
 
 
 @pytest.mark.parametrize("g", [16, 64])
@@ -156,8 +158,8 @@ def test_square_decode_forward(T, g, d_in):
     case = _case((226, T, g), T, d_in, d_out, g)
     d = _dev(case)
     Y = _fwd(d, g)
-    Yr, _, _ = _oracle(case)
-    assert_close("Y", host_f64_from_bf16(Y), Yr)
+    Yr, _, _, bY, _, _ = _oracle(case)
+    assert_close("Y", host_f64_from_bf16(Y), Yr, bound=bY)
 
 
 @pytest.mark.parametrize("g", [16, 32, 128])
@@ -189,9 +191,9 @@ def test_square_export_and_packed_forward(g):
     Y = empty_bf16(16, d_out)
     gm.gm_packed_linear_fwd(d["X"], Wp, chunk, scale, rowptr, d_out, g, Y)
     sync()
-    Yr, _, _ = _oracle(case, soft)
-    assert_close("Y (packed)", host_f64_from_bf16(Y), Yr)
-    assert_close("Y (in place, 16-token MFMA path)", host_f64_from_bf16(_fwd(d, g)), Yr)
+    Yr, _, _, bY, _, _ = _oracle(case, soft)
+    assert_close("Y (packed)", host_f64_from_bf16(Y), Yr, bound=bY)
+    assert_close("Y (in place, 16-token MFMA path)", host_f64_from_bf16(_fwd(d, g)), Yr, bound=bY)
 
 
 @pytest.mark.parametrize("g", [16, 64])
@@ -212,10 +214,9 @@ def test_square_llama2_7b_down_projection(g):
     t_s = np.sort(r.choice(T, size=32, replace=False))
     u_s = np.sort(r.choice(d_out // g, size=4, replace=False))
     rows = (u_s[:, None] * g + np.arange(g)[None, :]).reshape(-1)
-    assert_close("Y (sampled tokens)", host_f64_from_bf16(Y)[t_s], oracle.linear_fwd(X[t_s], W, m, g, g))
-    assert_close("dX (sampled tokens)", host_f64_from_bf16(dX)[t_s], oracle.linear_bwd_dx(dY[t_s], W, m, g, g))
-    assert_close("dgate (sampled group rows)", dgate.cpu().numpy()[u_s],
-                 oracle.linear_bwd_dgate(dY[:, rows], X, W[rows], g, g))
+    assert_fwd("Y (sampled tokens)", host_f64_from_bf16(Y)[t_s], X, W, m, g, g, rows=t_s)
+    assert_dx("dX (sampled tokens)", host_f64_from_bf16(dX)[t_s], dY, W, m, g, g, rows=t_s)
+    assert_dgate("dgate (sampled group rows)", dgate.cpu().numpy()[u_s], dY[:, rows], X, W[rows], g, g)
 
 
 def test_square_16_widest_rows():
@@ -227,10 +228,11 @@ def test_square_16_widest_rows():
     d = _dev(case)
     Y = _fwd(d, g)
     dX, dgate = _bwd(d, g)
-    Yr, dXr, dgr = _oracle(case)
-    assert_close("Y", host_f64_from_bf16(Y), Yr)
-    assert_close("dX", host_f64_from_bf16(dX), dXr)
-    assert_close("dgate", dgate.cpu().numpy(), dgr)
+    Yr, dXr, dgr, bY, bdX, bdg = _oracle(case)
+    assert_close("Y", host_f64_from_bf16(Y), Yr, bound=bY)
+    assert_close("dX", host_f64_from_bf16(dX), dXr, bound=bdX)
+    assert_close("dgate", dgate.cpu().numpy(), dgr, bound=bdg)
     case1 = _case((232,), 3, d_in, d_out, g)
     Y1 = _fwd(_dev(case1), g)
-    assert_close("Y (decode)", host_f64_from_bf16(Y1), _oracle(case1)[0])
+    o1 = _oracle(case1)
+    assert_close("Y (decode)", host_f64_from_bf16(Y1), o1[0], bound=o1[3])

@@ -18,6 +18,7 @@ from .gen import (  # noqa: F401
     f32_from_bf16_bits,
     draw_uniform_noise,
     budgeted_gate_inputs,
+    independent_gate_inputs,
     random_kept_mask,
     kept_counts_uniform_law,
     kept_counts_beta_law,

@@ -56,7 +56,8 @@ def random_kept_mask(rng: np.random.Generator, n_groups: int, kept: int) -> np.n
 
 
 def budgeted_gate_inputs(rng: np.random.Generator, keep: np.ndarray):
-    """Logits and uniform noise whose hard gate decision equals ``keep``.
+    """Logits and uniform noise whose hard gate decision equals ``keep`` (for tests of the
+    products given a mask; the gate itself is exercised on ``independent_gate_inputs``).
 
     The relaxed gate keeps a group when logit + (ln u - ln(1-u)) > 0.  The noise
     term is positive exactly when u > 1/2, so drawing |N(0,1)| logits with
@@ -73,6 +74,19 @@ def budgeted_gate_inputs(rng: np.random.Generator, keep: np.ndarray):
     u_lo = draw_uniform_noise(rng, n, "lo")
     noise = np.where(keep, u_hi, u_lo).astype(np.float32)
     return logits, noise
+
+
+def independent_gate_inputs(rng: np.random.Generator, n: int, loc=0.0):
+    """Gate logits ~ N(loc, 1) and uniform noise u ~ U(0, 1), drawn independently of each other.
+
+    ``loc`` (a scalar or one value per selector) is the caller's offset of the
+    logits; it is how a caller meets a kept budget other than the one half that
+    loc = 0 gives on average.  Nothing here evaluates the gate: which groups
+    such inputs keep is decided by the gate itself.
+    """
+    z = rng.standard_normal(n)
+    logits = (z + np.asarray(loc, dtype=np.float64)).astype(np.float32)
+    return logits, draw_uniform_noise(rng, n)
 
 
 def kept_counts_uniform_law(rng: np.random.Generator, n_groups: Sequence[int], lo: float, hi: float):
