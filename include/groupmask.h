@@ -45,7 +45,14 @@ extern "C" {
 /* Same object as a hipStream_t, declared here so that callers need no HIP headers. */
 typedef struct ihipStream_t* gm_stream_t;
 
-typedef enum gm_status {
+/* Status codes.  In C++ the enumeration has int as its fixed underlying type,
+ * so that every int a C caller passes (gm_status_string(99) included) is a
+ * valid value of it. */
+typedef enum gm_status
+#ifdef __cplusplus
+    : int
+#endif
+{
   GM_OK = 0,
   GM_ERR_NULL = 1,      /* a required pointer is NULL */
   GM_ERR_SHAPE = 2,     /* a size is out of range or inconsistent */

@@ -28,11 +28,25 @@ bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// With the environment variable GM_DEBUG set, the HIP error behind a
-// GM_ERR_DEVICE status is printed to stderr.
+// Debug modes, read once from the environment variable GM_DEBUG:
+//   unset   no reporting;
+//   "sync"  every launch is followed by a device-wide synchronisation and an
+//           error check, so a fault is reported by the entry point that caused
+//           it (GM_ERR_DEVICE) instead of by a later call (not for use under
+//           graph capture);
+//   other   the HIP error behind a GM_ERR_DEVICE status is printed to stderr
+//           (also in "sync" mode).
+int debug_mode() {
+  static const int mode = [] {
+    const char* v = std::getenv("GM_DEBUG");
+    if (v == nullptr) return 0;
+    return std::strcmp(v, "sync") == 0 ? 2 : 1;
+  }();
+  return mode;
+}
+
 gm_status device_error(const char* what, hipError_t e) {
-  static const bool debug = std::getenv("GM_DEBUG") != nullptr;
-  if (debug) std::fprintf(stderr, "libgroupmask: %s: HIP error %d (%s)\n", what, int(e), hipGetErrorName(e));
+  if (debug_mode()) std::fprintf(stderr, "libgroupmask: %s: HIP error %d (%s)\n", what, int(e), hipGetErrorName(e));
   return GM_ERR_DEVICE;
 }
 
@@ -52,7 +66,14 @@ gm_status check_device() {
   return ok[dev] == 1 ? GM_OK : device_error("not a gfx950 device", hipErrorInvalidDevice);
 }
 
-gm_status from_hip(hipError_t e) { return e == hipSuccess ? GM_OK : device_error("kernel launch", e); }
+gm_status from_hip(hipError_t e) {
+  if (e != hipSuccess) return device_error("kernel launch", e);
+  if (debug_mode() == 2) {
+    if (hipError_t s = hipDeviceSynchronize()) return device_error("kernel execution (GM_DEBUG=sync)", s);
+    if (hipError_t s = hipGetLastError()) return device_error("after synchronisation (GM_DEBUG=sync)", s);
+  }
+  return GM_OK;
+}
 
 gm_status check_tau(float tau) { return (std::isfinite(tau) && tau > 0.0f) ? GM_OK : GM_ERR_VALUE; }
 

@@ -305,3 +305,43 @@ def test_hyper_workspace_and_argument_errors():
     assert L.gm_adamw(FAKE, FAKE, FAKE, FAKE, -1, 1e-3, 0.9, 0.999, 1e-8, 0.05, 1, None) == gm.GM_ERR_SHAPE
     assert L.gm_adamw(FAKE, FAKE, FAKE, FAKE, 10, 1e-3, 0.9, 0.999, 1e-8, 0.05, 0, None) == gm.GM_ERR_VALUE
     assert L.gm_adamw(FAKE, FAKE, FAKE, FAKE, 0, 1e-3, 0.9, 0.999, 1e-8, 0.05, 1, None) == gm.GM_OK
+
+
+# ------------------------------------------------- the binding checks its tensors
+
+def _t(shape, dtype):
+    import torch
+    return torch.zeros(shape, dtype=dtype)
+
+
+def test_binding_rejects_wrong_dtypes_and_short_outputs_before_the_call():
+    import torch
+    T, d_in, d_out, g = 32, 512, 256, 256
+    X, W = _t((T, d_in), torch.bfloat16), _t((d_out, d_in), torch.bfloat16)
+    mask, Y = _t((d_out, d_in // g), torch.float32), _t((T, d_out), torch.bfloat16)
+    cases = [
+        (lambda: gm.gm_masked_linear_fwd(X.float(), W, mask, g, Y), "X must be torch.bfloat16"),
+        (lambda: gm.gm_masked_linear_fwd(X, W[:, :256], mask, g, Y), "W must have shape"),
+        (lambda: gm.gm_masked_linear_fwd(X, W, mask[:-1], g, Y), "mask must hold 512 elements"),
+        (lambda: gm.gm_masked_linear_fwd(X, W, mask.double(), g, Y), "mask must be torch.float32"),
+        (lambda: gm.gm_masked_linear_fwd(X, W, mask, g, Y[:-1]), "Y must have shape"),
+        (lambda: gm.gm_masked_linear_fwd(X, W, mask, 100, Y), "not tiled by"),
+        (lambda: gm.gm_masked_linear_bwd(Y, X, W, mask, g, X[:-1], None), "dX must have shape"),
+        (lambda: gm.gm_masked_linear_bwd(Y, X, W, mask, g, None, mask[:, :1]), "dgate must hold"),
+        (lambda: gm.gm_masked_linear_bwd(Y[:, :8], X, W, mask, g, X, None), "dY must have shape"),
+        (lambda: gm.gm_masked_linear_bwd(Y, X, W, None, g, X, None), "mask is required"),
+        (lambda: gm.gm_gate(mask, mask[:1], 0.5, True, mask), "noise must hold"),
+        (lambda: gm.gm_gate(mask, None, 0.5, True, Y), "mask_out must be torch.float32"),
+        (lambda: gm.gm_gate_bwd(mask, mask, 0.5, mask[1:]), "dlogits must hold"),
+        (lambda: gm.gm_adamw(mask, mask, mask, mask[1:], 1e-3, 0.9, 0.999, 1e-8, 0.0, 1), "v must hold"),
+        (lambda: gm.gm_pack_rows(W, mask, g, 10, Y, _t(10, torch.int32), _t(10, torch.float32),
+                                 _t(d_out, torch.int32)), "rowptr must hold"),
+    ]
+    for call, msg in cases:
+        with pytest.raises(ValueError, match=msg):
+            call()
+    # well-formed host tensors get as far as the device check
+    with pytest.raises(ValueError, match="must live on the GPU"):
+        gm.gm_masked_linear_fwd(X, W, mask, g, Y)
+    with pytest.raises(ValueError, match="must be contiguous"):
+        gm.gm_gate_bwd(mask.t(), mask.t(), 0.5, mask.t())
