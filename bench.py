@@ -3,19 +3,28 @@
 
 A step is one pass of the whole hot path over one batch: gate (Gumbel-Sigmoid,
 hard STE forward) -> masked forward -> backward (dX and dgate) -> gate backward.
-The headline workload is a LLaMA-2-7B attention projection: W [4096, 4096],
-X [4096 tokens, 4096], 1x256 groups, half of the 65,536 groups kept at random.
+The headline workload is the whole LLaMA-2-7B mask-learning step: all 224
+masked linears (32 layers x q, k, v, o 4096x4096, gate, up 11008x4096, down
+4096x11008), T = 4096 tokens (2 x 2048), 1x256 groups, per-matrix budgets from
+a Beta(2,2) law rescaled to 50 % of the 25,296,896 groups, one gate and one
+STE call over all selectors.
 
 Counted work per step: kept FLOPs 2*T*nnz for the forward and for dX, dense
 FLOPs 2*T*d_out*d_in for dgate (every selector receives a gradient).  Inputs
-are seeded synthetic tensors resident in HBM before timing starts.
+are seeded synthetic tensors resident in HBM before timing starts; the gate
+inputs are independent draws (logits ~ N(0,1), u ~ U(0,1)) shifted per matrix,
+with the library's own gate deciding, so that each matrix keeps its budget.
 
 The JSON line also carries the roofline of the dominant kernel (dgate), the
-fp64 oracle timed on the host cores as a reported baseline, the decode GEMV
-bandwidth on LLaMA-2-13B shapes, the sparsity-budget regulariser over the
-LLaMA-2-7B selectors, the same step with square g x g groups, and the
-distillation loss through the LLaMA-2-7B LM head, and the hypernetwork that
-generates the LLaMA-2-7B selector logits (forward, and backward with AdamW).
+gate's HBM bandwidth over all 25.3 M selectors with its near-threshold count,
+the fp64 oracle timed on the host cores (every workload, sampled where stated),
+the single-linear latency, the LLaMA-2-7B attention projection and MLP-trio
+steps, the decode GEMV bandwidth on LLaMA-2-13B shapes, the LLaMA-2-13B group
+size sweep and T = 512 forward, the sparsity-budget regulariser, square
+groups, the distillation loss and the hypernetwork.
+
+`--summarize-trace CSV` and `--summarize-counters CSV` print the rocprofv3
+kernel-trace and counter summaries that profiles/ holds (per kernel and grid).
 """
 from __future__ import annotations
 
@@ -34,14 +43,20 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 GEMM_SOURCES = ["paper_2609_33977_amd/csrc/gemm.hip", "paper_2609_33977_amd/csrc/gm_gemm.h", "paper_2609_33977_amd/csrc/gm_pipe.h",
                 "paper_2609_33977_amd/csrc/gm_device.h"]
 
-# HBM traffic of one dgate_kernel<256> launch on the headline workload, from
-# rocprofv3 --pmc FETCH_SIZE and --pmc WRITE_SIZE runs (KiB per dispatch),
-# calibrated with a 256 MiB device-to-device copy measured by the same counters
-# (FETCH_SIZE read 0.5x and WRITE_SIZE 1.0x of the copied bytes).  The numbers
-# describe the kernel built from sources with this digest and are reported only
-# while the sources still match it.
-DGATE_TRAFFIC = {"sources_sha256": "a3b8bb64f8810ea7c4eae14e95d0361ea53e73acac886544ad51170511a02331",
-                 "fetch_kib": 114785.0, "write_kib": 256.0, "fetch_scale": 2.0, "write_scale": 1.0}
+# HBM traffic of the roofline kernel, dgate_kernel<256, 1>, averaged over the
+# launches of the headline step (128 of 4096x4096, 64 of 11008x4096, 32 of
+# 4096x11008), from rocprofv3 --pmc FETCH_SIZE and --pmc WRITE_SIZE runs (KiB
+# per dispatch), calibrated with a device-to-device copy of known size measured
+# by the same counters (FETCH_SIZE read 0.5x and WRITE_SIZE 1.0x of the copied
+# bytes).  The numbers describe the kernel built from sources with this digest
+# and are reported only while the sources still match it (None: not measured).
+DGATE_TRAFFIC = {"sources_sha256": None, "fetch_kib": None, "write_kib": None, "fetch_scale": 2.0,
+                 "write_scale": 1.0}
+
+
+def _progress(msg: str) -> None:
+    """One line per leg on stderr (stdout carries only the JSON line)."""
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
 
 
 def _sources_digest() -> str:
@@ -63,44 +78,25 @@ def _dgate_traffic_bytes():
 def _parse():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=200)
-    ap.add_argument("--cpu-seconds", type=float, default=12.0,
-                    help="approximate host time spent timing the oracle baseline")
+    ap.add_argument("--steps", type=int, default=20, help="timed headline steps (each about 0.12 s)")
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--reps", type=int, default=10, help="repetitions of each secondary measurement")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gemv", action="store_true")
     ap.add_argument("--no-square", action="store_true")
     ap.add_argument("--no-distill", action="store_true")
     ap.add_argument("--no-hyper", action="store_true")
-    ap.add_argument("--no-model", action="store_true", help="skip the MLP-trio and whole-LLaMA-2-7B steps")
+    ap.add_argument("--no-model", action="store_true",
+                    help="skip the single-linear, attention-projection and MLP-trio steps")
     ap.add_argument("--no-sweep", action="store_true", help="skip the LLaMA-2-13B T=8192 sweep")
     ap.add_argument("--no-prefill", action="store_true", help="skip the LLaMA-2-13B T=512 forward")
     ap.add_argument("--gemv-layers", type=int, default=40)
     ap.add_argument("--profile-copy-mib", type=int, default=0,
-                    help="also run a plain device copy of this size (counter calibration runs)")
+                    help="also copy this many MiB device to device once (calibrates the HBM byte counters)")
+    ap.add_argument("--summarize-trace", metavar="CSV", help="print the summary of a rocprofv3 kernel trace and exit")
+    ap.add_argument("--summarize-counters", metavar="CSV",
+                    help="print the per-dispatch summary of a rocprofv3 counter collection and exit")
     return ap.parse_args()
-
-
-# ------------------------------------------------------------------ inputs
-
-def _headline_case():
-    import workloads
-    cfg = workloads.config("attn_4096")
-    _, d_out, d_in = cfg["linears"][0]
-    case = workloads.make_linear_case((2, 0, 0), cfg["T"], d_in, d_out, cfg["g"], None, tau=cfg["tau"])
-    return cfg, case
-
-
-def _to_device(case):
-    import torch
-
-    def bf16(bits):
-        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
-
-    def f32(a):
-        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
-
-    return dict(X=bf16(case.X), W=bf16(case.W), dY=bf16(case.dY), logits=f32(case.logits), noise=f32(case.noise))
 
 
 # ------------------------------------------------------------------ the step
@@ -176,11 +172,39 @@ def _events_batch_ms(fn, n):
     return float(start.elapsed_time(end)) / n
 
 
+def _shift_to_budget(gm, logits, noise, sizes, kept, tau, iters=64):
+    """Logits shifted by one offset per selector matrix so that the library's own hard gate keeps
+    exactly kept[l] of matrix l's selectors (bisection on the offsets, all matrices at once; nothing
+    here evaluates the gate's noise transform).  Returns the shifted logits."""
+    import torch
+    dev = logits.device
+    L = len(sizes)
+    seg = torch.repeat_interleave(torch.arange(L, device=dev), torch.tensor(sizes, device=dev))
+    want = torch.tensor(kept, dtype=torch.float64, device=dev)
+    lo = torch.full((L,), -24.0, dtype=torch.float64, device=dev)
+    hi = torch.full((L,), 24.0, dtype=torch.float64, device=dev)
+    mask = torch.empty_like(logits)
+    for _ in range(iters):
+        c = 0.5 * (lo + hi)
+        gm.gm_gate(logits + c.float()[seg], noise, tau, True, mask)
+        cnt = torch.zeros(L, dtype=torch.float64, device=dev).index_add_(0, seg, mask.double())
+        eq = cnt == want
+        lo = torch.where(eq | (cnt < want), c, lo)
+        hi = torch.where(eq | (cnt > want), c, hi)
+        if bool(eq.all()):
+            break
+    c = 0.5 * (lo + hi)
+    out = logits + c.float()[seg]
+    del seg, mask
+    return out
+
+
 class ModelStep:
     """One mask-learning step over several masked linears whose selectors share one flat array: one gate
     call over all of them, every linear's forward, every linear's backward (dX and dgate, last linear
-    first), one STE call.  Each linear has its own X, W and dY (drawn on the device); the kept set of
-    every selector matrix is drawn with its budget and encoded in the gate inputs."""
+    first), one STE call.  Each linear has its own X, W and dY (drawn on the device).  The gate inputs are
+    independent draws, logits ~ N(0,1) and u ~ U(0,1), with each matrix's logits shifted so that the
+    library's gate keeps exactly that matrix's budget."""
 
     def __init__(self, T, shapes, kept, g, tau, key):
         import torch
@@ -191,15 +215,16 @@ class ModelStep:
         sizes = [d_out * (d_in // g) for d_out, d_in in self.shapes]
         self.offsets = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
         n = int(self.offsets[-1])
-        r = workloads.gen.rng_for(*key)
-        logits, noise = np.empty(n, np.float32), np.empty(n, np.float32)
-        for l, (G, k) in enumerate(zip(sizes, kept)):
-            lo, hi = self.offsets[l], self.offsets[l + 1]
-            logits[lo:hi], noise[lo:hi] = workloads.budgeted_gate_inputs(r, workloads.random_kept_mask(r, G, k))
-        self.kept_total = int(sum(kept))
+        logits, noise = workloads.independent_gate_inputs(workloads.gen.rng_for(*key), n)
         dev = "cuda"
-        self.logits, self.noise = torch.from_numpy(logits).to(dev), torch.from_numpy(noise).to(dev)
+        self.noise = torch.from_numpy(noise).to(dev)
+        self.logits = _shift_to_budget(gm, torch.from_numpy(logits).to(dev), self.noise, sizes, kept, tau)
         self.mask, self.soft, self.dgate, self.dlogits = (torch.empty(n, device=dev) for _ in range(4))
+        self.gate()
+        seg_kept = [int(self.mask[int(a):int(b)].sum().item()) for a, b in zip(self.offsets[:-1], self.offsets[1:])]
+        self.kept = seg_kept
+        self.kept_total = int(sum(seg_kept))
+        self.kept_target = int(sum(kept))
         gen = torch.Generator(device=dev)
         gen.manual_seed(workloads.SEED + 1000 * key[0] + key[1])
         self.lin = []
@@ -217,7 +242,7 @@ class ModelStep:
             bws = max(bws, gm.gm_workspace_size(gm.GM_OP_BWD, T, d_in, d_out, g))
         self.fws = torch.empty(fws, dtype=torch.uint8, device=dev)
         self.ws = torch.empty(bws, dtype=torch.uint8, device=dev)
-        kept_params = [k * g for k in kept]
+        kept_params = [k * g for k in self.kept]
         self.flops = {"fwd": sum(2.0 * T * p for p in kept_params), "dx": sum(2.0 * T * p for p in kept_params),
                       "dgate": sum(2.0 * T * d_out * d_in for d_out, d_in in self.shapes)}
 
@@ -232,8 +257,16 @@ class ModelStep:
         for X, W, dY, _, dX, m, dg in reversed(self.lin):
             self.gm.gm_masked_linear_bwd(dY, X, W, m, self.g, dX, dg, self.ws)
 
+    def dgate_only(self):
+        for X, W, dY, _, _, m, dg in reversed(self.lin):
+            self.gm.gm_masked_linear_bwd(dY, X, W, m, self.g, None, dg, self.ws)
+
     def gate_bwd(self):
         self.gm.gm_gate_bwd(self.dgate, self.soft, self.tau, self.dlogits)
+
+    def near_threshold(self, band=1e-6):
+        """Gates of the last gate pass whose relaxed value lies within band of 1/2 (the GPU's fp32 value)."""
+        return int(((self.soft - 0.5).abs() <= band).sum().item())
 
     def __call__(self):
         self.gate()
@@ -243,22 +276,65 @@ class ModelStep:
 
 
 def _model_step(step, reps, workload):
+    """Time a ModelStep: whole steps as one batch between HIP events, then each phase the same way."""
     import torch
     for _ in range(2):
         step()
     torch.cuda.synchronize()
-    if int(step.mask.sum().item()) != step.kept_total:
-        raise RuntimeError("gate kept count differs from the budget")
     ms = _events_batch_ms(step, reps)
-    fwd = _events_batch_ms(step.fwd, reps)
-    bwd = _events_batch_ms(step.bwd, reps)
+    ph = {name: _events_batch_ms(getattr(step, name), reps) for name in ("gate", "fwd", "bwd", "gate_bwd")}
     fl = step.flops
     total = sum(fl.values())
     return {"workload": workload, "linears": len(step.shapes), "selectors": int(step.offsets[-1]),
             "kept": step.kept_total, "TFLOP_per_step": total / 1e12, "ms_per_step": ms,
             "TFLOP/s": total / (ms / 1e3) / 1e12, "frac_of_bf16_peak": total / (ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
-            "fwd_ms": fwd, "fwd_kept_TFLOP/s": fl["fwd"] / (fwd / 1e3) / 1e12,
-            "bwd_ms": bwd, "bwd_TFLOP/s": (fl["dx"] + fl["dgate"]) / (bwd / 1e3) / 1e12}
+            "breakdown_ms": ph, "fwd_kept_TFLOP/s": fl["fwd"] / (ph["fwd"] / 1e3) / 1e12,
+            "bwd_TFLOP/s": (fl["dx"] + fl["dgate"]) / (ph["bwd"] / 1e3) / 1e12,
+            "near_threshold_gates": step.near_threshold()}
+
+
+def _dgate_roofline(step, reps):
+    """Every linear's dgate-only backward (one dgate_kernel launch each) back to back between two HIP events
+    on the launch stream: average launch duration and achieved TFLOP/s on the dense dgate FLOPs."""
+    import torch
+    step.dgate_only()
+    torch.cuda.synchronize()
+    batch = _events_batch_ms(step.dgate_only, reps)
+    n = len(step.lin)
+    return {"launches_per_batch": n, "avg_launch_ms": batch / n, "flops_per_launch": step.flops["dgate"] / n,
+            "achieved_TFLOP/s": step.flops["dgate"] / (batch / 1e3) / 1e12}
+
+
+def _single_linear(reps):
+    """Single masked linear (T 128, 1024 x 1024, 1x256 groups, half of 4096 groups kept, tau 0.5): a
+    latency figure (the step is far too small to fill the GPU)."""
+    import workloads
+    cfg = workloads.config("single_1024")
+    _, d_out, d_in = cfg["linears"][0]
+    g = cfg["g"]
+    step = ModelStep(cfg["T"], [(d_out, d_in)], [d_out * (d_in // g) // 2], g, cfg["tau"], (1, 1))
+    out = _model_step(step, reps, f"single masked linear: T {cfg['T']}, W {d_out}x{d_in}, 1x{g} groups, "
+                                  f"2048 of 4096 kept, tau {cfg['tau']}")
+    out["us_per_step"] = out["ms_per_step"] * 1e3
+    out["breakdown_us"] = {k: v * 1e3 for k, v in out.pop("breakdown_ms").items()}
+    return out
+
+
+def _attention_4096(reps):
+    """LLaMA-2-7B attention projection (T 4096, W 4096 x 4096, 1x256 groups, half kept): the step, its
+    per-phase times, its dgate roofline and the vendor dense GEMMs on the same tensors."""
+    import workloads
+    cfg = workloads.config("attn_4096")
+    _, d_out, d_in = cfg["linears"][0]
+    g = cfg["g"]
+    step = ModelStep(cfg["T"], [(d_out, d_in)], [d_out * (d_in // g) // 2], g, cfg["tau"], (2, 1))
+    out = _model_step(step, reps, f"LLaMA-2-7B attention projection: W {d_out}x{d_in}, X {cfg['T']} tokens "
+                                  f"(2 x 2048), 1x{g} groups, 50% of {d_out * (d_in // g)} kept")
+    out["dgate_roofline"] = _dgate_roofline(step, reps)
+    X, W, dY = step.lin[0][0], step.lin[0][1], step.lin[0][2]
+    out["dense_context"] = _dense_context(X, W, dY, out["breakdown_ms"], reps)
+    out["_step"] = step
+    return out
 
 
 def _mlp_trio(reps):
@@ -276,18 +352,19 @@ def _mlp_trio(reps):
     return out
 
 
-def _llama2_7b_step(reps):
-    """Every masked linear of LLaMA-2-7B (32 layers x 7 = 224), T 4096, Beta(2,2) budgets at 50 % overall."""
+def _llama2_7b_shapes():
     import workloads
     cfg = workloads.config("llama2_7b_step")
     g = cfg["g"]
     shapes = [(d_out, d_in) for _ in range(cfg["layers"]) for _, d_out, d_in in cfg["linears"]]
     sizes = [o * (i // g) for o, i in shapes]
     kept, _ = workloads.kept_counts_beta_law(workloads.gen.rng_for(4, 0), sizes, [o * i for o, i in shapes], 0.5)
-    step = ModelStep(cfg["T"], shapes, kept, g, cfg["tau"], (4, 1))
-    return _model_step(step, reps, "LLaMA-2-7B, all 224 masked linears (32 layers x q,k,v,o,gate,up,down), "
-                                   "T 4096, 1x256 groups, Beta(2,2) per-matrix budgets, 50% of 25,296,896 kept; "
-                                   "one gate and one STE call over all selectors")
+    return cfg, shapes, kept
+
+
+LLAMA2_7B_WORKLOAD = ("LLaMA-2-7B mask-learning step: all 224 masked linears (32 layers x q,k,v,o 4096x4096, "
+                      "gate,up 11008x4096, down 4096x11008), T 4096 (2 x 2048), 1x256 groups, Beta(2,2) per-matrix "
+                      "budgets at 50% of 25,296,896 groups; one gate and one STE call over all selectors")
 
 
 def _sweep_13b(reps):
@@ -363,14 +440,13 @@ def _prefill_13b(reps):
             "ms_per_layer": ms, "kept_TFLOP/s": fl / (ms / 1e3) / 1e12, "GB/s": by / (ms / 1e3) / 1e9}
 
 
-def _dense_context(d, breakdown, reps):
+def _dense_context(X, W, dY, breakdown, reps):
     """Context, not a target: the vendor dense GEMM (hipBLASLt through torch.matmul) on the three dense products
-    of the same training step on the headline tensors, Y = X W^T, dX = dY W and the weight gradient dW = dY^T X,
+    of the same training step on the same tensors, Y = X W^T, dX = dY W and the weight gradient dW = dY^T X,
     every operand contiguous and row-major (the transposed ones copied beforehand).  The masked step computes
     the forward on kept groups, dX over kept groups and the per-group gradient instead of dW; the ratio of the
     dense time to the masked forward + backward time is the figure to set beside a dense layer."""
     import torch
-    X, W, dY = d["X"], d["W"], d["dY"]
     Wt = W.t().contiguous()
     dYt = dY.t().contiguous()
     T, d_in = X.shape
@@ -394,14 +470,32 @@ def _dense_context(d, breakdown, reps):
 
 # ------------------------------------------------------------------ CPU baseline
 
-def _cpu_baseline(case, flops_per_step, budget_s):
-    """The fp64 oracle, as it stands, timed on this host over whole steps of the workload."""
-    import oracle
+def _cpu_info():
+    """Cores this process may run on, the BLAS thread pools NumPy uses, and the CPU model."""
+    cores = len(os.sched_getaffinity(0))
+    blas = []
     try:
         from threadpoolctl import threadpool_info
-        threads = max([int(i.get("num_threads", 1)) for i in threadpool_info()] or [1])
+        blas = [{"library": i.get("internal_api"), "threads": int(i.get("num_threads", 1))} for i in threadpool_info()]
     except Exception:
-        threads = len(os.sched_getaffinity(0))
+        pass
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    threads = max([b["threads"] for b in blas] or [cores])
+    return cores, threads, blas, model
+
+
+def _oracle_step_s(case, min_s):
+    """Seconds per whole step of the oracle on one linear (gate, fwd, dX, dgate, STE), fp64 NumPy; repeated
+    until min_s have passed (at least once).  The bf16 -> fp64 widening of the inputs is done beforehand."""
+    import oracle
     X, W, dY = oracle.from_bf16(case.X), oracle.from_bf16(case.W), oracle.from_bf16(case.dY)
     reps, t0 = 0, time.perf_counter()
     while True:
@@ -411,22 +505,97 @@ def _cpu_baseline(case, flops_per_step, budget_s):
         oracle.gate_bwd(dgate, y, case.tau)
         reps += 1
         el = time.perf_counter() - t0
-        if el >= budget_s or el / reps * (reps + 1) > 2.5 * budget_s:
-            break
-    sec = el / reps
-    return {"value": flops_per_step / sec / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
-            "sample": f"{reps} whole step(s) of the headline workload (gate, fwd, dX, dgate, STE) in fp64 NumPy, "
-                      f"{sec:.2f} s per step"}
+        if el >= min_s:
+            return el / reps, reps
+
+
+def _step_flops(T, d_in, d_out, kept, g):
+    return 2.0 * T * kept * g * 2 + 2.0 * T * d_out * d_in
+
+
+def _cpu_baseline(headline_flops):
+    """The fp64 oracle, as it stands, timed on this host for every workload: the single linear, the attention
+    projection and the MLP trio in full, the LLaMA-2-7B step as its first layer (7 linears) times 32, and the
+    LLaMA-2-13B decode / T = 512 forward over one layer per token count."""
+    import oracle
+    import workloads
+    cores, threads, blas, model = _cpu_info()
+    per = {}
+    c1 = workloads.config("single_1024")
+    _, d_out, d_in = c1["linears"][0]
+    case = workloads.make_linear_case((1, 0, 0), c1["T"], d_in, d_out, c1["g"], None, tau=c1["tau"])
+    sec, reps = _oracle_step_s(case, 1.0)
+    per["single_1024"] = {"s_per_step": sec, "reps": reps,
+                          "TFLOP/s": _step_flops(c1["T"], d_in, d_out, case.kept, c1["g"]) / sec / 1e12}
+    c2 = workloads.config("attn_4096")
+    _, d_out, d_in = c2["linears"][0]
+    case = workloads.make_linear_case((2, 0, 0), c2["T"], d_in, d_out, c2["g"], None, tau=c2["tau"])
+    sec, reps = _oracle_step_s(case, 1.0)
+    per["attn_4096"] = {"s_per_step": sec, "reps": reps,
+                        "TFLOP/s": _step_flops(c2["T"], d_in, d_out, case.kept, c2["g"]) / sec / 1e12}
+    c3 = workloads.config("mlp_trio_7b")
+    g = c3["g"]
+    kept3, _ = workloads.kept_counts_uniform_law(workloads.gen.rng_for(3, 0),
+                                                 [o * (i // g) for _, o, i in c3["linears"]], *c3["law"][1:])
+    sec3, fl3 = 0.0, 0.0
+    for j, (_, d_out, d_in) in enumerate(c3["linears"]):
+        case = workloads.make_linear_case((3, 0, j), c3["T"], d_in, d_out, g, kept3[j], tau=c3["tau"])
+        sec3 += _oracle_step_s(case, 0.0)[0]
+        fl3 += _step_flops(c3["T"], d_in, d_out, kept3[j], g)
+        del case
+    per["mlp_trio_7b"] = {"s_per_step": sec3, "TFLOP/s": fl3 / sec3 / 1e12}
+    c4, shapes, kept4 = _llama2_7b_shapes()
+    g = c4["g"]
+    sec4 = 0.0
+    for j, (d_out, d_in) in enumerate(shapes[:7]):
+        case = workloads.make_linear_case((4, 0, j), c4["T"], d_in, d_out, g, kept4[j], tau=c4["tau"])
+        sec4 += _oracle_step_s(case, 0.0)[0]
+        del case
+    per["llama2_7b_step"] = {"s_per_layer": sec4, "s_per_step": 32 * sec4,
+                             "TFLOP/s": headline_flops / (32 * sec4) / 1e12,
+                             "sample": "layer 0's seven linears, one whole step each; the step time is 32 x that"}
+    c5 = workloads.config("llama2_13b_infer")
+    g = c5["g"]
+    r = workloads.gen.rng_for(5, 7)
+    mats = []
+    for _, d_out, d_in in c5["linears"]:
+        W = oracle.from_bf16(workloads.bf16_bits_from_f32(r.standard_normal((d_out, d_in), dtype=np.float32)
+                                                          * np.float32(0.02)))
+        G = d_out * (d_in // g)
+        m = workloads.random_kept_mask(r, G, G // 2).reshape(d_out, d_in // g).astype(np.float64)
+        mats.append((W, m))
+    kept_bytes = sum(int(m.sum()) * g * 2 for _, m in mats)
+    for T in c5["T_decode"]:
+        xs = {}
+        t0 = time.perf_counter()
+        for (W, m), src in zip(mats, ("a", "a", "a", "o", "m", "m", "d")):
+            if (src, W.shape[1]) not in xs:
+                xs[(src, W.shape[1])] = oracle.from_bf16(workloads.bf16_bits_from_f32(
+                    r.standard_normal((T, W.shape[1]), dtype=np.float32)))
+            oracle.linear_fwd(xs[(src, W.shape[1])], W, m, g)
+        sec = time.perf_counter() - t0
+        per[f"llama2_13b_T{T}"] = {"s_per_layer": sec, "kept_GB/s": kept_bytes / sec / 1e9,
+                                   "kept_TFLOP/s": 2.0 * T * kept_bytes / 2 / sec / 1e12}
+    del mats
+    return {"value": per["llama2_7b_step"]["TFLOP/s"], "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": "LLaMA-2-7B step: layer 0's seven masked linears (q,k,v,o,gate,up,down at T 4096), one whole "
+                      "step each (gate, fwd, dX, dgate, STE) in fp64 NumPy, times 32 layers; value counted like "
+                      "the GPU figure (kept FLOPs for fwd and dX, dense for dgate)",
+            "affinity_cores": cores, "blas": blas, "cpu_model": model, "per_config": per}
 
 
 # ------------------------------------------------------------------ square groups
 
-def _square_groups(d, case, reps):
-    """The same step on the headline tensors with g x g groups (g = 16 .. 128), half of the groups kept."""
+def _square_groups(X, W, dY, tau, reps):
+    """The same step on the attention-projection tensors with g x g groups (g = 16 .. 128), half of the
+    groups kept at random (gate inputs encode the kept set: the subject here is the GEMMs)."""
     import torch
     import workloads
-    T, d_in, d_out = case.T, case.d_in, case.d_out
-    out = {"workload": f"headline tensors (T {T}, W {d_out}x{d_in}) with square g x g groups, 50% kept at random"}
+    T, d_in = X.shape
+    d_out = W.shape[0]
+    d = dict(X=X, W=W, dY=dY)
+    out = {"workload": f"attention-projection tensors (T {T}, W {d_out}x{d_in}) with square g x g groups, "
+                       "50% kept at random"}
     for g in (16, 32, 64, 128):
         G = (d_out // g) * (d_in // g)
         r = workloads.gen.rng_for(2, 1, g)
@@ -435,7 +604,7 @@ def _square_groups(d, case, reps):
         shape = (d_out // g, d_in // g)
         dd = dict(d, logits=torch.from_numpy(np.ascontiguousarray(logits.reshape(shape), dtype=np.float32)).cuda(),
                   noise=torch.from_numpy(np.ascontiguousarray(noise.reshape(shape), dtype=np.float32)).cuda())
-        step = Step(dd, g, case.tau, g_out=g)
+        step = Step(dd, g, tau, g_out=g)
         for _ in range(3):
             step()
         torch.cuda.synchronize()
@@ -744,8 +913,104 @@ def _budget_bandwidth(reps):
 
 # ------------------------------------------------------------------ main
 
+# ------------------------------------------------------------------ rocprofv3 summaries
+
+def _short_kernel(name: str) -> str:
+    """`void gm::dgate_kernel<256, 1>(...)` -> `gm::dgate_kernel<256, 1>`; other names cut at 60 characters."""
+    n = name[5:] if name.startswith("void ") else name
+    depth, out = 0, []
+    for ch in n:
+        if ch == "(" and depth == 0:
+            break
+        depth += ch == "<"
+        depth -= ch == ">"
+        out.append(ch)
+    n = "".join(out)
+    return n if n.startswith("gm::") else n[:60]
+
+
+def _runs(items, key):
+    """Maximal runs of consecutive items (in start order) for which key(item) is true: list of (first, last)."""
+    runs, start = [], None
+    for k, it in enumerate(items):
+        if key(it):
+            start = k if start is None else start
+        elif start is not None:
+            runs.append((start, k - 1))
+            start = None
+    if start is not None:
+        runs.append((start, len(items) - 1))
+    return runs
+
+
+def _trace_summary(path: str) -> str:
+    """Markdown summary of a rocprofv3 kernel_trace.csv: per kernel and workgroup count, dispatches and
+    duration statistics; then the longest back-to-back run of dgate_kernel<256, 1> dispatches (the
+    bench's roofline batches: every linear's dgate-only backward) with its mean launch duration."""
+    import csv
+    rows = []
+    with open(path, newline="") as f:
+        for r in csv.DictReader(f):
+            if r.get("Kind", "KERNEL_DISPATCH") != "KERNEL_DISPATCH":
+                continue
+            wg = int(r["Grid_Size_X"]) // max(int(r["Workgroup_Size_X"]), 1)
+            rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), _short_kernel(r["Kernel_Name"]), wg))
+    rows.sort()
+    total = sum(e - b for b, e, _, _ in rows) or 1
+    agg = {}
+    for b, e, k, wg in rows:
+        agg.setdefault((k, wg), []).append((e - b) / 1e3)
+    lines = [f"{len(rows)} dispatches, {total / 1e6:.2f} ms of kernel time", "",
+             "| kernel | workgroups | calls | mean µs | median µs | min µs | max µs | % of kernel time |",
+             "|---|---:|---:|---:|---:|---:|---:|---:|"]
+    for (k, wg), d in sorted(agg.items(), key=lambda kv: -sum(kv[1]))[:40]:
+        d = np.array(d)
+        lines.append(f"| `{k}` | {wg} | {d.size} | {d.mean():.1f} | {np.median(d):.1f} | {d.min():.1f} | "
+                     f"{d.max():.1f} | {100 * d.sum() * 1e3 / total:.2f} |")
+    dg = "gm::dgate_kernel<256, 1>"
+    runs = _runs(rows, lambda r: r[2] == dg)
+    if runs:
+        a, b = max(runs, key=lambda ab: ab[1] - ab[0])
+        d = np.array([(rows[k][1] - rows[k][0]) / 1e3 for k in range(a, b + 1)])
+        span = (rows[b][1] - rows[a][0]) / 1e3 / d.size
+        mix = {}
+        for k in range(a, b + 1):
+            mix[rows[k][3]] = mix.get(rows[k][3], 0) + 1
+        lines += ["", f"Longest back-to-back run of `{dg}`: {d.size} dispatches (workgroups: "
+                      + ", ".join(f"{w} x {c}" for w, c in sorted(mix.items())) + f"), mean {d.mean():.2f} µs, "
+                      f"median {np.median(d):.2f}, min {d.min():.2f}, max {d.max():.2f}; "
+                      f"first start to last end / dispatches = {span:.2f} µs"]
+    return "\n".join(lines)
+
+
+def _counter_summary(path: str) -> str:
+    """Markdown summary of a rocprofv3 counter_collection.csv: per kernel and workgroup count, the mean of
+    each counter per dispatch (summed over the counter's instances within a dispatch)."""
+    import csv
+    per = {}
+    with open(path, newline="") as f:
+        for r in csv.DictReader(f):
+            wg = int(r["Grid_Size"]) // max(int(r["Workgroup_Size"]), 1)
+            key = (_short_kernel(r["Kernel_Name"]), wg)
+            disp = per.setdefault(key, {}).setdefault(r["Dispatch_Id"], {})
+            disp[r["Counter_Name"]] = disp.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    names = sorted({c for d in per.values() for v in d.values() for c in v})
+    lines = ["| kernel | workgroups | dispatches | " + " | ".join(f"mean {n}" for n in names) + " |",
+             "|---|---:|---:|" + "---:|" * len(names)]
+    for (k, wg), d in sorted(per.items()):
+        vals = [np.mean([v.get(n, 0.0) for v in d.values()]) for n in names]
+        lines.append(f"| `{k}` | {wg} | {len(d)} | " + " | ".join(f"{x:.1f}" for x in vals) + " |")
+    return "\n".join(lines)
+
+
 def main():
     args = _parse()
+    if args.summarize_trace:
+        print(_trace_summary(args.summarize_trace))
+        return
+    if args.summarize_counters:
+        print(_counter_summary(args.summarize_counters))
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU; --gpus {args.gpus} is not supported (this build has no multi-GPU path).",
               file=sys.stderr)
@@ -756,35 +1021,41 @@ def main():
         sys.exit(2)
     import paper_2609_33977_amd  # noqa: F401  (fails loudly when the HIP library is missing)
 
-    cfg, case = _headline_case()
-    T, d_in, d_out, g = case.T, case.d_in, case.d_out, case.g
-    kept = case.kept
-    nnz = kept * g
-    flops = {"fwd": 2.0 * T * nnz, "dx": 2.0 * T * nnz, "dgate": 2.0 * T * d_out * d_in}
+    # ---- headline: the whole LLaMA-2-7B mask-learning step (224 masked linears)
+    _progress("headline: building the LLaMA-2-7B step (224 linears)")
+    cfg, shapes, kept = _llama2_7b_shapes()
+    step = ModelStep(cfg["T"], shapes, kept, cfg["g"], cfg["tau"], (4, 1))
+    if step.kept_total != step.kept_target:
+        raise RuntimeError(f"gate kept {step.kept_total} groups, budget {step.kept_target}")
+    flops = step.flops
     flops_step = sum(flops.values())
-
-    d = _to_device(case)
-    step = Step(d, g, case.tau)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    if int(step.mask.sum().item()) != kept:
-        raise RuntimeError("gate kept count differs from the budget")
-
-    torch.cuda.synchronize()
+    _progress(f"headline: {args.steps} timed steps")
     t0 = time.perf_counter()
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
     ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
     tflops = flops_step / (ms_per_step / 1e3) / 1e12
+    near = step.near_threshold()
 
-    # Per-call breakdown and the dominant kernel's launch duration (HIP events on the launch stream).
-    reps = max(args.steps, 5)
-    breakdown = {name: _events_ms(getattr(step, name), reps) for name in ("gate", "fwd", "bwd", "gate_bwd")}
-    dgate_ms = _events_batch_ms(step.dgate_only, reps)
-    dgate_tflops = flops["dgate"] / (dgate_ms / 1e3) / 1e12
-    fwd_tflops = flops["fwd"] / (breakdown["fwd"] / 1e3) / 1e12
+    reps = max(3, args.reps)
+    breakdown = {name: _events_batch_ms(getattr(step, name), reps) for name in ("gate", "fwd", "bwd", "gate_bwd")}
+    roof = _dgate_roofline(step, reps)
+    n_sel = int(step.offsets[-1])
+    gate_leg = {"workload": f"the step's gate over all {n_sel} selectors (one call) and its STE backward",
+                "selectors": n_sel, "gate_ms": breakdown["gate"],
+                "gate_GB/s": 16.0 * n_sel / (breakdown["gate"] / 1e3) / 1e9,
+                "gate_bwd_ms": breakdown["gate_bwd"],
+                "gate_bwd_GB/s": 12.0 * n_sel / (breakdown["gate_bwd"] / 1e3) / 1e9,
+                "bytes": {"gate": 16 * n_sel, "gate_bwd": 12 * n_sel},
+                "near_threshold_gates": near,
+                "near_threshold_rule": "GPU relaxed value within 1e-6 of 1/2 in the last timed step"}
+    gate_leg["gate_frac_of_hbm_peak"] = gate_leg["gate_GB/s"] / PEAK_HBM_GBS
+    del step
+    torch.cuda.empty_cache()
 
     if args.profile_copy_mib:
         src = torch.empty(args.profile_copy_mib << 20, dtype=torch.uint8, device="cuda").fill_(1)
@@ -792,41 +1063,37 @@ def main():
         for _ in range(3):
             dst.copy_(src)
         torch.cuda.synchronize()
+        del src, dst
 
-    dense = _dense_context(d, breakdown, reps)
-
-    gemv = None
-    if not args.no_gemv:
-        gemv = _gemv_bandwidth(args.gemv_layers, max(3, args.steps // 4))
-
-    budget = _budget_bandwidth(max(5, args.steps))
-
+    single = attn = mlp = None
     square = None
-    if not args.no_square:
-        square = _square_groups(d, case, max(5, args.steps // 2))
-
-    distill = None
-    if not args.no_distill:
-        distill = _distill(max(3, args.steps // 4))
-
-    hyper = None
-    if not args.no_hyper:
-        hyper = _hyper(max(3, args.steps // 4))
-
-    mlp = model = None
     if not args.no_model:
-        mlp = _mlp_trio(max(5, args.steps // 4))
-        model = _llama2_7b_step(max(3, args.steps // 40))
+        _progress("single linear, attention projection, square groups, MLP trio")
+        single = _single_linear(max(reps, 50))
+        attn = _attention_4096(reps)
+        a_step = attn.pop("_step")
+        if not args.no_square:
+            square = _square_groups(a_step.lin[0][0], a_step.lin[0][1], a_step.lin[0][2], a_step.tau, reps)
+        del a_step
+        torch.cuda.empty_cache()
+        mlp = _mlp_trio(reps)
+        torch.cuda.empty_cache()
 
-    sweep = prefill = None
-    if not args.no_sweep:
-        sweep = _sweep_13b(max(5, args.steps // 10))
-    if not args.no_prefill:
-        prefill = _prefill_13b(max(5, args.steps // 4))
+    _progress("decode GEMV, budget, distillation, hypernetwork, sweep, T=512 forward")
+    gemv = None if args.no_gemv else _gemv_bandwidth(args.gemv_layers, reps)
+    torch.cuda.empty_cache()
+    budget = _budget_bandwidth(reps)
+    distill = None if args.no_distill else _distill(reps)
+    torch.cuda.empty_cache()
+    hyper = None if args.no_hyper else _hyper(reps)
+    torch.cuda.empty_cache()
+    sweep = None if args.no_sweep else _sweep_13b(reps)
+    prefill = None if args.no_prefill else _prefill_13b(reps)
+    torch.cuda.empty_cache()
 
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = _cpu_baseline(case, flops_step, args.cpu_seconds)
+    _progress("oracle on the host")
+    cpu = None if args.no_cpu_baseline else _cpu_baseline(flops_step)
+    _progress("done")
 
     out = {
         "metric": "masked-linear fwd+bwd TFLOP/s & % bf16 MFMA peak; sparse GEMV GB/s",
@@ -841,26 +1108,34 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": "LLaMA-2-7B attention projection: W 4096x4096, X 4096 tokens (2 x 2048), "
-                               "1x256 groups, 50% of 65,536 groups kept at random; gate + fwd + dX + dgate + STE",
-                   "T": T, "d_in": d_in, "d_out": d_out, "g": g, "kept_groups": kept, "tau": case.tau},
+        "config": {"workload": LLAMA2_7B_WORKLOAD, "T": cfg["T"], "linears": len(shapes), "g": cfg["g"],
+                   "selectors": n_sel, "kept_groups": sum(kept), "tau": cfg["tau"],
+                   "TFLOP_per_step": flops_step / 1e12,
+                   "counting": "kept FLOPs 2*T*nnz for fwd and dX, dense 2*T*d_out*d_in for dgate"},
         "frac_of_bf16_peak": tflops / PEAK_BF16_TFLOPS,
-        "roofline": {"bound": "mfma", "achieved": dgate_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": dgate_tflops / PEAK_BF16_TFLOPS, "traffic": _dgate_traffic_bytes()},
-        "kernels": {"dominant": "dgate_kernel<256> (dY^T X tile + fused W-weighted group reduction)",
-                    "dgate_flops_per_launch": flops["dgate"], "dgate_avg_launch_ms": dgate_ms,
-                    "dgate_algorithmic_bytes": 2.0 * T * (d_in + d_out) + 2.0 * d_out * d_in + 4.0 * d_out * (d_in // g),
-                    "sources_sha256": _sources_digest(),
-                    "fwd_kept_tflops": fwd_tflops, "breakdown_ms": breakdown},
+        "roofline": {"bound": "mfma", "achieved": roof["achieved_TFLOP/s"], "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": roof["achieved_TFLOP/s"] / PEAK_BF16_TFLOPS,
+                     "traffic": _dgate_traffic_bytes()},
+        "kernels": {"dominant": "dgate_kernel<256, 1> (X^T dY tile + fused W-weighted group reduction), one launch "
+                                "per linear: 128 of 4096x4096, 64 of 11008x4096, 32 of 4096x11008 per step",
+                    "dgate_flops_per_launch": roof["flops_per_launch"], "dgate_avg_launch_ms": roof["avg_launch_ms"],
+                    "dgate_launches_per_batch": roof["launches_per_batch"],
+                    "dgate_algorithmic_bytes_per_launch": sum(2.0 * cfg["T"] * (di + do) + 2.0 * do * di
+                                                              + 4.0 * do * (di // cfg["g"]) for do, di in shapes)
+                                                          / len(shapes),
+                    "sources_sha256": _sources_digest(), "breakdown_ms": breakdown,
+                    "fwd_kept_TFLOP/s": flops["fwd"] / (breakdown["fwd"] / 1e3) / 1e12,
+                    "bwd_TFLOP/s": (flops["dx"] + flops["dgate"]) / (breakdown["bwd"] / 1e3) / 1e12},
+        "gate": gate_leg,
         "cpu_baseline": cpu,
-        "dense_context": dense,
+        "single_linear": single,
+        "attn_4096": attn,
+        "mlp_trio": mlp,
         "gemv": gemv,
         "budget": budget,
         "square_groups": square,
         "distill": distill,
         "hypernetwork": hyper,
-        "mlp_trio": mlp,
-        "llama2_7b_step": model,
         "sweep_13b": sweep,
         "prefill_13b": prefill,
     }

@@ -132,15 +132,17 @@ def ref_dgate(dY, X, W, g, g_out=1):
 MIN_ROW = 64  # per-row relative errors are checked on rows of at least this many elements
 
 
-def check_close(name: str, got, ref, tol: float = TOL, bound=None) -> str:
+def check_close(name: str, got, ref, tol: float = TOL, bound=None, rows=None) -> str:
     """The parity checks as one verdict: '' when every check passes, else what failed.
 
     * relative Frobenius error of the whole tensor <= tol (the headline bar);
-    * for 2-D tensors, the same relative error <= tol for every row and every
-      column of at least MIN_ROW elements, and an exactly zero GPU slice where
-      the oracle's slice is exactly zero;
+    * with ``rows`` (by default: whenever a bound is given, i.e. for the masked
+      linear's Y, dX and dgate), for 2-D tensors the same relative error <= tol
+      for every row and every column of at least MIN_ROW elements, and an
+      exactly zero GPU slice where the oracle's slice is exactly zero;
     * with ``bound``, |got - ref| <= bound for every element.
     """
+    rows = bound is not None if rows is None else rows
     got = np.asarray(got, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
     if got.shape != ref.shape:
@@ -152,7 +154,7 @@ def check_close(name: str, got, ref, tol: float = TOL, bound=None) -> str:
     err = rel_fro(got, ref)
     if err > tol:
         return f"{name}: rel-Frobenius {err:.3e} > {tol}"
-    if got.ndim == 2:
+    if rows and got.ndim == 2:
         diff = got - ref
         for axis, what in ((1, "row"), (0, "column")):
             if ref.shape[axis] < MIN_ROW:
@@ -174,10 +176,10 @@ def check_close(name: str, got, ref, tol: float = TOL, bound=None) -> str:
     return ""
 
 
-def assert_close(name: str, got, ref, tol: float = TOL, bound=None) -> float:
+def assert_close(name: str, got, ref, tol: float = TOL, bound=None, rows=None) -> float:
     got = np.asarray(got, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
-    msg = check_close(name, got, ref, tol, bound)
+    msg = check_close(name, got, ref, tol, bound, rows)
     assert not msg, msg
     if not np.any(ref):
         return 0.0

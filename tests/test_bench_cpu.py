@@ -49,16 +49,36 @@ def test_without_a_gpu_exits_cleanly():
 def test_traffic_follows_the_counted_sources():
     b = _bench_module()
     t = b.DGATE_TRAFFIC
-    expected = (t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"]) * 1024.0
-    if t["sources_sha256"] == b._sources_digest():
+    if t["sources_sha256"] is not None and t["sources_sha256"] == b._sources_digest():
+        expected = (t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"]) * 1024.0
         assert b._dgate_traffic_bytes() == expected
         # the committed counter summary is of these sources and these readings
-        with open(os.path.join(ROOT, "profiles", "dgate_kernel_attn4096_traffic.md")) as f:
+        with open(os.path.join(ROOT, "profiles", "dgate_kernel_llama2_7b_step_traffic.md")) as f:
             text = f.read()
         assert t["sources_sha256"] in text
         assert re.search(r"\b%.1f\b" % t["fetch_kib"], text)
     else:
         assert b._dgate_traffic_bytes() is None
+
+
+def test_trace_summary_finds_the_roofline_batch(tmp_path):
+    b = _bench_module()
+    hdr = ('"Kind","Dispatch_Id","Kernel_Name","Start_Timestamp","End_Timestamp","Workgroup_Size_X",'
+           '"Grid_Size_X"\n')
+    rows, t = [], 0
+    dg = "void gm::dgate_kernel<256, 1>(int)"
+    seq = ([("void gm::fwd_kernel<256, 1>(int)", 256, 100), (dg, 256, 110), ("void gm::dx_kernel<256, 1>(int)", 256, 60)]
+           + [(dg, w, d) for w, d in [(256, 120), (688, 330)] * 3])
+    for name, wg, dur in seq:
+        rows.append(f'"KERNEL_DISPATCH",{len(rows) + 1},"{name}",{t},{t + dur * 1000},512,{wg * 512}\n')
+        t += dur * 1000 + 500
+    p = tmp_path / "k.csv"
+    p.write_text(hdr + "".join(rows))
+    out = b._trace_summary(str(p))
+    assert "| `gm::dgate_kernel<256, 1>` | 688 | 3 | 330.0 |" in out
+    assert ("Longest back-to-back run of `gm::dgate_kernel<256, 1>`: 6 dispatches (workgroups: 256 x 3, 688 x 3)"
+            in out)
+    assert "mean 225.00 µs" in out
 
 
 def test_traffic_is_null_for_other_sources():
