@@ -207,6 +207,29 @@ gm_status gm_masked_linear_bwd(const uint16_t* dY, const uint16_t* X, const uint
                                gm_stream_t stream);
 
 /*
+ * gm_masked_linear_bwd_noalloc -- gm_masked_linear_bwd for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation.  Same arguments without the workspace,
+ * same kernels, same results bit for bit.
+ *
+ * Its workspace is a fixed scratch array of GM_NOALLOC_SCRATCH_BYTES (96 MiB)
+ * that the library keeps on every device it runs on until the process ends
+ * (the array's device address is looked up once per device, on the first
+ * call there).  A shape whose backward workspace (gm_workspace_size with
+ * GM_OP_BWD) exceeds it returns GM_ERR_WORKSPACE before any launch; the
+ * backward of every LLaMA-2-7B linear at 4096 tokens fits.  Nothing in the
+ * scratch needs to start at zero: each call rewrites what it reads.  Every
+ * call on one device shares that device's scratch, so calls that overlap on
+ * one GPU (different streams, or host threads without ordering between them)
+ * race and give wrong results: order them on one stream.  The call allocates
+ * and frees nothing.  A dgate-only call (dX == NULL) uses no scratch.
+ */
+#define GM_NOALLOC_SCRATCH_BYTES ((size_t)96 << 20)
+gm_status gm_masked_linear_bwd_noalloc(const uint16_t* dY, const uint16_t* X, const uint16_t* W, const float* mask,
+                                       int64_t T, int64_t d_in, int64_t d_out, int32_t g, int32_t g_out,
+                                       uint16_t* dX, float* dgate, gm_stream_t stream);
+
+/*
  * gm_pack_rows -- export of a learned mask (Appendix F): copies the retained
  * groups of W, row by row, into a packed buffer for the pruned model.  A
  * g_out x g group is stored as its g_out row pieces of g weights, so the

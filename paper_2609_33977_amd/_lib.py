@@ -21,7 +21,7 @@ GM_OP_FWD, GM_OP_BWD = 0, 1
 EXPORTS = (
     "gm_abi_version", "gm_status_string", "gm_gate", "gm_gate_bwd", "gm_budget_loss", "gm_gate_bwd_budget",
     "gm_workspace_size",
-    "gm_masked_linear_fwd", "gm_masked_linear_bwd", "gm_pack_rows", "gm_packed_linear_fwd",
+    "gm_masked_linear_fwd", "gm_masked_linear_bwd", "gm_masked_linear_bwd_noalloc", "gm_pack_rows", "gm_packed_linear_fwd",
     "gm_distill_workspace_size", "gm_distill_fwd", "gm_distill_bwd",
     "gm_hyper_workspace_size", "gm_hyper_fwd", "gm_hyper_bwd", "gm_adamw",
 )
@@ -54,6 +54,7 @@ def _load() -> ctypes.CDLL:
         "gm_workspace_size": ([ctypes.c_int, I64, I64, I64, I32, I32, ctypes.POINTER(SZ)], ctypes.c_int),
         "gm_masked_linear_fwd": ([P, P, P, I64, I64, I64, I32, I32, P, P, SZ, P], ctypes.c_int),
         "gm_masked_linear_bwd": ([P, P, P, P, I64, I64, I64, I32, I32, P, P, P, SZ, P], ctypes.c_int),
+        "gm_masked_linear_bwd_noalloc": ([P, P, P, P, I64, I64, I64, I32, I32, P, P, P], ctypes.c_int),
         "gm_pack_rows": ([P, P, I64, I64, I32, I32, I64, P, P, P, P, P], ctypes.c_int),
         "gm_packed_linear_fwd": ([P, P, P, P, P, I64, I64, I64, I32, P, P], ctypes.c_int),
         "gm_distill_workspace_size": ([I64, I64, I64, ctypes.POINTER(SZ)], ctypes.c_int),
@@ -223,6 +224,26 @@ def gm_masked_linear_bwd(dY, X, W, mask, g: int, dX=None, dgate=None, ws=None, s
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check(LIB.gm_masked_linear_bwd(_ptr(dY), _ptr(X), _ptr(W), _ptr(mask), T, d_in, d_out, int(g), int(g_out),
                                     _ptr(dX), _ptr(dgate), _ptr(ws), nbytes, _stream(stream)), "gm_masked_linear_bwd")
+
+
+def gm_masked_linear_bwd_noalloc(dY, X, W, mask, g: int, dX=None, dgate=None, stream=None, g_out: int = 1) -> None:
+    """gm_masked_linear_bwd with the library's fixed device scratch instead of a workspace (no allocation)."""
+    w = "gm_masked_linear_bwd_noalloc"
+    _arg(w, "X", X, "bf16", shape=(None, None))
+    T, d_in = X.shape
+    _arg(w, "W", W, "bf16", shape=(None, d_in))
+    d_out = W.shape[0]
+    G = _groups(d_out, d_in, g, g_out, w)
+    _arg(w, "dY", dY, "bf16", shape=(T, d_out))
+    _arg(w, "mask", mask, "f32", numel=G, optional=dX is None)
+    _arg(w, "dX", dX, "bf16", shape=(T, d_in), optional=True)
+    _arg(w, "dgate", dgate, "f32", numel=G, optional=True)
+    _check(LIB.gm_masked_linear_bwd_noalloc(_ptr(dY), _ptr(X), _ptr(W), _ptr(mask), T, d_in, d_out, int(g),
+                                            int(g_out), _ptr(dX), _ptr(dgate), _stream(stream)),
+           "gm_masked_linear_bwd_noalloc")
+
+
+GM_NOALLOC_SCRATCH_BYTES = 96 << 20
 
 
 def gm_pack_rows(W, mask, g: int, capacity: int, Wp, chunk, scale, rowptr, stream=None, g_out: int = 1) -> None:

@@ -366,25 +366,15 @@ GM_EXPORT gm_status gm_masked_linear_fwd(const uint16_t* X, const uint16_t* W, c
   return from_hip(gm::launch_fwd(X, W, mask, t, di, dout, g, g_out, Y, ks, static_cast<float*>(ws), stream));
 }
 
-GM_EXPORT gm_status gm_masked_linear_bwd(const uint16_t* dY, const uint16_t* X, const uint16_t* W,
-                                         const float* mask, int64_t T, int64_t d_in, int64_t d_out, int32_t g,
-                                         int32_t g_out, uint16_t* dX, float* dgate, void* ws, size_t ws_bytes,
-                                         gm_stream_t stream) {
-  if (!dY || !X || !W) return GM_ERR_NULL;
-  if (dX && !mask) return GM_ERR_NULL;
-  if (gm_status st = check_linear_shape(T, d_in, d_out, g, g_out)) return st;
-  if (!aligned16(dY) || !aligned16(X) || !aligned16(W) || (mask && !aligned16(mask)) || (dX && !aligned16(dX)) ||
-      (dgate && !aligned16(dgate)))
-    return GM_ERR_ALIGN;
-  if (!dX && !dgate) return GM_OK;
-  const BwdLayout L = bwd_layout(T, d_in, d_out, g);
-  if (dX) {
-    if (!ws) return GM_ERR_WORKSPACE;
-    if (ws_bytes < L.total) return GM_ERR_WORKSPACE;
-    if (!aligned16(ws)) return GM_ERR_ALIGN;
-  }
-  if (gm_status st = check_device()) return st;
+namespace {
 
+// The backward after argument validation: column lists, dgate (with the dY^T
+// side output when dX is wanted), dX.  `ws` holds at least bwd_layout().total
+// bytes when dX is wanted.
+gm_status masked_linear_bwd_launch(const uint16_t* dY, const uint16_t* X, const uint16_t* W, const float* mask,
+                                   int64_t T, int64_t d_in, int64_t d_out, int32_t g, int32_t g_out, uint16_t* dX,
+                                   float* dgate, void* ws, gm_stream_t stream) {
+  const BwdLayout L = bwd_layout(T, d_in, d_out, g);
   const int t = int(T), di = int(d_in), dout = int(d_out), G_in = int(d_in / g);
   char* base = static_cast<char*>(ws);
   uint16_t* dyt = dX ? reinterpret_cast<uint16_t*>(base + L.dyt) : nullptr;
@@ -404,14 +394,79 @@ GM_EXPORT gm_status gm_masked_linear_bwd(const uint16_t* dY, const uint16_t* X, 
     } else {
       if (gm_status st = from_hip(gm::launch_transpose(dY, t, dout, dyt, L.ldt, stream))) return st;
     }
-    if (gm_status st = from_hip(gm::launch_dx(dyt, L.ldt, W, colcount, rows, scales, subbits, colsoft, t, di, dout,
-                                              g, dX, stream)))
-      return st;
-  } else {
-    if (gm_status st = from_hip(gm::launch_dgate(dY, X, W, t, di, dout, g, g_out, dgate, nullptr, 0, stream)))
-      return st;
+    return from_hip(gm::launch_dx(dyt, L.ldt, W, colcount, rows, scales, subbits, colsoft, t, di, dout, g, dX,
+                                  stream));
   }
+  return from_hip(gm::launch_dgate(dY, X, W, t, di, dout, g, g_out, dgate, nullptr, 0, stream));
+}
+
+// Shared argument checks of the two backward entry points (everything but the workspace).
+gm_status check_bwd_args(const uint16_t* dY, const uint16_t* X, const uint16_t* W, const float* mask, int64_t T,
+                         int64_t d_in, int64_t d_out, int32_t g, int32_t g_out, const uint16_t* dX,
+                         const float* dgate) {
+  if (!dY || !X || !W) return GM_ERR_NULL;
+  if (dX && !mask) return GM_ERR_NULL;
+  if (gm_status st = check_linear_shape(T, d_in, d_out, g, g_out)) return st;
+  if (!aligned16(dY) || !aligned16(X) || !aligned16(W) || (mask && !aligned16(mask)) || (dX && !aligned16(dX)) ||
+      (dgate && !aligned16(dgate)))
+    return GM_ERR_ALIGN;
   return GM_OK;
+}
+
+// Scratch of the allocation-free backward: a file-scope device array that
+// every device the library runs on holds until the process ends.  In host
+// code `scratch` names a host-side stand-in, never the device memory: its
+// device address is looked up once per device (with that device current) and
+// only that address is handed to kernels.
+constexpr size_t kNoAllocScratchBytes = GM_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+gm_status noalloc_scratch(void** out) {
+  static std::mutex mu;
+  static void* ptr[256];
+  int dev = 0;
+  if (hipError_t e = hipGetDevice(&dev)) return device_error("hipGetDevice", e);
+  if (dev < 0 || dev >= 256) return device_error("device index", hipErrorInvalidDevice);
+  std::lock_guard<std::mutex> lock(mu);
+  if (ptr[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch))) return device_error("hipGetSymbolAddress", e);
+    if (p == nullptr || !aligned16(p)) return device_error("scratch address", hipErrorInvalidValue);
+    ptr[dev] = p;
+  }
+  *out = ptr[dev];
+  return GM_OK;
+}
+
+}  // namespace
+
+GM_EXPORT gm_status gm_masked_linear_bwd(const uint16_t* dY, const uint16_t* X, const uint16_t* W,
+                                         const float* mask, int64_t T, int64_t d_in, int64_t d_out, int32_t g,
+                                         int32_t g_out, uint16_t* dX, float* dgate, void* ws, size_t ws_bytes,
+                                         gm_stream_t stream) {
+  if (gm_status st = check_bwd_args(dY, X, W, mask, T, d_in, d_out, g, g_out, dX, dgate)) return st;
+  if (!dX && !dgate) return GM_OK;
+  if (dX) {
+    if (!ws) return GM_ERR_WORKSPACE;
+    if (ws_bytes < bwd_layout(T, d_in, d_out, g).total) return GM_ERR_WORKSPACE;
+    if (!aligned16(ws)) return GM_ERR_ALIGN;
+  }
+  if (gm_status st = check_device()) return st;
+  return masked_linear_bwd_launch(dY, X, W, mask, T, d_in, d_out, g, g_out, dX, dgate, ws, stream);
+}
+
+GM_EXPORT gm_status gm_masked_linear_bwd_noalloc(const uint16_t* dY, const uint16_t* X, const uint16_t* W,
+                                                 const float* mask, int64_t T, int64_t d_in, int64_t d_out,
+                                                 int32_t g, int32_t g_out, uint16_t* dX, float* dgate,
+                                                 gm_stream_t stream) {
+  if (gm_status st = check_bwd_args(dY, X, W, mask, T, d_in, d_out, g, g_out, dX, dgate)) return st;
+  if (!dX && !dgate) return GM_OK;
+  if (dX && bwd_layout(T, d_in, d_out, g).total > kNoAllocScratchBytes) return GM_ERR_WORKSPACE;
+  if (gm_status st = check_device()) return st;
+  void* ws = nullptr;
+  if (dX)
+    if (gm_status st = noalloc_scratch(&ws)) return st;
+  return masked_linear_bwd_launch(dY, X, W, mask, T, d_in, d_out, g, g_out, dX, dgate, ws, stream);
 }
 
 GM_EXPORT gm_status gm_pack_rows(const uint16_t* W, const float* mask, int64_t d_in, int64_t d_out, int32_t g,
