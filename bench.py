@@ -317,7 +317,33 @@ def _single_linear(reps):
                                   f"2048 of 4096 kept, tau {cfg['tau']}")
     out["us_per_step"] = out["ms_per_step"] * 1e3
     out["breakdown_us"] = {k: v * 1e3 for k, v in out.pop("breakdown_ms").items()}
+    out["graph_us_per_step"] = _graph_us(step, reps)
     return out
+
+
+def _graph_us(step, reps):
+    """The step captured once in a HIP graph and replayed: its time without the host's per-call cost.  Every
+    replay's outputs (mask, Y, dX, dgate, logit gradient) are checked against the eager step's; None if they
+    differ.  The single linear's path launches kernels only (no memset nodes)."""
+    import torch
+    step()
+    torch.cuda.synchronize()
+    X, W, dY, Y, dX, m, dg = step.lin[0]
+    outs = lambda: [step.mask, Y, dX, step.dgate, step.dlogits]
+    eager = [t.clone() for t in outs()]
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for _ in range(3):
+        for t in outs():
+            t.zero_()
+        graph.replay()
+        torch.cuda.synchronize()
+        if not all(torch.equal(a, b) for a, b in zip(outs(), eager)):
+            return None
+    ms = _events_batch_ms(graph.replay, max(reps, 50))
+    del graph
+    return ms * 1e3
 
 
 def _attention_4096(reps):
