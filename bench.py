@@ -50,8 +50,8 @@ GEMM_SOURCES = ["paper_2609_33977_amd/csrc/gemm.hip", "paper_2609_33977_amd/csrc
 # by the same counters (FETCH_SIZE read 0.5x and WRITE_SIZE 1.0x of the copied
 # bytes).  The numbers describe the kernel built from sources with this digest
 # and are reported only while the sources still match it (None: not measured).
-DGATE_TRAFFIC = {"sources_sha256": None, "fetch_kib": None, "write_kib": None, "fetch_scale": 2.0,
-                 "write_scale": 1.0}
+DGATE_TRAFFIC = {"sources_sha256": "a3b8bb64f8810ea7c4eae14e95d0361ea53e73acac886544ad51170511a02331",
+                 "fetch_kib": 218501.6, "write_kib": 596.5, "fetch_scale": 2.0, "write_scale": 1.0}
 
 
 def _progress(msg: str) -> None:
@@ -180,14 +180,20 @@ def _shift_to_budget(gm, logits, noise, sizes, kept, tau, iters=64):
     dev = logits.device
     L = len(sizes)
     seg = torch.repeat_interleave(torch.arange(L, device=dev), torch.tensor(sizes, device=dev))
+    ends = torch.tensor(np.cumsum(sizes), dtype=torch.int64, device=dev)
     want = torch.tensor(kept, dtype=torch.float64, device=dev)
+
+    def counts(m):  # kept selectors per matrix: a running sum read at the matrix ends
+        cs = torch.cumsum(m.to(torch.int32), 0, dtype=torch.int64)[ends - 1]
+        return torch.diff(cs, prepend=torch.zeros(1, dtype=torch.int64, device=dev)).double()
+
     lo = torch.full((L,), -24.0, dtype=torch.float64, device=dev)
     hi = torch.full((L,), 24.0, dtype=torch.float64, device=dev)
     mask = torch.empty_like(logits)
     for _ in range(iters):
         c = 0.5 * (lo + hi)
         gm.gm_gate(logits + c.float()[seg], noise, tau, True, mask)
-        cnt = torch.zeros(L, dtype=torch.float64, device=dev).index_add_(0, seg, mask.double())
+        cnt = counts(mask)
         eq = cnt == want
         lo = torch.where(eq | (cnt < want), c, lo)
         hi = torch.where(eq | (cnt > want), c, hi)
@@ -1026,6 +1032,19 @@ def _counter_summary(path: str) -> str:
     for (k, wg), d in sorted(per.items()):
         vals = [np.mean([v.get(n, 0.0) for v in d.values()]) for n in names]
         lines.append(f"| `{k}` | {wg} | {len(d)} | " + " | ".join(f"{x:.1f}" for x in vals) + " |")
+    # the roofline batches: the longest run of consecutive dispatches that are all dgate_kernel<256, 1>
+    dg = "gm::dgate_kernel<256, 1>"
+    order = sorted(((int(i), k, wg) for (k, wg), d in per.items() for i in d), key=lambda x: x[0])
+    runs = _runs(order, lambda x: x[1] == dg)
+    if runs:
+        a, b = max(runs, key=lambda ab: ab[1] - ab[0])
+        sel = order[a:b + 1]
+        lines += ["", f"Longest back-to-back run of `{dg}` (dispatches {sel[0][0]}-{sel[-1][0]}): {len(sel)} dispatches"]
+        for wg in sorted({x[2] for x in sel}) + [None]:
+            part = [per[(dg, x[2])][str(x[0])] for x in sel if wg is None or x[2] == wg]
+            what = f"workgroups {wg}" if wg is not None else "all of the run"
+            lines.append(f"- {what}: {len(part)} dispatches, mean " + ", ".join(
+                f"{n} {np.mean([v.get(n, 0.0) for v in part]):.1f}" for n in names))
     return "\n".join(lines)
 
 
