@@ -880,6 +880,23 @@ def _gemv_bandwidth(n_layers, reps):
     else:
         out["packed_stacked"] = None
     del packed
+    # Each launch shape on its own: the same projection of all layers back to back (serialised on the stream,
+    # as in the pass); the rate of one kernel at one shape, free of the pass's mix of small and large launches.
+    per_shape = {}
+    for j, name in enumerate(("qkv_stacked", "o", "gateup_stacked", "down")):
+        mats = [f[j] for f in fused]
+        nbytes = sum(2 * int((m != 0).sum().item()) * g + 4 * m.numel() + 2 * (W.shape[1] + W.shape[0])
+                     for _, W, m, _ in mats)
+
+        def one(mats=mats):
+            for mat in mats:
+                run(mat)
+        one()
+        torch.cuda.synchronize()
+        t = _events_ms(one, reps)
+        per_shape[name] = {"rows_x_d_in": list(mats[0][1].shape), "us_per_launch": 1e3 * t / len(mats),
+                           "GB/s": nbytes / (t / 1e3) / 1e9}
+    out["per_shape"] = per_shape
     # 8 and 16 tokens over the same weights and masks, seven launches per layer (eager)
     for T in (8, 16):
         xs, ys, extra = {}, [], 0

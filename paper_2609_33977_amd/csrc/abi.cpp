@@ -104,9 +104,12 @@ gm_status check_linear_shape(int64_t T, int64_t d_in, int64_t d_out, int32_t g, 
 // tiles (half the CUs or fewer, e.g. T = 512 at LLaMA-2-13B shapes) spreads
 // each tile's K range over ksplit blocks, up to 256 blocks in all, at most 8
 // shares and at least four column units per share (fewer, longer shares
-// measured 3.6 % faster per LLaMA-2-13B layer at T = 512 than two-unit ones).  The partial tiles take
+// measured 3.6 % faster per LLaMA-2-13B layer at T = 512 than two-unit ones);
+// launches of at most 16 tiles (the 128-token, 1024 x 1024 linear has 4) may
+// take shares of a single unit, since there the latency of one long K range,
+// not the per-share cost, sets the time.  The partial tiles take
 // ksplit * T * d_out fp32 of workspace.
-constexpr int64_t kSplitMaxTiles = 128, kSplitBlocks = 256, kSplitMax = 8;
+constexpr int64_t kSplitMaxTiles = 128, kSplitBlocks = 256, kSplitMax = 8, kSplitFewTiles = 16;
 
 int fwd_splits(int64_t T, int64_t d_in, int64_t d_out, int32_t g) {
   if (T <= kDecodeTokens) return 1;
@@ -114,7 +117,7 @@ int fwd_splits(int64_t T, int64_t d_in, int64_t d_out, int32_t g) {
   if (tiles > kSplitMaxTiles) return 1;
   int64_t ks = kSplitBlocks / tiles;
   ks = std::min(ks, kSplitMax);
-  ks = std::min(ks, d_in / unit_width(g) / 4);
+  ks = std::min(ks, d_in / unit_width(g) / (tiles <= kSplitFewTiles ? 1 : 4));
   return int(std::max<int64_t>(ks, 1));
 }
 

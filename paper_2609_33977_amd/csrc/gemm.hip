@@ -724,7 +724,10 @@ hipError_t launch_dx(const uint16_t* dYt, int ldt, const uint16_t* W, const int*
                      const float* scales, const int* subbits, const int* colsoft, int T, int d_in, int d_out, int g,
                      uint16_t* dX, hipStream_t s) {
   const int lc = g < 64 ? 64 : g;  // list-column width
-  const int bm = lc < 256 ? lc : 256;
+  int bm = lc < 256 ? lc : 256;
+  // A launch of fewer than 64 tiles (the 128-token, 1024 x 1024 linear has 4)
+  // takes tiles of 64 columns, four times as many blocks over the same lists.
+  if (g >= 64 && bm > 64 && (d_in / bm) * ((T + 255) / 256) < 64) bm = 64;
   const int tiles = (d_in / bm) * ((T + 255) / 256);
 #define GM_DX(BM, NSUB)                                                                                        \
   hipLaunchKernelGGL((dx_kernel<BM, NSUB>), dim3(tiles), dim3(64 * dx_waves(BM)), 0, s, dYt, ldt, W, colcount, \
@@ -733,9 +736,13 @@ hipError_t launch_dx(const uint16_t* dYt, int ldt, const uint16_t* W, const int*
     case 16: GM_DX(64, 4); break;
     case 32: GM_DX(64, 2); break;
     case 64: GM_DX(64, 1); break;
-    case 128: GM_DX(128, 1); break;
+    case 128:
+      if (bm == 64) GM_DX(64, 1); else GM_DX(128, 1);
+      break;
     case 256:
-    case 512: GM_DX(256, 1); break;
+    case 512:
+      if (bm == 64) GM_DX(64, 1); else GM_DX(256, 1);
+      break;
     default: return hipErrorInvalidValue;
   }
 #undef GM_DX

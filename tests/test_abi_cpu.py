@@ -68,13 +68,14 @@ def test_workspace_size_square_groups(g, nsub):
 
 def _fwd_split_bytes(T, d_in, d_out, g):
     """The documented rule: at most 128 output tiles of 256 x 256 (and T > 16) split K into
-    min(256 // tiles, 8, units // 4) shares of fp32 partial tiles; units of max(g, 32) columns."""
+    min(256 // tiles, 8, units // 4) shares of fp32 partial tiles (units // 1 with at most 16 tiles);
+    units of max(g, 32) columns."""
     if T <= 16:
         return 0
     tiles = -(-T // 256) * -(-d_out // 256)
     if tiles > 128:
         return 0
-    ks = min(256 // tiles, 8, d_in // max(g, 32) // 4)
+    ks = min(256 // tiles, 8, d_in // max(g, 32) // (1 if tiles <= 16 else 4))
     return 0 if ks <= 1 else (ks * T * d_out * 4 + 255) // 256 * 256
 
 
@@ -86,9 +87,11 @@ def _fwd_split_bytes(T, d_in, d_out, g):
     (512, 13824, 5120, 256, 6 * 512 * 5120 * 4),
     (2048, 4096, 4096, 256, 2 * 2048 * 4096 * 4),     # 128 tiles: 2 shares
     (2048, 4096, 4352, 256, 0),                       # 136 tiles: unsplit
-    (17, 4096, 4096, 256, 4 * 17 * 4096 * 4),         # 16 tiles, 16 units: 4 shares
-    (300, 2048, 1024, 512, 0),                        # four units: a share would hold fewer
-    (300, 4096, 1024, 512, 2 * 300 * 1024 * 4),
+    (17, 4096, 4096, 256, 8 * 17 * 4096 * 4),         # 16 tiles, 16 units: 8 shares of two
+    (128, 1024, 1024, 256, 4 * 128 * 1024 * 4),       # 4 tiles, 4 units: one unit per share
+    (300, 2048, 1024, 512, 4 * 300 * 1024 * 4),       # 8 tiles, 4 units
+    (520, 2048, 4608, 512, 0),                        # 54 tiles, 4 units: a share would hold fewer than four
+    (520, 8192, 4608, 512, 4 * 520 * 4608 * 4),
 ])
 def test_forward_split_workspace(T, d_in, d_out, g, expect):
     assert gm.gm_workspace_size(gm.GM_OP_FWD, T, d_in, d_out, g) == expect == _fwd_split_bytes(T, d_in, d_out, g)
