@@ -277,6 +277,23 @@ def test_decode_soft_selectors_in_place_and_packed(T, g):
     assert_close("Y packed", host_f64_from_bf16(Yp), Yr, bound=bY)
 
 
+@pytest.mark.parametrize("T", [2, 8, 16])
+def test_decode_one_soft_selector_among_binary(T):
+    # the 2-16 token kernel scales weights only in blocks whose staged
+    # selectors include a fractional one: a binary mask with a single
+    # fractional selector (row 333) mixes both kinds of block in one launch
+    d_in, d_out, g = 4096, 640, 256
+    say(f"decode one soft selector: T={T}")
+    case = workloads.make_linear_case((216, T), T, d_in, d_out, g, None)
+    m = case.mask.astype(np.float32).copy()
+    m[333, 5] = 0.37
+    d = _dev_case(case, m)
+    Yr, _, _, bY, _, _ = _oracle_all(case, m)
+    Y = host_f64_from_bf16(_fwd(d, g))
+    assert_close("Y", Y, Yr, bound=bY)
+    assert_close("Y row 333", Y[:, 333:334], Yr[:, 333:334], bound=bY[:, 333:334])
+
+
 @pytest.mark.parametrize("T", [1, 8])
 def test_decode_degenerate_rows(T):
     # rows with every group kept (64 groups: the one-token kernel's longest
