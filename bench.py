@@ -897,26 +897,29 @@ def _gemv_bandwidth(n_layers, reps):
         per_shape[name] = {"rows_x_d_in": list(mats[0][1].shape), "us_per_launch": 1e3 * t / len(mats),
                            "GB/s": nbytes / (t / 1e3) / 1e9}
     out["per_shape"] = per_shape
-    # 8 and 16 tokens over the same weights and masks, seven launches per layer (eager)
+    # 8 and 16 tokens over the same weights and masks (eager): seven launches
+    # per layer, and the stacked layout's four (q|k|v and gate|up read one input
+    # each, so the stacked launches read it once)
     for T in (8, 16):
-        xs, ys, extra = {}, [], 0
-        for mats in layers:
-            for X1, W, m, _ in mats:
-                key = id(X1)
-                if key not in xs:
-                    xs[key] = torch.randn(T, X1.shape[1], device="cuda", generator=gen).to(torch.bfloat16)
-                ys.append((xs[key], W, m, torch.empty(T, W.shape[0], dtype=torch.bfloat16, device="cuda")))
-                extra += 2 * (T - 1) * (W.shape[0] + W.shape[1])
+        for name, mats_of in (("", lambda i: layers[i]), ("stacked_", lambda i: fused[i])):
+            xs, ys, nbytes = {}, [], kept_bytes
+            for i in range(n_layers):
+                for X1, W, m, _ in mats_of(i):
+                    key = id(X1)
+                    if key not in xs:
+                        xs[key] = torch.randn(T, X1.shape[1], device="cuda", generator=gen).to(torch.bfloat16)
+                    ys.append((xs[key], W, m, torch.empty(T, W.shape[0], dtype=torch.bfloat16, device="cuda")))
+                    nbytes += 4 * m.numel() + 2 * T * (W.shape[0] + W.shape[1])
 
-        def serial_t():
-            for mat in ys:
-                run(mat)
-        serial_t()
-        torch.cuda.synchronize()
-        t = _events_ms(serial_t, reps)
-        out[f"T{T}_GB/s"] = (total + extra) / (t / 1e3) / 1e9
-        out[f"T{T}_ms_per_pass"] = t
-        del ys, xs
+            def serial_t():
+                for mat in ys:
+                    run(mat)
+            serial_t()
+            torch.cuda.synchronize()
+            t = _events_ms(serial_t, reps)
+            out[f"T{T}_{name}GB/s"] = nbytes / (t / 1e3) / 1e9
+            out[f"T{T}_{name}ms_per_pass"] = t
+            del ys, xs
     return out
 
 

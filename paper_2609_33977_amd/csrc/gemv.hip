@@ -168,7 +168,11 @@ __device__ __forceinline__ u32x4 ld16_rsrc(__amdgpu_buffer_rsrc_t r, uint32_t of
 // eight waves of the block split the input columns and sum their partial tiles
 // in LDS in wave order.  The mask rows of the block are staged in LDS first; a
 // lane reads a W chunk only when its group is kept (pruned chunks are zeros),
-// so HBM traffic is the kept weights, as in the GEMV.  The weights go through
+// so HBM traffic is the kept weights, as in the GEMV.  The packed export runs
+// the same K loop: the block turns its rows' piece lists into the same
+// (row, group) table, with each kept group's piece index beside its selector,
+// and reads the pieces instead of W's rows; both layouts therefore give
+// identical results.  The weights go through
 // the caches: an instruction reads 64 bytes of each of 16 rows, and the other
 // half of each 128-byte line is requested by the very next instruction
 // (nontemporal loads measured 3-8 % slower here).
@@ -177,14 +181,20 @@ constexpr int kMmaMaskFloats = 8192;  // staged mask floats per block: mask rows
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-template <int RT>
+template <int RT, bool PACKED>
 __global__ __launch_bounds__(64 * kMmaWaves) void gemv_mfma_kernel(const uint16_t* __restrict__ X,
                                                                   const uint16_t* __restrict__ W,
-                                                                  const float* __restrict__ mask, int T, int d_in,
+                                                                  const float* __restrict__ mask,
+                                                                  const int* __restrict__ chunk,
+                                                                  const float* __restrict__ scale,
+                                                                  const int* __restrict__ rowptr, int T, int d_in,
                                                                   int d_out, int g, int go,
                                                                   uint16_t* __restrict__ Y) {
   constexpr int R = 16 * RT;
+  constexpr int NT = 64 * kMmaWaves;
   __shared__ float s_m[kMmaMaskFloats];
+  __shared__ int s_idx[PACKED ? kMmaMaskFloats : 1];  // packed: piece of (row, group) from the block's first piece
+  __shared__ int s_rp[PACKED ? R + 1 : 1];
   __shared__ f32x4 s_part[kMmaWaves][RT][64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int o0 = blockIdx.x * R;
@@ -192,15 +202,43 @@ __global__ __launch_bounds__(64 * kMmaWaves) void gemv_mfma_kernel(const uint16_
   const int mrows = go == 1 ? R : (R > go ? R / go : 1);
   const int u0 = o0 / go;
   const int G_out = (d_out + go - 1) / go;
+  const int rows = min(R, d_out - o0);  // rows of this block inside W
   // Staged selectors; the block notes whether any lies strictly between 0 and
   // 1 (a soft selector), so that the K loop scales weights only in blocks
-  // that hold one and carries no per-slice branch otherwise.
+  // that hold one and carries no per-slice branch otherwise.  In place the
+  // selectors are the mask rows of the block.  Packed (W = Wp, go = 1), the
+  // table starts at zero (pruned) and every piece p of the block's rows
+  // writes its selector scale[p] and its index into (row, chunk[p]); pieces
+  // whose column is out of range are ignored.
   int soft_here = 0;
-  for (int e = tid; e < mrows * G_in; e += 64 * kMmaWaves) {
-    const int rr = e / G_in;
-    const float v = u0 + rr < G_out ? mask[int64_t(u0) * G_in + e] : 0.0f;
-    s_m[e] = v;
-    soft_here |= v != 0.0f && v != 1.0f;
+  int p0 = 0;  // packed: first piece of the block
+  if constexpr (PACKED) {
+    for (int e = tid; e <= rows; e += NT) s_rp[e] = rowptr[o0 + e];
+    for (int e = tid; e < R * G_in; e += NT) s_m[e] = 0.0f;
+    __syncthreads();
+    p0 = s_rp[0];
+    const int np = s_rp[rows] - p0;
+    for (int e = tid; e < np; e += NT) {
+      int lo = 0, hi = rows;  // the row of piece p0 + e: s_rp[lo] <= p0 + e < s_rp[lo + 1]
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (s_rp[mid] <= p0 + e) lo = mid; else hi = mid;
+      }
+      const int v = chunk[p0 + e];
+      if (v >= 0 && v < G_in) {
+        const float sv = scale[p0 + e];
+        s_m[lo * G_in + v] = sv;
+        s_idx[lo * G_in + v] = e;
+        soft_here |= sv != 0.0f && sv != 1.0f;
+      }
+    }
+  } else {
+    for (int e = tid; e < mrows * G_in; e += NT) {
+      const int rr = e / G_in;
+      const float v = u0 + rr < G_out ? mask[int64_t(u0) * G_in + e] : 0.0f;
+      s_m[e] = v;
+      soft_here |= v != 0.0f && v != 1.0f;
+    }
   }
   const bool soft = __syncthreads_or(soft_here);
 
@@ -217,8 +255,11 @@ __global__ __launch_bounds__(64 * kMmaWaves) void gemv_mfma_kernel(const uint16_
   }
   const bool tok = r < T;
   const uint32_t xrow = (uint32_t(tok ? r : 0) * uint32_t(d_in) + uint32_t(8 * kc)) * 2u;
-  // the block's rows of W and the T rows of X (the launcher keeps both under 2 GiB)
-  const __amdgpu_buffer_rsrc_t rw = t1_rsrc(W + int64_t(o0) * d_in, uint32_t(min(R, d_out - o0) * d_in) * 2u);
+  // the block's rows of W (packed: the block's pieces) and the T rows of X
+  // (the launcher keeps both under 2 GiB)
+  const __amdgpu_buffer_rsrc_t rw =
+      PACKED ? t1_rsrc(W + int64_t(p0) * g, uint32_t(s_rp[rows] - p0) * uint32_t(g) * 2u)
+             : t1_rsrc(W + int64_t(o0) * d_in, uint32_t(rows * d_in) * 2u);
   const __amdgpu_buffer_rsrc_t rx = t1_rsrc(X, uint32_t(T) * uint32_t(d_in) * 2u);
   const int lg = __builtin_ctz(unsigned(g));  // g is a power of two: the group of a column by shift
   const int nsl = d_in / 32;
@@ -233,12 +274,20 @@ __global__ __launch_bounds__(64 * kMmaWaves) void gemv_mfma_kernel(const uint16_
   // a slice past the wave's range, a row past d_out or a token past T reads
   // zeros through an out-of-range offset, without a memory access).
   float mn[RT][U];
+  uint32_t on[RT][U];  // packed: byte offset of the lane's 16 bytes in the block's pieces
   auto read_masks = [&](int sb) {
 #pragma unroll
     for (int q = 0; q < U; ++q) {
       const int k = (sb + q) * 32;
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt) mn[rt][q] = sb + q < s1 && orow[rt] ? mrow[rt][(k + 8 * kc) >> lg] : 0.0f;
+      for (int rt = 0; rt < RT; ++rt) {
+        const int at = int(mrow[rt] - s_m) + ((k + 8 * kc) >> lg);
+        mn[rt][q] = sb + q < s1 && orow[rt] ? s_m[at] : 0.0f;
+        if constexpr (PACKED)
+          on[rt][q] = sb + q < s1 && orow[rt]
+                          ? (uint32_t(s_idx[at]) * uint32_t(g) + uint32_t((k + 8 * kc) & (g - 1))) * 2u
+                          : kOutOfRange;
+      }
     }
   };
   auto k_loop = [&](auto soft_tag) {
@@ -255,7 +304,8 @@ __global__ __launch_bounds__(64 * kMmaWaves) void gemv_mfma_kernel(const uint16_
 #pragma unroll
         for (int q = 0; q < U; ++q) {
           m[rt][q] = mn[rt][q];
-          av[rt][q] = ld16_rsrc(rw, m[rt][q] != 0.0f ? wrow[rt] + uint32_t(sb + q) * 64u : kOutOfRange, 0);
+          const uint32_t off = PACKED ? on[rt][q] : wrow[rt] + uint32_t(sb + q) * 64u;
+          av[rt][q] = ld16_rsrc(rw, m[rt][q] != 0.0f ? off : kOutOfRange, 0);
         }
 #pragma unroll
       for (int q = 0; q < U; ++q)
@@ -468,28 +518,40 @@ static hipError_t gemv_passes(const uint16_t* X, const uint16_t* W, const float*
   return hipSuccess;
 }
 
+// The 2..16 token MFMA kernel when its staged tables fit in LDS and its byte
+// offsets fit in 32 bits: four row tiles while that still gives 192 blocks or
+// more, else two, fewer when the block's tables do not fit.  Returns false
+// (nothing launched) otherwise.
+template <bool PACKED>
+static bool launch_mfma(const uint16_t* X, const uint16_t* W, const float* mask, const int* chunk, const float* scale,
+                        const int* rowptr, int T, int d_in, int d_out, int g, int go, uint16_t* Y, hipStream_t s,
+                        hipError_t& err) {
+  const int G_in = d_in / g;
+  auto fits = [&](int R) { return (go == 1 ? R : (R > go ? R / go : 1)) * G_in <= kMmaMaskFloats; };
+  int rt = (d_out + 63) / 64 >= 192 ? 4 : 2;
+  while (rt > 1 && !fits(16 * rt)) rt /= 2;
+  // byte offsets into the block's rows of W (or its pieces) and into X are 32-bit, below the out-of-range marker
+  const int64_t span = int64_t(16 * rt > T ? 16 * rt : T) * d_in * 2;
+  if (!fits(16 * rt) || span >= int64_t(kOutOfRange)) return false;
+  const dim3 grid(unsigned((d_out + 16 * rt - 1) / (16 * rt))), block(64 * kMmaWaves);
+  if (rt == 4)
+    hipLaunchKernelGGL((gemv_mfma_kernel<4, PACKED>), grid, block, 0, s, X, W, mask, chunk, scale, rowptr, T, d_in,
+                       d_out, g, go, Y);
+  else if (rt == 2)
+    hipLaunchKernelGGL((gemv_mfma_kernel<2, PACKED>), grid, block, 0, s, X, W, mask, chunk, scale, rowptr, T, d_in,
+                       d_out, g, go, Y);
+  else
+    hipLaunchKernelGGL((gemv_mfma_kernel<1, PACKED>), grid, block, 0, s, X, W, mask, chunk, scale, rowptr, T, d_in,
+                       d_out, g, go, Y);
+  err = hipGetLastError();
+  return true;
+}
+
 hipError_t launch_gemv_inplace(const uint16_t* X, const uint16_t* W, const float* mask, int T, int d_in, int d_out,
                                int g, int go, uint16_t* Y, hipStream_t s) {
-  if (T >= 2 && T <= 16) {
-    // four row tiles while that still gives 192 blocks or more, else two; fewer
-    // when the block's mask rows do not fit in LDS
-    const int G_in = d_in / g;
-    auto fits = [&](int R) { return (go == 1 ? R : (R > go ? R / go : 1)) * G_in <= kMmaMaskFloats; };
-    int rt = (d_out + 63) / 64 >= 192 ? 4 : 2;
-    while (rt > 1 && !fits(16 * rt)) rt /= 2;
-    // byte offsets into the block's rows of W and into X are 32-bit, below the out-of-range marker
-    const int64_t span = int64_t(16 * rt > T ? 16 * rt : T) * d_in * 2;
-    if (fits(16 * rt) && span < int64_t(kOutOfRange)) {
-      const dim3 grid(unsigned((d_out + 16 * rt - 1) / (16 * rt))), block(64 * kMmaWaves);
-      if (rt == 4)
-        hipLaunchKernelGGL(gemv_mfma_kernel<4>, grid, block, 0, s, X, W, mask, T, d_in, d_out, g, go, Y);
-      else if (rt == 2)
-        hipLaunchKernelGGL(gemv_mfma_kernel<2>, grid, block, 0, s, X, W, mask, T, d_in, d_out, g, go, Y);
-      else
-        hipLaunchKernelGGL(gemv_mfma_kernel<1>, grid, block, 0, s, X, W, mask, T, d_in, d_out, g, go, Y);
-      return hipGetLastError();
-    }
-  }
+  hipError_t err = hipSuccess;
+  if (T >= 2 && T <= 16 && launch_mfma<false>(X, W, mask, nullptr, nullptr, nullptr, T, d_in, d_out, g, go, Y, s, err))
+    return err;
   if (T == 1 && d_in / g <= 64)
     return launch_t1<false>(X, W, mask, nullptr, nullptr, nullptr, nullptr, d_in, d_out, g, go, Y, s);
   if (d_in / g <= 512)
@@ -501,6 +563,8 @@ hipError_t launch_gemv_inplace(const uint16_t* X, const uint16_t* W, const float
 hipError_t launch_gemv_packed(const uint16_t* X, const uint16_t* Wp, const int* chunk, const float* scale,
                               const int* rowptr, int T, int d_in, int d_out, int g, uint16_t* Y, hipStream_t s) {
   if (T == 1) return launch_t1<true>(X, nullptr, nullptr, Wp, chunk, scale, rowptr, d_in, d_out, g, 1, Y, s);
+  hipError_t err = hipSuccess;
+  if (T <= 16 && launch_mfma<true>(X, Wp, nullptr, chunk, scale, rowptr, T, d_in, d_out, g, 1, Y, s, err)) return err;
   return gemv_passes<true, 1>(X, nullptr, nullptr, Wp, chunk, scale, rowptr, T, d_in, d_out, g, 1, Y, s);
 }
 

@@ -202,10 +202,8 @@ def test_llama2_13b_inference_path(T):
         t_s = np.arange(T) if T <= 64 else np.sort(workloads.gen.rng_for(5, T).choice(T, 64, replace=False))
         ref, b = ref_fwd(oracle.from_bf16(case.X)[t_s], oracle.from_bf16(case.W), case.mask, g)
         assert_close("Y", host_f64_from_bf16(Y)[t_s], ref, bound=b)
-        if T == 1:  # one kernel reads both layouts: identical results
+        if T <= 16:  # one kernel reads both layouts (one token; 2-16 tokens on MFMA): identical results
             assert np.array_equal(host_bits(Yp), host_bits(Y))
-        elif T <= 16:  # the packed layout keeps the per-row GEMV; in place, 2..16 tokens run on MFMA
-            assert_close("Y (packed)", host_f64_from_bf16(Yp)[t_s], ref, bound=b)
 
 
 @pytest.mark.parametrize("g", [64, 128, 256, 512])
