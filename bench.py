@@ -881,7 +881,9 @@ def _gemv_bandwidth(n_layers, reps):
         out["packed_stacked"] = None
     del packed
     # Each launch shape on its own: the same projection of all layers back to back (serialised on the stream,
-    # as in the pass); the rate of one kernel at one shape, free of the pass's mix of small and large launches.
+    # as in the pass, captured in a HIP graph so that small launches are not timed against the host's per-call
+    # cost; every replay's outputs checked against the eager launches); the rate of one kernel at one shape,
+    # free of the pass's mix of small and large launches.
     per_shape = {}
     for j, name in enumerate(("qkv_stacked", "o", "gateup_stacked", "down")):
         mats = [f[j] for f in fused]
@@ -893,13 +895,30 @@ def _gemv_bandwidth(n_layers, reps):
                 run(mat)
         one()
         torch.cuda.synchronize()
-        t = _events_ms(one, reps)
+        want = [mat[3].clone() for mat in mats]
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            one()
+        ok = True
+        for _ in range(3):
+            for mat in mats:
+                mat[3].zero_()
+            graph.replay()
+            torch.cuda.synchronize()
+            ok = ok and all(torch.equal(mat[3], w) for mat, w in zip(mats, want))
+        if not ok:
+            per_shape[name] = None
+            continue
+        t = _events_ms(graph.replay, reps)
+        del graph
         per_shape[name] = {"rows_x_d_in": list(mats[0][1].shape), "us_per_launch": 1e3 * t / len(mats),
                            "GB/s": nbytes / (t / 1e3) / 1e9}
     out["per_shape"] = per_shape
-    # 8 and 16 tokens over the same weights and masks (eager): seven launches
-    # per layer, and the stacked layout's four (q|k|v and gate|up read one input
-    # each, so the stacked launches read it once)
+    # 8 and 16 tokens over the same weights and masks: seven launches per layer,
+    # and the stacked layout's four (q|k|v and gate|up read one input each, so
+    # the stacked launches read it once); each pass captured in a HIP graph
+    # (replays checked against the eager launches), since a 5120 x 5120 launch
+    # takes about as long on the GPU as the host needs to issue it
     for T in (8, 16):
         for name, mats_of in (("", lambda i: layers[i]), ("stacked_", lambda i: fused[i])):
             xs, ys, nbytes = {}, [], kept_bytes
@@ -916,10 +935,21 @@ def _gemv_bandwidth(n_layers, reps):
                     run(mat)
             serial_t()
             torch.cuda.synchronize()
-            t = _events_ms(serial_t, reps)
-            out[f"T{T}_{name}GB/s"] = nbytes / (t / 1e3) / 1e9
-            out[f"T{T}_{name}ms_per_pass"] = t
-            del ys, xs
+            want = [mat[3].clone() for mat in ys]
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                serial_t()
+            ok = True
+            for _ in range(2):
+                for mat in ys:
+                    mat[3].zero_()
+                graph.replay()
+                torch.cuda.synchronize()
+                ok = ok and all(torch.equal(mat[3], w) for mat, w in zip(ys, want))
+            t = _events_ms(graph.replay, reps) if ok else float("nan")
+            out[f"T{T}_{name}GB/s"] = nbytes / (t / 1e3) / 1e9 if ok else None
+            out[f"T{T}_{name}ms_per_pass"] = t if ok else None
+            del graph, ys, xs, want
     return out
 
 
