@@ -210,6 +210,28 @@ def test_packed_forward(T):
         assert np.array_equal(host_bits(Y), host_bits(Y2))
 
 
+@pytest.mark.parametrize("T,d_in,d_out,g", [
+    (2, 2048, 200, 64),      # 32 groups per row, ragged last block (200 = 6 x 32 + 8 rows)
+    (16, 4096, 72, 512),     # pieces of 512 weights, rows of 8 groups
+    (7, 32768, 40, 64),      # 512 groups per row (the most a row may have): 16-row blocks, a 16 x 512 table
+])
+def test_packed_matches_in_place_at_2_to_16_tokens(T, d_in, d_out, g):
+    import paper_2609_33977_amd as gm
+    say(f"packed vs in place: T={T} d_in={d_in} d_out={d_out} g={g}")
+    case = workloads.make_linear_case((217, T, d_in, g), T, d_in, d_out, g, None)
+    d = _dev_case(case)
+    Wp, chunk, scale, rowptr = _pack(d, g)
+    Yp = empty_bf16(T, d_out)
+    gm.gm_packed_linear_fwd(d["X"], Wp, chunk, scale, rowptr, d_out, g, Yp)
+    sync()
+    Yr, _, _, bY, _, _ = _oracle_all(case)
+    assert_close("Y packed", host_f64_from_bf16(Yp), Yr, bound=bY)
+    Yi = _fwd(d, g)
+    assert_close("Y in place", host_f64_from_bf16(Yi), Yr, bound=bY)
+    # both layouts on the MFMA kernel: the same products in the same order
+    assert np.array_equal(host_bits(Yp), host_bits(Yi))
+
+
 def test_workspace_too_small_is_rejected_without_launch():
     import paper_2609_33977_amd as gm
     T, d_in, d_out, g = 64, 512, 256, 256
