@@ -172,6 +172,28 @@ def _events_batch_ms(fn, n):
     return float(start.elapsed_time(end)) / n
 
 
+def _graph_pass_ms(fn, outs, reps):
+    """fn() captured once in a HIP graph and replayed: the average time of a replay between HIP events, or None
+    when a replay's outputs (zeroed before each of two checked replays) differ from the eager call's."""
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    want = [o.clone() for o in outs]
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        fn()
+    for _ in range(2):
+        for o in outs:
+            o.zero_()
+        graph.replay()
+        torch.cuda.synchronize()
+        if not all(torch.equal(o, w) for o, w in zip(outs, want)):
+            return None
+    ms = _events_ms(graph.replay, reps)
+    del graph
+    return ms
+
+
 def _shift_to_budget(gm, logits, noise, sizes, kept, tau, iters=64):
     """Logits shifted by one offset per selector matrix so that the library's own hard gate keeps
     exactly kept[l] of matrix l's selectors (bisection on the offsets, all matrices at once; nothing
@@ -873,13 +895,11 @@ def _gemv_bandwidth(n_layers, reps):
     serial_fused()
     serial_packed()
     torch.cuda.synchronize()
-    if all(torch.equal(Yp, Y) for *_, Yp, Y in packed):
-        t = _events_ms(serial_packed, reps)
-        out["packed_stacked"] = {"bytes_per_pass": packed_bytes, "GB/s": packed_bytes / (t / 1e3) / 1e9,
-                                 "frac_of_peak": packed_bytes / (t / 1e3) / 1e9 / PEAK_HBM_GBS, "ms_per_pass": t}
-    else:
-        out["packed_stacked"] = None
-    del packed
+    t = _graph_pass_ms(serial_packed, [p[6] for p in packed], reps) \
+        if all(torch.equal(Yp, Y) for *_, Yp, Y in packed) else None
+    out["packed_stacked"] = None if t is None else {
+        "bytes_per_pass": packed_bytes, "GB/s": packed_bytes / (t / 1e3) / 1e9,
+        "frac_of_peak": packed_bytes / (t / 1e3) / 1e9 / PEAK_HBM_GBS, "ms_per_pass": t}
     # Each launch shape on its own: the same projection of all layers back to back (serialised on the stream,
     # as in the pass, captured in a HIP graph so that small launches are not timed against the host's per-call
     # cost; every replay's outputs checked against the eager launches); the rate of one kernel at one shape,
@@ -893,63 +913,53 @@ def _gemv_bandwidth(n_layers, reps):
         def one(mats=mats):
             for mat in mats:
                 run(mat)
-        one()
-        torch.cuda.synchronize()
-        want = [mat[3].clone() for mat in mats]
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            one()
-        ok = True
-        for _ in range(3):
-            for mat in mats:
-                mat[3].zero_()
-            graph.replay()
-            torch.cuda.synchronize()
-            ok = ok and all(torch.equal(mat[3], w) for mat, w in zip(mats, want))
-        if not ok:
-            per_shape[name] = None
-            continue
-        t = _events_ms(graph.replay, reps)
-        del graph
-        per_shape[name] = {"rows_x_d_in": list(mats[0][1].shape), "us_per_launch": 1e3 * t / len(mats),
-                           "GB/s": nbytes / (t / 1e3) / 1e9}
+        t = _graph_pass_ms(one, [mat[3] for mat in mats], reps)
+        per_shape[name] = None if t is None else {
+            "rows_x_d_in": list(mats[0][1].shape), "us_per_launch": 1e3 * t / len(mats),
+            "GB/s": nbytes / (t / 1e3) / 1e9}
     out["per_shape"] = per_shape
     # 8 and 16 tokens over the same weights and masks: seven launches per layer,
-    # and the stacked layout's four (q|k|v and gate|up read one input each, so
-    # the stacked launches read it once); each pass captured in a HIP graph
-    # (replays checked against the eager launches), since a 5120 x 5120 launch
-    # takes about as long on the GPU as the host needs to issue it
+    # the stacked layout's four (q|k|v and gate|up read one input each, so the
+    # stacked launches read it once), and the packed export of the stacked
+    # layout (outputs checked bit for bit against the stacked in-place ones:
+    # both layouts run the same MFMA kernel); each pass captured in a HIP graph,
+    # since a 5120 x 5120 launch takes about as long on the GPU as the host
+    # needs to issue it
     for T in (8, 16):
+        xs = {}
+
+        def x_for(X1):
+            if id(X1) not in xs:
+                xs[id(X1)] = torch.randn(T, X1.shape[1], device="cuda", generator=gen).to(torch.bfloat16)
+            return xs[id(X1)]
+
+        def y_for(d_o):
+            return torch.empty(T, d_o, dtype=torch.bfloat16, device="cuda")
+
+        sched = {}
         for name, mats_of in (("", lambda i: layers[i]), ("stacked_", lambda i: fused[i])):
-            xs, ys, nbytes = {}, [], kept_bytes
+            ys, nbytes = [], kept_bytes
             for i in range(n_layers):
                 for X1, W, m, _ in mats_of(i):
-                    key = id(X1)
-                    if key not in xs:
-                        xs[key] = torch.randn(T, X1.shape[1], device="cuda", generator=gen).to(torch.bfloat16)
-                    ys.append((xs[key], W, m, torch.empty(T, W.shape[0], dtype=torch.bfloat16, device="cuda")))
+                    ys.append((x_for(X1), W, m, y_for(W.shape[0])))
                     nbytes += 4 * m.numel() + 2 * T * (W.shape[0] + W.shape[1])
-
-            def serial_t():
-                for mat in ys:
-                    run(mat)
-            serial_t()
-            torch.cuda.synchronize()
-            want = [mat[3].clone() for mat in ys]
-            graph = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(graph):
-                serial_t()
-            ok = True
-            for _ in range(2):
-                for mat in ys:
-                    mat[3].zero_()
-                graph.replay()
-                torch.cuda.synchronize()
-                ok = ok and all(torch.equal(mat[3], w) for mat, w in zip(ys, want))
-            t = _events_ms(graph.replay, reps) if ok else float("nan")
-            out[f"T{T}_{name}GB/s"] = nbytes / (t / 1e3) / 1e9 if ok else None
-            out[f"T{T}_{name}ms_per_pass"] = t if ok else None
-            del graph, ys, xs, want
+            sched[name] = (ys, nbytes, lambda ys=ys: [run(mat) for mat in ys], [mat[3] for mat in ys])
+        pys, pbytes = [], 0
+        for X1, Wp, chunk, scale, rowptr, d_o, _, _ in packed:
+            pys.append((x_for(X1), Wp, chunk, scale, rowptr, d_o, y_for(d_o)))
+            pbytes += Wp.numel() * 2 + chunk.numel() * 8 + 4 * (d_o + 1) + 2 * T * (X1.shape[1] + d_o)
+        sched["packed_stacked_"] = (pys, pbytes, lambda: [gm.gm_packed_linear_fwd(x, Wp, c, sc, rp, d_o, g, y)
+                                                          for x, Wp, c, sc, rp, d_o, y in pys], [p[6] for p in pys])
+        for name, (ys, nbytes, fn, outs) in sched.items():
+            t = _graph_pass_ms(fn, outs, reps)
+            out[f"T{T}_{name}GB/s"] = None if t is None else nbytes / (t / 1e3) / 1e9
+            out[f"T{T}_{name}ms_per_pass"] = t
+        same = all(torch.equal(a, b) for a, b in zip(sched["packed_stacked_"][3], sched["stacked_"][3]))
+        out[f"T{T}_packed_equals_in_place"] = bool(same)
+        if not same:
+            out[f"T{T}_packed_stacked_GB/s"] = None
+        del sched, pys, xs
+    del packed
     return out
 
 
