@@ -172,10 +172,10 @@ __device__ __forceinline__ u32x4 ld16_rsrc(__amdgpu_buffer_rsrc_t r, uint32_t of
 // the same K loop: the block turns its rows' piece lists into the same
 // (row, group) table, with each kept group's piece index beside its selector,
 // and reads the pieces instead of W's rows; both layouts therefore give
-// identical results.  The weights go through
-// the caches: an instruction reads 64 bytes of each of 16 rows, and the other
-// half of each 128-byte line is requested by the very next instruction
-// (nontemporal loads measured 3-8 % slower here).
+// identical results.  The weights go through the caches: an instruction
+// reads 64 bytes of each of 16 rows, and the other half of each 128-byte line
+// is requested by the very next instruction (nontemporal loads measured 3-8 %
+// slower here).
 constexpr int kMmaWaves = 8;
 constexpr int kMmaMaskFloats = 8192;  // staged mask floats per block: mask rows of the block x selectors per row
 
