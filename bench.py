@@ -51,7 +51,7 @@ GEMM_SOURCES = ["paper_2609_33977_amd/csrc/gemm.hip", "paper_2609_33977_amd/csrc
 # bytes).  The numbers describe the kernel built from sources with this digest
 # and are reported only while the sources still match it (None: not measured).
 DGATE_TRAFFIC = {"sources_sha256": "057756bdcffe5d61c12d9c057a15afa67a58f6b14794c46ab7914d0b50d0e0b3",
-                 "fetch_kib": 218501.6, "write_kib": 596.4, "fetch_scale": 2.0, "write_scale": 1.0}
+                 "launch_mix": "separate", "fetch_kib": 218501.6, "write_kib": 596.4, "fetch_scale": 2.0, "write_scale": 1.0}
 
 
 def _progress(msg: str) -> None:
@@ -68,9 +68,13 @@ def _sources_digest() -> str:
     return h.hexdigest()
 
 
-def _dgate_traffic_bytes():
+def _dgate_traffic_bytes(launch_mix=None):
+    """Calibrated HBM bytes per dgate launch of the roofline batches, while the GEMM sources and the launch mix
+    (which linears the batches launch: "separate" or "stacked") are the ones the counters were taken on."""
     t = DGATE_TRAFFIC
     if t["sources_sha256"] is None or t["sources_sha256"] != _sources_digest():
+        return None
+    if launch_mix is not None and launch_mix != t["launch_mix"]:
         return None
     return (t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"]) * 1024.0
 
@@ -230,11 +234,18 @@ def _shift_to_budget(gm, logits, noise, sizes, kept, tau, iters=64):
 class ModelStep:
     """One mask-learning step over several masked linears whose selectors share one flat array: one gate
     call over all of them, every linear's forward, every linear's backward (dX and dgate, last linear
-    first), one STE call.  Each linear has its own X, W and dY (drawn on the device).  The gate inputs are
-    independent draws, logits ~ N(0,1) and u ~ U(0,1), with each matrix's logits shifted so that the
-    library's gate keeps exactly that matrix's budget."""
+    first), one STE call.  The gate inputs are independent draws, logits ~ N(0,1) and u ~ U(0,1), with each
+    matrix's logits shifted so that the library's gate keeps exactly that matrix's budget.
 
-    def __init__(self, T, shapes, kept, g, tau, key):
+    groups (default: every linear alone) lists runs of consecutive linears that read one input, e.g. a
+    layer's q, k and v: each run is stored and launched as one stacked linear (weights, selectors, output
+    and output gradient of its members one after the other, as the fused layouts of inference and training
+    frameworks keep them).  Its forward gives every member's Y, its dgate every member's selector gradient,
+    and its dX the sum of the members' input gradients, which is what the shared input receives.  The
+    members' selectors are contiguous in the flat array, so the gate and the budgets are those of the
+    separate linears.  Each launch has its own X, W and dY (drawn on the device)."""
+
+    def __init__(self, T, shapes, kept, g, tau, key, groups=None):
         import torch
         import paper_2609_33977_amd as gm
         import workloads
@@ -255,10 +266,16 @@ class ModelStep:
         self.kept_target = int(sum(kept))
         gen = torch.Generator(device=dev)
         gen.manual_seed(workloads.SEED + 1000 * key[0] + key[1])
+        self.groups = [(l,) for l in range(len(self.shapes))] if groups is None else [tuple(gr) for gr in groups]
+        if sorted(l for gr in self.groups for l in gr) != list(range(len(self.shapes))) or any(
+                list(gr) != list(range(gr[0], gr[0] + len(gr))) or len({self.shapes[l][1] for l in gr}) != 1
+                for gr in self.groups):
+            raise ValueError("groups must cover every linear once, as runs of consecutive linears of one d_in")
         self.lin = []
         fws = bws = 16
-        for l, (d_out, d_in) in enumerate(self.shapes):
-            lo, hi = int(self.offsets[l]), int(self.offsets[l + 1])
+        for gr in self.groups:
+            d_out, d_in = sum(self.shapes[l][0] for l in gr), self.shapes[gr[0]][1]
+            lo, hi = int(self.offsets[gr[0]]), int(self.offsets[gr[-1] + 1])
             X = torch.randn(T, d_in, device=dev, generator=gen).to(torch.bfloat16)
             W = (torch.randn(d_out, d_in, device=dev, generator=gen) * 0.02).to(torch.bfloat16)
             dY = torch.randn(T, d_out, device=dev, generator=gen).to(torch.bfloat16)
@@ -414,6 +431,12 @@ def _llama2_7b_shapes():
     sizes = [o * (i // g) for o, i in shapes]
     kept, _ = workloads.kept_counts_beta_law(workloads.gen.rng_for(4, 0), sizes, [o * i for o, i in shapes], 0.5)
     return cfg, shapes, kept
+
+
+def _llama2_7b_groups(layers):
+    """Per layer, q|k|v and gate|up (each run reads one input) as one stacked linear; o and down alone."""
+    return [gr for l in range(layers) for gr in ((7 * l, 7 * l + 1, 7 * l + 2), (7 * l + 3,), (7 * l + 4, 7 * l + 5),
+                                                 (7 * l + 6,))]
 
 
 LLAMA2_7B_WORKLOAD = ("LLaMA-2-7B mask-learning step: all 224 masked linears (32 layers x q,k,v,o 4096x4096, "
@@ -1162,6 +1185,20 @@ def main():
     del step
     torch.cuda.empty_cache()
 
+    # The same step with the linears that read one input (q|k|v, gate|up) launched as one stacked linear each
+    # (four launches per layer and phase, as fused layouts keep them): the same counted work, another schedule.
+    _progress("headline step with q|k|v and gate|up stacked")
+    stk = ModelStep(cfg["T"], shapes, kept, cfg["g"], cfg["tau"], (4, 1), groups=_llama2_7b_groups(cfg["layers"]))
+    for _ in range(2):
+        stk()
+    torch.cuda.synchronize()
+    stk_ms = _events_batch_ms(stk, max(3, args.steps // 2))
+    stacked = {"launches_per_phase": len(stk.lin), "ms_per_step": stk_ms,
+               "TFLOP/s": flops_step / (stk_ms / 1e3) / 1e12,
+               "breakdown_ms": {name: _events_batch_ms(getattr(stk, name), reps) for name in ("fwd", "bwd")}}
+    del stk
+    torch.cuda.empty_cache()
+
     if args.profile_copy_mib:
         src = torch.empty(args.profile_copy_mib << 20, dtype=torch.uint8, device="cuda").fill_(1)
         dst = torch.empty_like(src)
@@ -1220,7 +1257,7 @@ def main():
         "frac_of_bf16_peak": tflops / PEAK_BF16_TFLOPS,
         "roofline": {"bound": "mfma", "achieved": roof["achieved_TFLOP/s"], "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": roof["achieved_TFLOP/s"] / PEAK_BF16_TFLOPS,
-                     "traffic": _dgate_traffic_bytes()},
+                     "traffic": _dgate_traffic_bytes("separate")},
         "kernels": {"dominant": "dgate_kernel<256, 1> (X^T dY tile + fused W-weighted group reduction), one launch "
                                 "per linear: 128 of 4096x4096, 64 of 11008x4096, 32 of 4096x11008 per step",
                     "dgate_flops_per_launch": roof["flops_per_launch"], "dgate_avg_launch_ms": roof["avg_launch_ms"],
@@ -1230,7 +1267,8 @@ def main():
                                                           / len(shapes),
                     "sources_sha256": _sources_digest(), "breakdown_ms": breakdown,
                     "fwd_kept_TFLOP/s": flops["fwd"] / (breakdown["fwd"] / 1e3) / 1e12,
-                    "bwd_TFLOP/s": (flops["dx"] + flops["dgate"]) / (breakdown["bwd"] / 1e3) / 1e12},
+                    "bwd_TFLOP/s": (flops["dx"] + flops["dgate"]) / (breakdown["bwd"] / 1e3) / 1e12,
+                    "stacked_launches": stacked},
         "gate": gate_leg,
         "cpu_baseline": cpu,
         "single_linear": single,

@@ -52,10 +52,13 @@ def test_traffic_follows_the_counted_sources():
     if t["sources_sha256"] is not None and t["sources_sha256"] == b._sources_digest():
         expected = (t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"]) * 1024.0
         assert b._dgate_traffic_bytes() == expected
+        assert b._dgate_traffic_bytes(t["launch_mix"]) == expected
+        assert b._dgate_traffic_bytes("another launch mix") is None
         # the committed counter summary is of these sources and these readings
         with open(os.path.join(ROOT, "profiles", "dgate_kernel_llama2_7b_step_traffic.md")) as f:
             text = f.read()
         assert t["sources_sha256"] in text
+        assert f'launch mix: {t["launch_mix"]}' in text
         assert re.search(r"\b%.1f\b" % t["fetch_kib"], text)
     else:
         assert b._dgate_traffic_bytes() is None

@@ -339,3 +339,42 @@ def test_decode_degenerate_rows(T):
     zeros = np.zeros_like(m)
     Yz = _fwd(_dev_case(case, zeros), g)
     assert not np.any(host_bits(Yz) & 0x7FFF)
+
+
+def test_stacked_linears_match_their_members():
+    # linears that read one input (a layer's q, k and v) launched as one stacked linear: its Y is the members'
+    # Y side by side and its dgate their dgate (bit for bit), and its dX the sum the shared input receives
+    import torch
+    T, d_in, g = 300, 1024, 256
+    rows = (512, 384, 128)  # member boundaries on and off the 256-row tiles
+    say(f"stacked linears: T={T} rows={rows}")
+    cases = [workloads.make_linear_case((218, j), T, d_in, r, g, None) for j, r in enumerate(rows)]
+    X = cases[0].X
+    members = []
+    for c in cases:
+        d = _dev_case(c)
+        d["X"] = dev_bf16(X)
+        members.append(d)
+    import paper_2609_33977_amd as gm
+
+    def fwd_unsplit(d):  # no workspace: K is not split, so the two tilings sum each element in one order
+        Y = empty_bf16(T, d["W"].shape[0])
+        gm.gm_masked_linear_fwd(d["X"], d["W"], d["mask"], g, Y)
+        sync()
+        return Y
+    Ys = [fwd_unsplit(d) for d in members]
+    bw = [_bwd(d, g) for d in members]
+    stack = dict(X=dev_bf16(X), W=torch.cat([d["W"] for d in members]), mask=torch.cat([d["mask"] for d in members]),
+                 dY=torch.cat([d["dY"] for d in members], dim=1).contiguous())
+    Y = fwd_unsplit(stack)
+    dX, dgate = _bwd(stack, g)
+    assert torch.equal(Y, torch.cat(Ys, dim=1))
+    assert torch.equal(dgate, torch.cat([b[1] for b in bw]))
+    m = np.concatenate([c.mask for c in cases])
+    W = np.concatenate([oracle.from_bf16(c.W) for c in cases])
+    dY = np.concatenate([oracle.from_bf16(c.dY) for c in cases], axis=1)
+    ref, bnd = ref_dx(dY, W, m, g)
+    assert_close("dX (stack)", host_f64_from_bf16(dX), ref, bound=bnd)
+    # the members' dX summed in fp32 agree with it to their bf16 rounding
+    summed = sum(host_f64_from_bf16(b[0]) for b in bw)
+    assert_close("dX (sum of members)", summed, ref, tol=1e-2)
