@@ -378,3 +378,36 @@ def test_stacked_linears_match_their_members():
     # the members' dX summed in fp32 agree with it to their bf16 rounding
     summed = sum(host_f64_from_bf16(b[0]) for b in bw)
     assert_close("dX (sum of members)", summed, ref, tol=1e-2)
+
+
+def test_debug_sync_mode_gives_the_same_results(tmp_path):
+    # GM_DEBUG is read once per process: a child process runs the same forward and
+    # backward with a device synchronisation and error check after every launch
+    import os
+    import subprocess
+    import sys
+    T, d_in, d_out, g = 200, 1024, 512, 256
+    say("GM_DEBUG=sync in a child process")
+    case = workloads.make_linear_case((219,), T, d_in, d_out, g, None)
+    d = _dev_case(case)
+    Y = host_bits(_fwd(d, g))
+    dX, dgate = _bwd(d, g)
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    out = tmp_path / "child.npz"
+    code = f"""
+import sys
+sys.path[:0] = [{root!r}, {os.path.join(root, 'tests')!r}]
+import numpy as np, workloads, test_gpu_linear as t
+case = workloads.make_linear_case((219,), {T}, {d_in}, {d_out}, {g}, None)
+d = t._dev_case(case)
+Y = t.host_bits(t._fwd(d, {g}))
+dX, dgate = t._bwd(d, {g})
+np.savez({str(out)!r}, Y=Y, dX=t.host_bits(dX), dgate=dgate.cpu().numpy())
+"""
+    env = dict(os.environ, GM_DEBUG="sync")
+    r = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True, timeout=240)
+    assert r.returncode == 0, r.stderr[-2000:]
+    got = np.load(out)
+    assert np.array_equal(got["Y"], Y)
+    assert np.array_equal(got["dX"], host_bits(dX))
+    assert np.array_equal(got["dgate"], dgate.cpu().numpy())
