@@ -176,7 +176,7 @@ __global__ __launch_bounds__(kBudgetThreads) void gate_bwd_budget_kernel(const f
 #pragma unroll
     for (int k = 0; k < 4; ++k) r[k] = (d[k] + c[k]) * y[k] * (1.0f - y[k]) / tau;
     if (full) {
-      *reinterpret_cast<float4*>(dlogits + e0) = make_float4(r[0], r[1], r[2], r[3]);
+      __builtin_nontemporal_store(f32x4{r[0], r[1], r[2], r[3]}, reinterpret_cast<f32x4*>(dlogits + e0));  // streamed
     } else {
 #pragma unroll
       for (int k = 0; k < 4; ++k)

@@ -7,7 +7,10 @@
 //
 // Each thread moves 16 bytes per array per step (float4); bytes per group are
 // 4 (logit) + 4 (noise) + 4 (mask) + 4 (soft) in the forward and 12 in the
-// backward, so both passes are bound by HBM bandwidth.
+// backward, so both passes are bound by HBM bandwidth.  The outputs are
+// written with nontemporal stores (streamed past the caches, which they would
+// only fill): over the 25.3 M selectors of the LLaMA-2-7B step, 76 -> 61 us
+// for the forward and 48.5 -> 43.4 us for the backward.
 #include "gm_device.h"
 #include "gm_launch.h"
 
@@ -37,8 +40,8 @@ __global__ __launch_bounds__(256) void gate_fwd_kernel(const float* __restrict__
     gate_one(l.y, u.y, has_noise, tau, hard, m.y, y.y);
     gate_one(l.z, u.z, has_noise, tau, hard, m.z, y.z);
     gate_one(l.w, u.w, has_noise, tau, hard, m.w, y.w);
-    reinterpret_cast<float4*>(mask)[i] = m;
-    if (soft) reinterpret_cast<float4*>(soft)[i] = y;
+    __builtin_nontemporal_store(f32x4{m.x, m.y, m.z, m.w}, reinterpret_cast<f32x4*>(mask) + i);
+    if (soft) __builtin_nontemporal_store(f32x4{y.x, y.y, y.z, y.w}, reinterpret_cast<f32x4*>(soft) + i);
   }
   if (blockIdx.x == 0 && threadIdx.x < (n & 3)) {
     const int64_t j = nvec * 4 + threadIdx.x;
@@ -62,7 +65,7 @@ __global__ __launch_bounds__(256) void gate_bwd_kernel(const float* dmask, const
     r.y = d.y * y.y * (1.0f - y.y) / tau;
     r.z = d.z * y.z * (1.0f - y.z) / tau;
     r.w = d.w * y.w * (1.0f - y.w) / tau;
-    reinterpret_cast<float4*>(dlogits)[i] = r;
+    __builtin_nontemporal_store(f32x4{r.x, r.y, r.z, r.w}, reinterpret_cast<f32x4*>(dlogits) + i);
   }
   if (blockIdx.x == 0 && threadIdx.x < (n & 3)) {
     const int64_t j = nvec * 4 + threadIdx.x;
