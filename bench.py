@@ -59,12 +59,17 @@ def _progress(msg: str) -> None:
     print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
 
 
-def _sources_digest() -> str:
+def _sources_digest():
+    """sha256 over the GEMM sources, or None when one of them is absent (a tree with the built library only):
+    the stored traffic figure is then not claimed."""
     import hashlib
     h = hashlib.sha256()
     for rel in GEMM_SOURCES:
-        with open(os.path.join(HERE, rel), "rb") as f:
-            h.update(f.read())
+        try:
+            with open(os.path.join(HERE, rel), "rb") as f:
+                h.update(f.read())
+        except FileNotFoundError:
+            return None
     return h.hexdigest()
 
 
