@@ -28,6 +28,10 @@ namespace gm {
 constexpr int kLmWaves = 8;
 constexpr int kLmTokens = 128;  // tokens of each pass per forward tile
 constexpr int kLmStats = 5;     // m_T, s_T, m_S, s_S, c per token and vocabulary tile
+// MFMA rows of a wave tile issued after each slice's barrier in the K-loop:
+// four measured 1.6 % faster for the backward GEMM and 0.6 % slower for the
+// forward one (whose epilogue dominates), so the forward keeps one.
+constexpr int kLmFwdRowsAfter = 1, kLmBwdRowsAfter = 4;
 
 // (m, s) <- merge of two (max, sum of exp(x - max)) summaries; an empty one has m = -inf, s = 0.
 __device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2) {
@@ -105,8 +109,8 @@ __global__ __launch_bounds__(64 * kLmWaves) void lmhead_fwd_kernel(const uint16_
       dma16_group(j, rB, offB[j], ldsB + dst);
   };
   f32x4 acc[MB][NB];
-  gemm_mainloop<MB, NB, true, true, 0, 0, PER_STAGE, STAGES>(As, Bs, nst, wm * 128, wn * NB * 16, lane, acc, prepare,
-                                                            issue, [](int) {}, [](int, const u32x4(&)[NB]) {});
+  gemm_mainloop<MB, NB, true, true, 0, 0, PER_STAGE, STAGES, kLmFwdRowsAfter>(
+      As, Bs, nst, wm * 128, wn * NB * 16, lane, acc, prepare, issue, [](int) {}, [](int, const u32x4(&)[NB]) {});
 
   // Lane (q = l >> 4, r = l & 15) holds, for every (mb, nb), rows v .. v + 3 of token column tl.
   const bool teacher = wn < WN / 2;
@@ -365,9 +369,8 @@ __global__ __launch_bounds__(64 * kLmWaves) void lmhead_bwd_kernel(const uint16_
       dma16_group(j, rB, offB[j], ldsB + dst);
   };
   f32x4 acc[MB][NB];
-  gemm_mainloop<MB, NB, false, true, BM, 0, PER_STAGE, STAGES>(As, Bs, nst, wm * 128, wn * NB * 16, lane, acc,
-                                                              prepare, issue, [](int) {},
-                                                              [](int, const u32x4(&)[NB]) {});
+  gemm_mainloop<MB, NB, false, true, BM, 0, PER_STAGE, STAGES, kLmBwdRowsAfter>(
+      As, Bs, nst, wm * 128, wn * NB * 16, lane, acc, prepare, issue, [](int) {}, [](int, const u32x4(&)[NB]) {});
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll

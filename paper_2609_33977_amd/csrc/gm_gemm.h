@@ -90,22 +90,29 @@ struct AllRows {
 // kt; rows whose A operand is all zeros for the slice skip them.  The first
 // slice runs every row, since its MFMAs also initialise the accumulators.
 //
-// Software pipeline: rows 0 .. MB-2 of slice kt run first (A fragments
-// streamed one row ahead); then the wave waits for slice kt+1, meets the
-// others at the barrier (which also frees buffer kt % STAGES), and issues the
-// last MFMA row of slice kt interleaved with the copies of slice kt + STAGES
-// and the reads of slice kt+1's B fragments into the registers each MFMA has
-// just consumed.  Copies run STAGES slices ahead; fragment-read latency and
-// copy issue hide behind MFMA work.  Every iteration issues exactly PER_STAGE
-// copies (slices past the end copy zeros), so the wait count is a constant,
-// and the loop body has no branches around the accumulators; the first and
-// the last slice are peeled off.
-template <int MB, int NB, bool A_KM, bool B_KM, int CA, int CB, int PER_STAGE, int STAGES, int ABUF, int BBUF,
+// Software pipeline: rows 0 .. MB-RA-1 of slice kt run first (A fragments
+// streamed one row ahead), and the A fragments of the last RA rows are read;
+// then the wave waits for slice kt+1, meets the others at the barrier (which
+// also frees buffer kt % STAGES), and issues the last RA MFMA rows of slice kt
+// column by column, interleaved with the copies of slice kt + STAGES and the
+// reads of slice kt+1's B fragments into the registers those MFMAs have just
+// consumed.  Copies run STAGES slices ahead; fragment-read latency and copy
+// issue hide behind MFMA work.  RA (rows after the barrier; 1 <= RA <= MB)
+// trades MFMAs that cover the barrier wait against MFMAs that cover the next
+// slice's B-fragment reads: with MB = 8, four rows after the barrier measured
+// 2.5-5 % faster than one for the forward and dgate (six or eight: slower),
+// level for dX.  The MFMAs of each accumulator keep their order, so RA does
+// not change any result.  Every iteration issues exactly PER_STAGE copies
+// (slices past the end copy zeros), so the wait count is a constant, and the
+// loop body has no branches around the accumulators; the first and the last
+// slice are peeled off.
+template <int MB, int NB, bool A_KM, bool B_KM, int CA, int CB, int PER_STAGE, int STAGES, int RA, int ABUF, int BBUF,
           class Prepare, class Issue, class Landed, class BHook, class Live = AllRows>
 __device__ __forceinline__ void gemm_mainloop(u32x4 (*As)[ABUF], u32x4 (*Bs)[BBUF], int nst, int a0, int b0, int lane,
                                               f32x4 (&acc)[MB][NB], Prepare&& prepare, Issue&& issue,
                                               Landed&& landed, BHook&& bhook, Live live = Live{}) {
   static_assert(PER_STAGE <= NB, "copies are interleaved with the NB MFMAs of one row");
+  static_assert(RA >= 1 && RA <= MB, "rows after the barrier");
   constexpr int AHEAD = PER_STAGE * (STAGES - 2);  // copies issued after the slice being waited for
   if (nst <= 0) {
 #pragma unroll
@@ -139,11 +146,15 @@ __device__ __forceinline__ void gemm_mainloop(u32x4 (*As)[ABUF], u32x4 (*Bs)[BBU
     bhook(kt, bf);
     const u32x4* A = As[kt % STAGES];
 #pragma unroll
-    for (int mb = 0; mb < MB - 1; ++mb) {
+    for (int mb = 0; mb < MB - RA; ++mb) {
       const u32x4 an = load_afrag<A_KM, CA>(A, a0 + (mb + 1) * 16, lane);
       if ((lv >> mb) & 1u) mfma_row<FIRST, MB, NB>(mb, af, bf, acc);
       af = an;
     }
+    u32x4 ar[RA];  // A fragments of the rows after the barrier
+    ar[0] = af;
+#pragma unroll
+    for (int r = 1; r < RA; ++r) ar[r] = load_afrag<A_KM, CA>(A, a0 + (MB - RA + r) * 16, lane);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's reads of slice kt are done
     prepare(kt + STAGES);
     wait_vmcnt<AHEAD>();                                 // ... and its copies of slice kt+1
@@ -152,7 +163,9 @@ __device__ __forceinline__ void gemm_mainloop(u32x4 (*As)[ABUF], u32x4 (*Bs)[BBU
     const u32x4* Bn = Bs[(kt + 1) % STAGES];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      if ((lv >> (MB - 1)) & 1u) mfma_at<FIRST, MB, NB>(MB - 1, nb, af, bf[nb], acc);
+#pragma unroll
+      for (int r = 0; r < RA; ++r)
+        if ((lv >> (MB - RA + r)) & 1u) mfma_at<FIRST, MB, NB>(MB - RA + r, nb, ar[r], bf[nb], acc);
       __builtin_amdgcn_sched_barrier(0);
       if (nb < PER_STAGE) issue(kt + STAGES, nb);
       bf[nb] = B_KM ? km_frag(Bn, b0 + nb * 16, lane) : mn_frag<CB>(Bn, b0 + nb * 16, lane);
