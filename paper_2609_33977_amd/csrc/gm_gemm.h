@@ -138,8 +138,9 @@ __device__ __forceinline__ void gemm_mainloop(u32x4 (*As)[ABUF], u32x4 (*Bs)[BBU
   load_bfrags<NB, B_KM, CB>(Bs[0], b0, lane, bf);
   af = load_afrag<A_KM, CA>(As[0], a0, lane);
 
-  // One slice that is followed by another: rows 0 .. MB-2, the barrier, then
-  // the last row interleaved with the next slice's copies and fragment reads.
+  // One slice that is followed by another: rows 0 .. MB-RA-1, the barrier,
+  // then the last RA rows interleaved with the next slice's copies and
+  // fragment reads.
   auto slice = [&](int kt, auto first) {
     constexpr bool FIRST = decltype(first)::value;
     const uint32_t lv = FIRST ? ~0u : live(kt);
