@@ -88,6 +88,25 @@ def test_soft_mask_scales_groups(T, d_in, d_out, g):
     assert_close("dgate", dgate.cpu().numpy(), dgr, bound=bdg)
 
 
+@pytest.mark.parametrize("where", ["first", "middle", "last"])
+def test_soft_selectors_in_one_chunk_of_a_long_column(where):
+    """Column lists are built per 1024-row chunk: a column whose only fractional
+    selectors lie in one chunk (first, middle or last of three, the last one
+    ragged) must still be marked soft, so that dX scales those rows."""
+    T, d_in, d_out, g = 64, 512, 3000, 256
+    say(f"soft selectors only in the {where} 1024-row chunk: T={T} d_in={d_in} d_out={d_out} g={g}")
+    case = workloads.make_linear_case((231, T), T, d_in, d_out, g, None)
+    m = case.mask.astype(np.float32).copy()
+    lo = {"first": 0, "middle": 1024, "last": 2048}[where]
+    rows = np.arange(lo + 5, min(lo + 1024, d_out), 97)
+    m[rows, 0] = np.where(np.arange(rows.size) % 2, 0.5, 1.25).astype(np.float32)  # column 0 only
+    d = _dev_case(case, m)
+    dX, dgate = _bwd(d, g)
+    Yr, dXr, dgr, bY, bdX, bdg = _oracle_all(case, m)
+    assert_close("dX", host_f64_from_bf16(dX), dXr, bound=bdX)
+    assert_close("dgate", dgate.cpu().numpy(), dgr, bound=bdg)
+
+
 def test_all_ones_is_dense_and_all_zeros_is_exact_zero():
     import torch
     T, d_in, d_out, g = 256, 1024, 768, 256

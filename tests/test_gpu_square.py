@@ -94,6 +94,24 @@ def test_square_soft_mask(g):
     assert_close("dgate", dgate.cpu().numpy(), dgr, bound=bdg)
 
 
+@pytest.mark.parametrize("g", [16, 32])
+def test_square_soft_selectors_in_the_first_chunk_only(g):
+    """List columns of 64 input columns hold 64/g group columns and are built per
+    1024-row chunk: fractional selectors only in the rows of the first chunk
+    (of three, the last one ragged) must still mark the list column soft."""
+    T, d_in, d_out = 64, 512, 3008
+    say(f"square {g}x{g}: soft selectors only in the first 1024-row chunk, d_out={d_out}")
+    case = _case((232, g), T, d_in, d_out, g)
+    m = case.mask.astype(np.float32).copy()
+    u = np.arange(1, 1024 // g, 5)           # mask rows inside output rows 0 .. 1023
+    m[u, 1] = np.where(np.arange(u.size) % 2, 0.5, 1.25).astype(np.float32)  # group column 1 (list column 0)
+    d = _dev(case, m)
+    dX, dgate = _bwd(d, g)
+    Yr, dXr, dgr, bY, bdX, bdg = _oracle(case, m)
+    assert_close("dX", host_f64_from_bf16(dX), dXr, bound=bdX)
+    assert_close("dgate", dgate.cpu().numpy(), dgr, bound=bdg)
+
+
 @pytest.mark.parametrize("g", [16, 128])
 def test_square_dense_and_empty_masks(g):
     T, d_in, d_out = 256, 1024, 768
