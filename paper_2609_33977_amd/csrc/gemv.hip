@@ -14,6 +14,7 @@
 //              by the export (Appendix F), the row's groups contiguous.
 #include "gm_device.h"
 #include "gm_launch.h"
+#include "gm_pipe.h"
 
 namespace gm {
 
@@ -181,14 +182,20 @@ __device__ __forceinline__ u32x4 ld16_rsrc(__amdgpu_buffer_rsrc_t r, uint32_t of
 // loaded with four adjacent lanes per 64-byte row segment (one access per
 // kept row) and moved into the operand layout with ds_bpermute: 4-10 %
 // faster on the LLaMA-2-13B shapes at 2-16 tokens, identical results.
-// Loading X the same way saved 0.5 us at 16 tokens and cost as much at 2 and
-// 8 (more permutes, fewer tokens to coalesce), so X keeps the operand layout.
+// X has the same problem (one access per active lane).  Permuting it too
+// saved 0.5 us at 16 tokens and cost as much at 2 and 8; copying each batch's
+// X slices into LDS with buffer loads (four lanes per token segment) and
+// reading the operands from there is 2-4 % faster for blocks of 64 rows at
+// every token count and for 32-row blocks at 16 tokens (2-5 %), but 2-4 %
+// slower for 32-row blocks at 2 and 8 tokens, which keep the direct loads.
 constexpr int kMmaWaves = 8;
 constexpr int kMmaMaskFloats = 8192;  // staged mask floats per block: mask rows of the block x selectors per row
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-template <int RT, bool PACKED>
+// XL: X goes through LDS (see the K loop); the launcher picks it for blocks of
+// 64 rows, or more than 8 tokens, where it measured 2-5 % faster.
+template <int RT, bool PACKED, bool XL>
 __global__ __launch_bounds__(64 * kMmaWaves) void gemv_mfma_kernel(const uint16_t* __restrict__ X,
                                                                   const uint16_t* __restrict__ W,
                                                                   const float* __restrict__ mask,
@@ -203,6 +210,7 @@ __global__ __launch_bounds__(64 * kMmaWaves) void gemv_mfma_kernel(const uint16_
   __shared__ int s_idx[PACKED ? kMmaMaskFloats : 1];  // packed: piece of (row, group) from the block's first piece
   __shared__ int s_rp[PACKED ? R + 1 : 1];
   __shared__ f32x4 s_part[kMmaWaves][RT][64];
+  __shared__ u32x4 s_x[kMmaWaves][XL ? 4 * 64 : 1];  // XL: per wave, the X slices of one load batch
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int o0 = blockIdx.x * R;
   const int G_in = d_in / g;
@@ -267,6 +275,16 @@ __global__ __launch_bounds__(64 * kMmaWaves) void gemv_mfma_kernel(const uint16_
   }
   const bool tok = r < T;
   const uint32_t xrow = (uint32_t(tok ? r : 0) * uint32_t(d_in) + uint32_t(8 * kc)) * 2u;
+  // XL: four adjacent lanes copy one token's 64-byte segment of a slice into
+  // LDS (lane 4 t + j takes chunk j ^ ((t >> 2) & 3), so that the operand
+  // reads, chunk kc of token r, hit distinct banks): one cache access per
+  // token instead of one per lane.
+  const int xt = lane >> 2;
+  const bool xtok = xt < T;
+  const uint32_t xoff = (uint32_t(xtok ? xt : 0) * uint32_t(d_in) + uint32_t(8 * ((lane & 3) ^ ((xt >> 2) & 3)))) * 2u;
+  const i32x4_t rxd = make_rsrc_grouped(X, uint32_t(T) * uint32_t(d_in) * 2u);
+  const uint32_t xlds = XL ? lds_addr(&s_x[wave][0]) : 0u;
+  const int xread = r * 4 + ((kc ^ (r >> 2)) & 3);  // this lane's operand chunk in a slice of s_x
   // the block's rows of W (packed: the block's pieces) and the T rows of X
   // (the launcher keeps both under 2 GiB)
   const __amdgpu_buffer_rsrc_t rw =
@@ -307,6 +325,13 @@ __global__ __launch_bounds__(64 * kMmaWaves) void gemv_mfma_kernel(const uint16_
     for (int sb = s0; sb < s1; sb += U) {
       float m[RT][U];
       u32x4 av[RT][U], bv[U];
+      if constexpr (XL) {  // before the weight loads, so that the wait below counts those after them
+        static_assert(U == 4, "one grouped copy per slice of the batch");
+        dma16_group<0>(rxd, group_voffset(sb + 0 < s1 && xtok ? xoff + uint32_t(sb + 0) * 64u : kOOB, 0), xlds);
+        dma16_group<1>(rxd, group_voffset(sb + 1 < s1 && xtok ? xoff + uint32_t(sb + 1) * 64u : kOOB, 1), xlds);
+        dma16_group<2>(rxd, group_voffset(sb + 2 < s1 && xtok ? xoff + uint32_t(sb + 2) * 64u : kOOB, 2), xlds);
+        dma16_group<3>(rxd, group_voffset(sb + 3 < s1 && xtok ? xoff + uint32_t(sb + 3) * 64u : kOOB, 3), xlds);
+      }
       // Row tile by row tile, consecutive slices back to back: the two 64-byte
       // halves of a row's 128-byte line (slices 2j and 2j + 1) are requested by
       // adjacent instructions (measured 15-25 % faster on 13824 x 5120 than
@@ -319,10 +344,17 @@ __global__ __launch_bounds__(64 * kMmaWaves) void gemv_mfma_kernel(const uint16_
           const uint32_t off = PACKED ? on[rt][q] : wrow[rt] + uint32_t(sb + q) * 64u;
           av[rt][q] = ld16_rsrc(rw, m[rt][q] != 0.0f ? off : kOutOfRange, 0);
         }
+      if constexpr (XL) {
+        read_masks(sb + U);
+        wait_vmcnt<RT * U>();  // the X copies (issued before the RT U weight loads) have landed
 #pragma unroll
-      for (int q = 0; q < U; ++q)
-        bv[q] = ld16_rsrc(rx, sb + q < s1 && tok ? xrow + uint32_t(sb + q) * 64u : kOutOfRange, 0);
-      read_masks(sb + U);
+        for (int q = 0; q < U; ++q) bv[q] = s_x[wave][q * 64 + xread];
+      } else {
+#pragma unroll
+        for (int q = 0; q < U; ++q)
+          bv[q] = ld16_rsrc(rx, sb + q < s1 && tok ? xrow + uint32_t(sb + q) * 64u : kOutOfRange, 0);
+        read_masks(sb + U);
+      }
 #pragma unroll
       for (int q = 0; q < U; ++q)
 #pragma unroll
@@ -550,15 +582,18 @@ static bool launch_mfma(const uint16_t* X, const uint16_t* W, const float* mask,
   const int64_t span = int64_t(16 * rt > T ? 16 * rt : T) * d_in * 2;
   if (!fits(16 * rt) || span >= int64_t(kOutOfRange)) return false;
   const dim3 grid(unsigned((d_out + 16 * rt - 1) / (16 * rt))), block(64 * kMmaWaves);
-  if (rt == 4)
-    hipLaunchKernelGGL((gemv_mfma_kernel<4, PACKED>), grid, block, 0, s, X, W, mask, chunk, scale, rowptr, T, d_in,
-                       d_out, g, go, Y);
-  else if (rt == 2)
-    hipLaunchKernelGGL((gemv_mfma_kernel<2, PACKED>), grid, block, 0, s, X, W, mask, chunk, scale, rowptr, T, d_in,
-                       d_out, g, go, Y);
-  else
-    hipLaunchKernelGGL((gemv_mfma_kernel<1, PACKED>), grid, block, 0, s, X, W, mask, chunk, scale, rowptr, T, d_in,
-                       d_out, g, go, Y);
+  const bool xl = rt == 4 || T > 8;
+#define GM_MFMA_LAUNCH(RTV, XLV)                                                                                  \
+  hipLaunchKernelGGL((gemv_mfma_kernel<RTV, PACKED, XLV>), grid, block, 0, s, X, W, mask, chunk, scale, rowptr, T, \
+                     d_in, d_out, g, go, Y)
+  if (rt == 4) {
+    if (xl) GM_MFMA_LAUNCH(4, true); else GM_MFMA_LAUNCH(4, false);
+  } else if (rt == 2) {
+    if (xl) GM_MFMA_LAUNCH(2, true); else GM_MFMA_LAUNCH(2, false);
+  } else {
+    if (xl) GM_MFMA_LAUNCH(1, true); else GM_MFMA_LAUNCH(1, false);
+  }
+#undef GM_MFMA_LAUNCH
   err = hipGetLastError();
   return true;
 }
