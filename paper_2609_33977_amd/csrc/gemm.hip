@@ -103,48 +103,62 @@ __global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __r
   const int m0 = tm * BM, n0 = tn * BN;
 
   // Prologue: kept bits of every mask row of the tile, the units some row keeps, soft values.
+  // The tile's RB mask rows are one contiguous run of RB * G_in selectors.
+  // Pass 1 reads it coalesced, eight independent loads per thread at a time
+  // (past the run or the layer's last mask row they read zeros), and stores
+  // the kept flags as a flat bitmap, one ballot per 64 selectors, into the
+  // first stage of the A tile, which the K-loop has not started to fill.
   if (tid < MAXU / 32) s_any[tid] = 0;
-  if constexpr (GO > 1)
-    for (int w = tid; w < RB * (MAXG / 32); w += 64 * NW) (&s_bits[0][0])[w] = 0u;
   if (tid == 0) {
     s_soft = 0;
     s_cols[0] = 0;  // read (unused) by the zero-fill copies when no unit is kept
   }
-  __syncthreads();
-  if constexpr (GO == 1) {
-    // one thread per row; a unit is one group
-    if (tid < BM) {
-      const int o = m0 + tid;
-      const int words = (G_in + 31) / 32;
-      bool soft = false;
-      for (int w = 0; w < words; ++w) {
-        uint32_t b = 0;
-        if (o < d_out)
-          for (int q = 0; q < 32 && w * 32 + q < G_in; ++q) {
-            const float m = mask[int64_t(o) * G_in + w * 32 + q];
-            b |= uint32_t(m != 0.0f) << q;
-            soft |= (m != 0.0f) && (m != 1.0f);
-          }
-        s_bits[tid][w] = b;
-        if (b) atomicOr(&s_any[w], b);
-      }
-      if (soft) s_soft = 1;
-    }
-  } else {
-    // the tile's RB mask rows are contiguous in the mask: read them coalesced
-    const int u0 = m0 / GO, G_out = d_out / GO;
+  uint32_t* flat = reinterpret_cast<uint32_t*>(&As[0][0]);
+  {
+    const int u0 = m0 / GO, rows = min(RB, d_out / GO - u0), n = RB * G_in;
+    const __amdgpu_buffer_rsrc_t rm = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(mask + int64_t(u0) * G_in), short(0), rows * G_in * 4, 0x00020000);
     bool soft = false;
-    for (int e = tid; e < RB * G_in; e += 64 * NW) {
-      const int rb = e / G_in, v = e - rb * G_in;
-      const float m = u0 + rb < G_out ? mask[int64_t(u0) * G_in + e] : 0.0f;
-      if (m != 0.0f) {
-        atomicOr(&s_bits[rb][v >> 5], 1u << (v & 31));
-        const int un = v / UG;
-        atomicOr(&s_any[un >> 5], 1u << (un & 31));
-        soft |= m != 1.0f;
+    for (int e0 = wave * 64; e0 < n; e0 += 8 * 64 * NW) {
+      float m[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int e = e0 + i * 64 * NW + lane;
+        m[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rm, e < n ? uint32_t(e) * 4u : kOOB, 0, 0));
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const uint64_t bal = __ballot(m[i] != 0.0f);
+        soft |= m[i] != 0.0f && m[i] != 1.0f;
+        const int e = e0 + i * 64 * NW;
+        if (lane < 2 && e < n) flat[e / 32 + lane] = uint32_t(bal >> (32 * lane));
       }
     }
+    __syncthreads();
     if (soft) s_soft = 1;
+  }
+  // Pass 2: word w of mask row r holds bits 32w .. 32w+31 of the row's G_in
+  // (bits past the run are never extracted: a word stops at its row's end).
+  {
+    const int words = (G_in + 31) / 32;
+    for (int e = tid; e < RB * words; e += 64 * NW) {
+      const int r = e % RB, w = e / RB;
+      const int p = r * G_in + 32 * w, nb = min(32, G_in - 32 * w);
+      const uint64_t two = (uint64_t(flat[p / 32 + 1]) << 32) | flat[p / 32];
+      const uint32_t b = uint32_t(two >> (p & 31)) & (nb == 32 ? ~0u : (1u << nb) - 1u);
+      s_bits[r][w] = b;
+      if constexpr (UG == 1) {
+        if (b) atomicOr(&s_any[w], b);
+      } else {
+        // 16-wide groups: unit u holds groups 2u and 2u + 1; pack the pairs' ORs
+        uint32_t u = (b | (b >> 1)) & 0x55555555u;
+        u = (u | (u >> 1)) & 0x33333333u;
+        u = (u | (u >> 2)) & 0x0f0f0f0fu;
+        u = (u | (u >> 4)) & 0x00ff00ffu;
+        u = (u | (u >> 8)) & 0x0000ffffu;
+        if (u) atomicOr(&s_any[w >> 1], u << (16 * (w & 1)));
+      }
+    }
   }
   __syncthreads();
   if (wave == 0) {
