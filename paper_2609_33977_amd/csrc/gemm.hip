@@ -257,15 +257,28 @@ __global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __r
     else
       dma16_group(j, rB, offB[j], ldsB + dst);
   };
-  // Soft selectors: scale this lane's freshly landed W chunks by their mask value.
+  // Soft selectors.  With every slice's copies, lane l of wave w also copies the
+  // mask value of tile row 32 w + (l & 31) for the slice's unit (with 16-wide
+  // groups: for the group of the slice's half l >> 5) into LDS; the wave's own
+  // rows are exactly those rows, so after its copies land each lane scales its
+  // W chunks by values its own wave brought in, with no extra wait.
+  static_assert(CA * 16 == 32, "a wave copies the W chunks of 32 tile rows");
+  __shared__ float s_msoft[STAGES][64 * NW];
+  const i32x4_t rM = make_rsrc(mask, uint32_t(d_out / GO) * uint32_t(G_in) * 4u);
+  const uint32_t ldsM = lds_addr(s_msoft) + uint32_t(wave) * 256u;
+  auto prepare_soft = [&](int st) {
+    const int r = 32 * wave + (lane & 31), h = lane >> 5;
+    const bool ok = st < nst && m0 + r < d_out && (UG == 2 || h == 0);
+    dma4_buf(rM, ok ? (uint32_t((m0 + r) / GO) * uint32_t(G_in) + uint32_t(v_cur * UG + h)) * 4u : kOOB,
+             ldsM + uint32_t(st % STAGES) * (64u * NW * 4u));
+    prepare(st);
+  };
   auto rescale = [&](int st) {
-    const int un = cols[st / SUB];
+    const float* ms = s_msoft[st % STAGES] + 64 * wave;
     u32x4* A = As[st % STAGES];
     float m[CA];
 #pragma unroll
-    for (int j = 0; j < CA; ++j)
-      m[j] = m0 + rowj[j] < d_out ? mask[int64_t((m0 + rowj[j]) / GO) * G_in + group_of(un, j)] : 0.0f;
-    wait_vmcnt<0>();
+    for (int j = 0; j < CA; ++j) m[j] = ms[16 * j + (lane >> 2) + 32 * gsub[j]];
 #pragma unroll
     for (int j = 0; j < CA; ++j) {
       u32x4* p = A + (wave * CA + j) * 64 + lane;
@@ -277,8 +290,9 @@ __global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __r
   // Hard masks (the common case) run a loop without the rescaling step.
   f32x4 acc[MB][NB];
   if (s_soft)
-    gemm_mainloop<MB, NB, true, true, 0, 0, PER_STAGE, STAGES, kFwdRowsAfter>(
-        As, Bs, nst, wm * 128, wn * NB * 16, lane, acc, prepare, issue, rescale, [](int, const u32x4(&)[NB]) {}, live);
+    gemm_mainloop<MB, NB, true, true, 0, 0, PER_STAGE, STAGES, kFwdRowsAfter, 1>(
+        As, Bs, nst, wm * 128, wn * NB * 16, lane, acc, prepare_soft, issue, rescale, [](int, const u32x4(&)[NB]) {},
+        live);
   else
     gemm_mainloop<MB, NB, true, true, 0, 0, PER_STAGE, STAGES, kFwdRowsAfter>(
         As, Bs, nst, wm * 128, wn * NB * 16, lane, acc, prepare, issue, [](int) {}, [](int, const u32x4(&)[NB]) {}, live);

@@ -89,6 +89,8 @@ struct AllRows {
 // (wave-uniform) has bit mb set when fragment row mb needs the MFMAs of slice
 // kt; rows whose A operand is all zeros for the slice skip them.  The first
 // slice runs every row, since its MFMAs also initialise the accumulators.
+// XTRA: further DMA instructions per slice that `prepare(st)` itself issues
+// (before the slice's copies); the wait counts include them.
 //
 // Software pipeline: rows 0 .. MB-RA-1 of slice kt run first (A fragments
 // streamed one row ahead), and the A fragments of the last RA rows are read;
@@ -106,14 +108,16 @@ struct AllRows {
 // (slices past the end copy zeros), so the wait count is a constant, and the
 // loop body has no branches around the accumulators; the first and the last
 // slice are peeled off.
-template <int MB, int NB, bool A_KM, bool B_KM, int CA, int CB, int PER_STAGE, int STAGES, int RA, int ABUF, int BBUF,
-          class Prepare, class Issue, class Landed, class BHook, class Live = AllRows>
+template <int MB, int NB, bool A_KM, bool B_KM, int CA, int CB, int PER_STAGE, int STAGES, int RA, int XTRA = 0,
+          int ABUF, int BBUF, class Prepare, class Issue, class Landed, class BHook, class Live = AllRows>
 __device__ __forceinline__ void gemm_mainloop(u32x4 (*As)[ABUF], u32x4 (*Bs)[BBUF], int nst, int a0, int b0, int lane,
                                               f32x4 (&acc)[MB][NB], Prepare&& prepare, Issue&& issue,
                                               Landed&& landed, BHook&& bhook, Live live = Live{}) {
   static_assert(PER_STAGE <= NB, "copies are interleaved with the NB MFMAs of one row");
   static_assert(RA >= 1 && RA <= MB, "rows after the barrier");
-  constexpr int AHEAD = PER_STAGE * (STAGES - 2);  // copies issued after the slice being waited for
+  // loads issued after the copies of the slice being waited for: the later
+  // slices' copies and the XTRA loads of every prepare() since
+  constexpr int AHEAD = (PER_STAGE + XTRA) * (STAGES - 2) + XTRA;
   if (nst <= 0) {
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)

@@ -95,6 +95,16 @@ __device__ __forceinline__ void dma16_group(int j, i32x4_t rsrc, uint32_t voffse
   }
 }
 
+// buffer_load_dword ... offen lds: 4 bytes at rsrc + voffset into LDS at
+// lds_wave_base + 4 lane (zeros when voffset is out of range).  It sets M0, so
+// it must not sit between the copies of a group (dma16_group<J > 0> reuse M0).
+__device__ __forceinline__ void dma4_buf(i32x4_t rsrc, uint32_t voffset, uint32_t lds_wave_base) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dword %0, %1, 0 offen lds"
+               :
+               : "v"(voffset), "s"(rsrc), "s"(lds_wave_base)
+               : "memory");
+}
+
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
