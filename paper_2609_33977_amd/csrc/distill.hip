@@ -371,14 +371,8 @@ __global__ __launch_bounds__(64 * kLmWaves) void lmhead_bwd_kernel(const uint16_
   f32x4 acc[MB][NB];
   gemm_mainloop<MB, NB, false, true, BM, 0, PER_STAGE, STAGES, kLmBwdRowsAfter>(
       As, Bs, nst, wm * 128, wn * NB * 16, lane, acc, prepare, issue, [](int) {}, [](int, const u32x4(&)[NB]) {});
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const int j = m0 + wm * 128 + mb * 16 + 4 * (lane >> 4);
-      const int t = n0 + wn * NB * 16 + nb * 16 + (lane & 15);
-      if (t < N && j < d) store4_bf16(dH + int64_t(t) * d + j, acc[mb][nb]);
-    }
+  store_tile_rows<BM, MB, NB, NW>(acc, reinterpret_cast<char*>(&As[0][0]), reinterpret_cast<char*>(&Bs[0][0]), wm, wn,
+                                  tid, lane, dH, d, n0, N, m0, d);
 }
 
 // ---------------------------------------------------------------- launchers

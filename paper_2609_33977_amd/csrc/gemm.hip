@@ -297,19 +297,19 @@ __global__ __launch_bounds__(64 * kFwdWaves) void fwd_kernel(const uint16_t* __r
     gemm_mainloop<MB, NB, true, true, 0, 0, PER_STAGE, STAGES, kFwdRowsAfter>(
         As, Bs, nst, wm * 128, wn * NB * 16, lane, acc, prepare, issue, [](int) {}, [](int, const u32x4(&)[NB]) {}, live);
 
+  if (part) {
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
+    for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const int o = m0 + wm * 128 + mb * 16 + 4 * (lane >> 4);
-      const int t = n0 + wn * NB * 16 + nb * 16 + (lane & 15);
-      if (t < T && o < d_out) {
-        if (part)
-          *reinterpret_cast<f32x4*>(part + (int64_t(share) * T + t) * d_out + o) = acc[mb][nb];
-        else
-          store4_bf16(Y + int64_t(t) * d_out + o, acc[mb][nb]);
+      for (int nb = 0; nb < NB; ++nb) {
+        const int o = m0 + wm * 128 + mb * 16 + 4 * (lane >> 4);
+        const int t = n0 + wn * NB * 16 + nb * 16 + (lane & 15);
+        if (t < T && o < d_out) *reinterpret_cast<f32x4*>(part + (int64_t(share) * T + t) * d_out + o) = acc[mb][nb];
       }
-    }
+    return;
+  }
+  store_tile_rows<BM, MB, NB, NW>(acc, reinterpret_cast<char*>(&As[0][0]), reinterpret_cast<char*>(&Bs[0][0]), wm, wn,
+                                  tid, lane, Y, d_out, n0, T, m0, d_out);
 }
 
 // Y = bf16(sum over shares s = 0 .. ksplit-1 of part[s]), eight outputs per thread.
@@ -668,14 +668,9 @@ __global__ __launch_bounds__(64 * dx_waves(BM)) void dx_kernel(const uint16_t* _
     gemm_mainloop<MB, NB, false, false, BM, BN, PER_STAGE, STAGES, kDxRowsAfter>(
         As, Bs, nst, wm * (BM / 2), wn * NB * 16, lane, acc, prepare, issue, [](int) {}, [](int, const u32x4(&)[NB]) {});
 
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const int i = m0 + wm * (BM / 2) + mb * 16 + 4 * (lane >> 4);
-      const int t = n0 + wn * NB * 16 + nb * 16 + (lane & 15);
-      if (t < T) store4_bf16(dX + int64_t(t) * d_in + i, acc[mb][nb]);
-    }
+  char* const hi = reinterpret_cast<char*>(&Bs[0][0]);
+  store_tile_rows<BM, MB, NB, NW>(acc, BM == 256 ? reinterpret_cast<char*>(&As[0][0]) : hi, hi, wm, wn, tid, lane, dX,
+                                  d_in, n0, T, m0, d_in);
 }
 
 // ============================================================================ dY^T
