@@ -204,14 +204,6 @@ __device__ __forceinline__ void gemm_mainloop(u32x4 (*As)[ABUF], u32x4 (*Bs)[BBU
   acc_drain<kAgprRows<MB> * NB>(reinterpret_cast<f32x4(&)[MB * NB]>(acc));
 }
 
-// Store 4 adjacent bf16 (rows m .. m+3 of the MFMA tile = consecutive output columns).
-__device__ __forceinline__ void store4_bf16(uint16_t* p, const f32x4& v) {
-  uint2 w;
-  w.x = pack_bf16x2(v[0], v[1]);
-  w.y = pack_bf16x2(v[2], v[3]);
-  *reinterpret_cast<uint2*>(p) = w;
-}
-
 // Epilogue of a K-loop tile of BM (m) x 256 (n) accumulators, waves 2 (m) x
 // NW/2 (n): out[r0 + n][c0 + m] = bf16(C[m][n]) for r0 + n < rlim (c0 + BM <=
 // clim or whole 8-column chunks below clim).  The bf16 tile goes through LDS

@@ -47,16 +47,11 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return __builtin_amdgcn_readfirstlane(uint32_t(reinterpret_cast<uintptr_t>((lds_void*)p)));
 }
 
-// buffer_load_dwordx4 ... offen lds: 16 bytes at rsrc + voffset into LDS at
-// lds_wave_base + 16 lane (zeros when voffset is out of the resource's range;
-// ranges stay below 2 GiB, so setting bit 31 of an offset marks it out of range).
-// lds_wave_base is an LDS byte address, uniform across the wave.
-__device__ __forceinline__ void dma16_buf(i32x4_t rsrc, uint32_t voffset, uint32_t lds_wave_base) {
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
-               :
-               : "v"(voffset), "s"(rsrc), "s"(lds_wave_base)
-               : "memory");
-}
+// buffer_load_dwordx4 (or _dword) ... offen lds copies 16 (or 4) bytes per
+// lane from rsrc + voffset into LDS at M0 + 16 lane (or 4 lane), zeros when
+// voffset is out of the resource's range (ranges stay below 2 GiB, so setting
+// bit 31 of an offset marks it out of range).  M0 holds an LDS byte address,
+// uniform across the wave.
 
 // Grouped copies: up to four copies J = 0..3 of a wave share one M0 value.
 // The instruction offset of buffer_load ... lds adds to both the memory
@@ -95,8 +90,7 @@ __device__ __forceinline__ void dma16_group(int j, i32x4_t rsrc, uint32_t voffse
   }
 }
 
-// buffer_load_dword ... offen lds: 4 bytes at rsrc + voffset into LDS at
-// lds_wave_base + 4 lane (zeros when voffset is out of range).  It sets M0, so
+// One 4-byte copy per lane into LDS at lds_wave_base + 4 lane.  It sets M0, so
 // it must not sit between the copies of a group (dma16_group<J > 0> reuse M0).
 __device__ __forceinline__ void dma4_buf(i32x4_t rsrc, uint32_t voffset, uint32_t lds_wave_base) {
   asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dword %0, %1, 0 offen lds"
