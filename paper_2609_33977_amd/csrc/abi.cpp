@@ -387,20 +387,23 @@ gm_status masked_linear_bwd_launch(const uint16_t* dY, const uint16_t* X, const 
     int* rows = reinterpret_cast<int*>(base + L.rows);
     float* scales = reinterpret_cast<float*>(base + L.scales);
     int* subbits = L.nsub > 1 ? reinterpret_cast<int*>(base + L.subbits) : nullptr;
-    if (gm_status st = from_hip(gm::launch_col_lists(mask, dout, G_in, g_out, L.nsub, colcount, colsoft, rows, scales,
-                                                     subbits, stream)))
-      return st;
-    // dY^T: a side output of the dgate GEMM, or a transpose pass without it.
+    // dY^T: a side output of the dgate GEMM, whose launch also builds the
+    // column lists; without dgate, a lists pass and a transpose pass.
     if (dgate) {
-      if (gm_status st = from_hip(gm::launch_dgate(dY, X, W, t, di, dout, g, g_out, dgate, dyt, L.ldt, stream)))
+      if (gm_status st = from_hip(gm::launch_dgate(dY, X, W, t, di, dout, g, g_out, dgate, dyt, L.ldt, mask, L.nsub,
+                                                   colcount, colsoft, rows, scales, subbits, stream)))
         return st;
     } else {
+      if (gm_status st = from_hip(gm::launch_col_lists(mask, dout, G_in, g_out, L.nsub, colcount, colsoft, rows,
+                                                       scales, subbits, stream)))
+        return st;
       if (gm_status st = from_hip(gm::launch_transpose(dY, t, dout, dyt, L.ldt, stream))) return st;
     }
     return from_hip(gm::launch_dx(dyt, L.ldt, W, colcount, rows, scales, subbits, colsoft, t, di, dout, g, dX,
                                   stream));
   }
-  return from_hip(gm::launch_dgate(dY, X, W, t, di, dout, g, g_out, dgate, nullptr, 0, stream));
+  return from_hip(gm::launch_dgate(dY, X, W, t, di, dout, g, g_out, dgate, nullptr, 0, nullptr, 1, nullptr, nullptr,
+                                   nullptr, nullptr, nullptr, stream));
 }
 
 // Shared argument checks of the two backward entry points (everything but the workspace).

@@ -32,6 +32,7 @@
 //         of W and of dY^T are gathered, MN-major tiles, transposing reads.
 #include "gm_gemm.h"
 #include "gm_launch.h"
+#include "gm_lists.h"
 
 namespace gm {
 
@@ -336,10 +337,23 @@ __global__ __launch_bounds__(256) void fwd_reduce_kernel(const float* __restrict
 // The epilogue forms dgate[o, v] = sum_{i in v} W[o, i] C[i, o].  For g = 512 a
 // group spans two tiles, each adding its half onto a zeroed dgate (two
 // addends onto zero: the same sum whichever lands first).
+//
+// Blocks past the tiles (when the dX GEMM follows) build the mask's column
+// lists, one col_lists_unit each: they start as the first tiles finish, on
+// CUs that would otherwise idle through the last tiles' tail (or a partial
+// last round of tiles), instead of in a launch of their own before dgate.
+struct ListArgs {
+  const float* mask;
+  int nunits, nchunks, nsub;
+  int *colcount, *colsoft, *rows, *subbits;
+  float* scales;
+};
+
 template <int G, int GO>
 __global__ __launch_bounds__(64 * kDgateWaves) void dgate_kernel(const uint16_t* __restrict__ dY, const uint16_t* __restrict__ X,
                                                     const uint16_t* __restrict__ W, int T, int d_in, int d_out,
-                                                    float* __restrict__ dgate, uint16_t* __restrict__ dYt, int ldt) {
+                                                    float* __restrict__ dgate, uint16_t* __restrict__ dYt, int ldt,
+                                                    ListArgs la) {
   constexpr int NW = kDgateWaves, WN = NW / 2;  // waves per block; wave grid 2 (i) x WN (o)
   constexpr int BM = 256, BN = 256, MB = 8, NB = BN / WN / 16;
   constexpr int PER_STAGE = 32 / NW;
@@ -352,9 +366,14 @@ __global__ __launch_bounds__(64 * kDgateWaves) void dgate_kernel(const uint16_t*
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
   const int G_in = d_in / G;
-  const int tiles_m = (d_in + BM - 1) / BM, tiles_n = (d_out + BN - 1) / BN;
+  const int tiles_m = (d_in + BM - 1) / BM, tiles_n = (d_out + BN - 1) / BN, tiles = tiles_m * tiles_n;
+  if (int(blockIdx.x) >= tiles) {
+    col_lists_unit<64 * NW>(int(blockIdx.x) - tiles, la.nchunks, la.mask, d_out, G_in, GO, la.nsub, la.colcount,
+                            la.colsoft, la.rows, la.scales, la.subbits);
+    return;
+  }
   int tm, tn;
-  tile_coords(gridDim.x, tiles_m, tiles_n, tm, tn);
+  tile_coords(int(blockIdx.x), tiles, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int nst = (T + kBK - 1) / kBK;
 
@@ -727,8 +746,11 @@ hipError_t launch_fwd(const uint16_t* X, const uint16_t* W, const float* mask, i
 }
 
 hipError_t launch_dgate(const uint16_t* dY, const uint16_t* X, const uint16_t* W, int T, int d_in, int d_out, int g,
-                        int go, float* dgate, uint16_t* dYt, int ldt, hipStream_t s) {
+                        int go, float* dgate, uint16_t* dYt, int ldt, const float* mask, int nsub, int* colcount,
+                        int* colsoft, int* rows, float* scales, int* subbits, hipStream_t s) {
   const int tiles = ((d_out + 255) / 256) * ((d_in + 255) / 256);
+  ListArgs la{mask, 0, (d_out + kListChunk - 1) / kListChunk, nsub, colcount, colsoft, rows, subbits, scales};
+  if (colcount) la.nunits = (d_in / g / nsub) * la.nchunks;
   if (g == 512) {
     const int64_t n = int64_t(d_out) * (d_in / g);
     const unsigned blocks = unsigned(n / 256 + 1 < 4096 ? n / 256 + 1 : 4096);
@@ -736,7 +758,7 @@ hipError_t launch_dgate(const uint16_t* dY, const uint16_t* X, const uint16_t* W
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  GM_LAUNCH_G(dgate_kernel, tiles, 64 * kDgateWaves, dY, X, W, T, d_in, d_out, dgate, dYt, ldt)
+  GM_LAUNCH_G(dgate_kernel, tiles + la.nunits, 64 * kDgateWaves, dY, X, W, T, d_in, d_out, dgate, dYt, ldt, la)
   return hipGetLastError();
 }
 

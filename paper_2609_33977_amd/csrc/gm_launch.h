@@ -35,8 +35,10 @@ int gemv_max_groups_per_row();
 // partial tiles into part [ksplit][T][d_out]; a second kernel adds them in order.
 hipError_t launch_fwd(const uint16_t* X, const uint16_t* W, const float* mask, int T, int d_in, int d_out, int g,
                       int go, uint16_t* Y, int ksplit, float* part, hipStream_t s);
+// With colcount set, the launch also builds the column lists (as launch_col_lists).
 hipError_t launch_dgate(const uint16_t* dY, const uint16_t* X, const uint16_t* W, int T, int d_in, int d_out, int g,
-                        int go, float* dgate, uint16_t* dYt, int ldt, hipStream_t s);
+                        int go, float* dgate, uint16_t* dYt, int ldt, const float* mask, int nsub, int* colcount,
+                        int* colsoft, int* rows, float* scales, int* subbits, hipStream_t s);
 hipError_t launch_transpose(const uint16_t* dY, int T, int d_out, uint16_t* dYt, int ldt, hipStream_t s);
 hipError_t launch_dx(const uint16_t* dYt, int ldt, const uint16_t* W, const int* colcount, const int* rows,
                      const float* scales, const int* subbits, const int* colsoft, int T, int d_in, int d_out, int g,

@@ -15,99 +15,20 @@
 // written by three passes (count per row, scan, copy).
 #include "gm_device.h"
 #include "gm_launch.h"
+#include "gm_lists.h"
 
 namespace gm {
 
 // One 1024-thread block per list column c and chunk of 1024 rows, so that the
-// chunks of a column run side by side.  The block of chunk k counts the kept
-// rows of chunks 0 .. k-1 itself (every thread loads its share of those
-// selectors and of its own row at once: one memory round trip), then places
-// its chunk's kept rows after them with a block-wide exclusive scan (a shuffle
-// scan inside each wave, then the 16 wave totals in LDS).  Rows stay in
-// increasing order; the block of the last chunk writes the column's count and
-// soft flag.  Against one block per column walking its chunks in turn: 7.8 ->
-// 6.6 us for 4096 rows, 19.4 -> 9.2 us for 11008 rows (LLaMA-2-7B shapes,
-// 16 list columns), identical lists.
-constexpr int kListChunk = 1024;
-
-__device__ __forceinline__ int block_sum_1024(int v, int* s_red) {
-#pragma unroll
-  for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d);
-  if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = v;
-  __syncthreads();
-  int t = 0;
-#pragma unroll
-  for (int q = 0; q < 16; ++q) t += s_red[q];
-  __syncthreads();
-  return t;
-}
-
+// chunks of a column run side by side (col_lists_unit).  Against one block
+// per column walking its chunks in turn: 7.8 -> 6.6 us for 4096 rows, 19.4 ->
+// 9.2 us for 11008 rows (LLaMA-2-7B shapes, 16 list columns), identical lists.
 __global__ __launch_bounds__(1024) void col_lists_kernel(const float* __restrict__ mask, int d_out, int G_in,
                                                         int go, int nsub, int nchunks, int* __restrict__ colcount,
                                                         int* __restrict__ colsoft, int* __restrict__ rows,
                                                         float* __restrict__ scales, int* __restrict__ subbits) {
-  const int c = blockIdx.x / nchunks, k = blockIdx.x % nchunks;
-  const int lane = threadIdx.x & 63;
-  const int w = threadIdx.x >> 6;
-  __shared__ int wave_tot[16];
-  __shared__ int s_red[16];
-  auto kept_bits = [&](int o, float (&m)[4]) {
-    int b = 0;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      m[q] = (q < nsub && o < d_out) ? mask[int64_t(o / go) * G_in + c * nsub + q] : 0.0f;
-      b |= int(m[q] != 0.0f) << q;
-    }
-    return b;
-  };
-  // this thread's row of the chunk, and its rows of the preceding chunks
-  const int o = k * kListChunk + int(threadIdx.x);
-  float m[4];
-  const int bits = kept_bits(o, m);
-  bool soft = false;
-  int before = 0;
-  for (int kk = 0; kk < k; ++kk) {
-    float mp[4];
-    const int bp = kept_bits(kk * kListChunk + int(threadIdx.x), mp);
-    before += bp != 0;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) soft |= mp[q] != 0.0f && mp[q] != 1.0f;
-  }
-#pragma unroll
-  for (int q = 0; q < 4; ++q) soft |= m[q] != 0.0f && m[q] != 1.0f;
-  const int base = block_sum_1024(before, s_red);
-  const int cnt = bits != 0;
-  int inc = cnt;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const int up = __shfl_up(inc, d);
-    if (lane >= d) inc += up;
-  }
-  if (lane == 63) wave_tot[w] = inc;
-  __syncthreads();
-  int off = base + inc - cnt;
-  int chunk_total = 0;
-#pragma unroll
-  for (int q = 0; q < 16; ++q) {
-    const int t = wave_tot[q];
-    if (q < w) off += t;
-    chunk_total += t;
-  }
-  if (bits) {
-    const int64_t e = int64_t(c) * d_out + off;
-    rows[e] = o;
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (q < nsub) scales[e * nsub + q] = m[q];
-    if (nsub > 1) subbits[e] = bits;
-  }
-  if (k == nchunks - 1) {
-    const int any_soft = block_sum_1024(int(soft), s_red);
-    if (threadIdx.x == 0) {
-      colcount[c] = base + chunk_total;
-      colsoft[c] = any_soft != 0;
-    }
-  }
+  col_lists_unit<1024>(int(blockIdx.x), nchunks, mask, d_out, G_in, go, nsub, colcount, colsoft, rows, scales,
+                       subbits);
 }
 
 hipError_t launch_col_lists(const float* mask, int d_out, int G_in, int go, int nsub, int* colcount, int* colsoft,
