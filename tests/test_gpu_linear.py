@@ -134,10 +134,14 @@ def test_all_ones_is_dense_and_all_zeros_is_exact_zero():
     del torch
 
 
-def test_dgate_does_not_depend_on_mask_and_single_outputs():
-    T, d_in, d_out, g = 192, 1024, 512, 128
-    case = workloads.make_linear_case((204,), T, d_in, d_out, g, None)
-    say("dgate mask independence, dgate-only and dX-only calls")
+@pytest.mark.parametrize("T,d_in,d_out,g", [(192, 1024, 512, 128), (64, 512, 3000, 256), (33, 1024, 2056, 64)])
+def test_dgate_does_not_depend_on_mask_and_single_outputs(T, d_in, d_out, g):
+    """dgate with or without dX and whatever the mask; dX alone (column lists
+    from their own launch, dY^T from the transpose) equal to dX beside dgate
+    (lists built by the dgate launch's spare blocks, dY^T its side output),
+    also with several 1024-row list chunks and a ragged last one."""
+    case = workloads.make_linear_case((204, d_out), T, d_in, d_out, g, None)
+    say(f"dgate mask independence, dgate-only and dX-only calls: T={T} d_in={d_in} d_out={d_out} g={g}")
     d1 = _dev_case(case)
     d2 = _dev_case(case, np.ones_like(case.mask))
     _, g1 = _bwd(d1, g)
